@@ -1,0 +1,139 @@
+"""The DLM forward Phi_theta in its two modes (oracle; test infrastructure only).
+
+Sec. 4.1 of the paper writes Phi_theta(g; C) for the generation forward that
+uses prompt cache C, and C_p(g) for the prompt K/V of every layer obtained
+when the response is g (App. A.1: C_p(g) stacks the prompt K/V states from
+every transformer layer).
+
+* Eager / full forward (Eq. archer-fresh, Eq. app-eager):
+  z*_t = Phi_theta(g_t; C_p(g_t)) -- all P+G positions are recomputed and the
+  prompt K/V of every layer is returned as the new cache
+  (FullForward of Algorithm 1).
+* Cached forward (Eq. archer-cached, Eq. app-cached):
+  zhat_t = Phi_theta(g_t; C_p(g_r)) -- only the G response positions are
+  recomputed; at every layer their queries attend, with no causal mask, to
+  [K_p(g_r) || K_g(g_t)] and [V_p(g_r) || V_g(g_t)] (Eq. archer-attention)
+  (CachedForward of Algorithm 1).
+
+The backbone itself is not specified by the paper beyond the model families
+it evaluates (LLaDA, Dream, DiffuCoder).  The reading used here: a pre-norm
+bidirectional transformer -- x <- E[tok]; per layer
+x += Attn(RMSNorm(x)) W_o^T and x += SwiGLU(RMSNorm(x)) W_down^T; final RMSNorm
+and an untied LM head; attention scale 1/sqrt(hd); no biases; grouped-query
+attention with query head h reading key/value head h // (Hq/Hkv); RoPE at
+absolute positions (prompt 0..P-1, response P..P+G-1).  The prompt K is
+cached after RoPE (positions never change, so this equals caching it before).
+
+bf16 models: the oracle rounds to bf16 where the bf16 path stores bf16
+operands -- the normalised activations entering each projection, the
+post-RoPE Q/K/V (hence the prompt cache), the attention output, the SwiGLU
+product and the final normalised hidden state.  The residual stream and the
+logits are not rounded.  fp32 models round nowhere.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from .numerics import attention, rms_norm, rope, round_bf16, silu, weights_f64
+
+
+def _rnd(m, x):
+    return round_bf16(x) if m.dtype == "bf16" else x
+
+
+def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
+                prefix_kv: list | None = None, out_rows: np.ndarray | None = None,
+                keep_hidden: bool = False):
+    """Run the bidirectional transformer on ``tokens`` at ``positions``.
+
+    ``prefix_kv`` -- optional per-layer ``(K, V)``, each ``[Hkv][n_prefix][hd]``,
+    prepended (in that order) to the keys/values computed from ``tokens`` at
+    every layer.  ``out_rows`` -- rows whose logits are returned (default all).
+
+    Returns ``(z, kv, hidden)``: logits ``[len(out_rows)][V]``; per-layer
+    ``(K, V)`` of the computed rows, each ``[Hkv][n][hd]`` (post-RoPE, rounded
+    like the cache); and, if ``keep_hidden``, the residual stream after the
+    embedding and after every layer (``[L+1][n][d]``) plus the final
+    normalised hidden state of ``out_rows``.
+    """
+    tokens = np.asarray(tokens)
+    positions = np.asarray(positions)
+    n = tokens.shape[0]
+    d, hq, hkv, hd = m.d_model, m.n_heads, m.n_kv_heads, m.head_dim
+    group = hq // hkv
+    if out_rows is None:
+        out_rows = np.arange(n)
+
+    x = weights_f64(W["tok_emb"][tokens])
+    hidden = [x.copy()] if keep_hidden else None
+    kv = []
+    for l in range(m.n_layers):
+        Wl = W["layers"][l]
+        # attention block
+        a = _rnd(m, rms_norm(x, Wl["attn_norm"], m.rms_eps))
+        qkv = a @ weights_f64(Wl["w_qkv"]).T
+        q = qkv[:, : hq * hd].reshape(n, hq, hd)
+        k = qkv[:, hq * hd: (hq + hkv) * hd].reshape(n, hkv, hd)
+        v = qkv[:, (hq + hkv) * hd:].reshape(n, hkv, hd)
+        q = _rnd(m, rope(q, positions, m.rope_theta))
+        k = _rnd(m, rope(k, positions, m.rope_theta))
+        v = _rnd(m, v)
+        k_rows = k.transpose(1, 0, 2)          # [Hkv][n][hd]
+        v_rows = v.transpose(1, 0, 2)
+        kv.append((k_rows, v_rows))
+        if prefix_kv is not None:
+            k_all = np.concatenate([prefix_kv[l][0], k_rows], axis=1)
+            v_all = np.concatenate([prefix_kv[l][1], v_rows], axis=1)
+        else:
+            k_all, v_all = k_rows, v_rows
+        o = np.empty((n, hq, hd))
+        for h in range(hq):
+            o[:, h, :] = attention(q[:, h, :], k_all[h // group], v_all[h // group])
+        o = _rnd(m, o.reshape(n, hq * hd))
+        x = x + o @ weights_f64(Wl["w_o"]).T
+        # SwiGLU MLP block
+        b = _rnd(m, rms_norm(x, Wl["mlp_norm"], m.rms_eps))
+        gate = b @ weights_f64(Wl["w_gate"]).T
+        up = b @ weights_f64(Wl["w_up"]).T
+        hmid = _rnd(m, silu(gate) * up)
+        x = x + hmid @ weights_f64(Wl["w_down"]).T
+        if keep_hidden:
+            hidden.append(x.copy())
+    c = _rnd(m, rms_norm(x[out_rows], W["final_norm"], m.rms_eps))
+    z = c @ weights_f64(W["lm_head"]).T
+    if keep_hidden:
+        return z, kv, (np.stack(hidden), c)
+    return z, kv, None
+
+
+def full_forward(W: dict, m, prompt: np.ndarray, g: np.ndarray, keep_hidden: bool = False):
+    """FullForward(p, g): exact logits z* = Phi_theta(g; C_p(g)) and the new cache.
+
+    Recomputes all N = P + G positions of [p; g] (Eq. archer-fresh).  Returns
+    ``(z [G][V], cache, hidden)`` where ``cache`` is C_p(g): per layer the
+    post-RoPE prompt K and the prompt V, each ``[Hkv][P][hd]``.
+    """
+    P, G = len(prompt), len(g)
+    tokens = np.concatenate([np.asarray(prompt), np.asarray(g)])
+    positions = np.arange(P + G)
+    z, kv, hidden = transformer(W, m, tokens, positions, None,
+                                out_rows=np.arange(P, P + G), keep_hidden=keep_hidden)
+    cache = [(k[:, :P, :].copy(), v[:, :P, :].copy()) for (k, v) in kv]
+    return z, cache, hidden
+
+
+def cached_forward(W: dict, m, g: np.ndarray, cache: list, prompt_len: int,
+                   keep_hidden: bool = False):
+    """CachedForward(g; C_r): zhat = Phi_theta(g; C_r) with C_r = C_p(g_r).
+
+    Only the G response rows are recomputed (at positions P..P+G-1); their
+    queries attend to the anchored prompt K/V followed by the fresh response
+    K/V at every layer (Eq. archer-attention).  No response tensor from an
+    earlier step is used (Prop. app-revisability).
+    """
+    G = len(g)
+    positions = np.arange(prompt_len, prompt_len + G)
+    z, _, hidden = transformer(W, m, np.asarray(g), positions, prefix_kv=cache,
+                               keep_hidden=keep_hidden)
+    return z, hidden

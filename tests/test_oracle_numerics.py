@@ -1,0 +1,125 @@
+"""Pins of the oracle's elementary operations against library routines,
+closed forms and brute force (no GPU)."""
+
+import math
+from itertools import product
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import numerics as on
+
+
+# --- bf16 rounding -----------------------------------------------------------
+
+def test_round_bf16_matches_torch_on_float32_inputs(rng):
+    x = (rng.standard_normal(200000) * np.exp(rng.uniform(-20, 20, 200000))).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(on.round_bf16(x.astype(np.float64)), ref)
+
+
+def test_round_bf16_ties_and_direct_rounding():
+    u = 2.0 ** -7                         # bf16 spacing in [1, 2)
+    cases = {
+        1.0 + u / 2: 1.0,                 # tie -> even (1.0)
+        1.0 + 3 * u / 2: 1.0 + 2 * u,     # tie -> even (1 + 2u)
+        -(1.0 + u / 2): -1.0,
+        1.0 + u / 2 + 2.0 ** -40: 1.0 + u,  # above the tie: a float32 detour would give 1.0
+        3.0: 3.0,
+        0.0: 0.0,
+    }
+    for x, want in cases.items():
+        assert on.round_bf16(np.array([x]))[0] == want, x
+
+
+# --- RMSNorm / SiLU against torch --------------------------------------------
+
+def test_rms_norm_matches_torch(rng):
+    x = rng.standard_normal((7, 33)) * 3
+    g = rng.standard_normal(33)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (33,), torch.from_numpy(g), eps=1e-5)
+    np.testing.assert_allclose(on.rms_norm(x, g, 1e-5), ref.numpy(), rtol=1e-13, atol=1e-13)
+
+
+def test_silu_matches_torch(rng):
+    x = rng.standard_normal(1000) * 6
+    ref = torch.nn.functional.silu(torch.from_numpy(x)).numpy()
+    np.testing.assert_allclose(on.silu(x), ref, rtol=1e-13, atol=1e-15)
+
+
+# --- RoPE ---------------------------------------------------------------------
+
+def test_rope_identity_at_position_zero(rng):
+    x = rng.standard_normal((1, 3, 8))
+    np.testing.assert_allclose(on.rope(x, np.array([0]), 10000.0), x, atol=0)
+
+
+def test_rope_matches_complex_rotation(rng):
+    """Rotate-half RoPE == multiplying (x_j + i x_{j+hd/2}) by exp(i pos theta^(-2j/hd))."""
+    hd, theta = 16, 500.0
+    x = rng.standard_normal((5, 2, hd))
+    pos = np.array([0, 1, 7, 100, 4097])
+    y = on.rope(x, pos, theta)
+    for r, p in enumerate(pos):
+        for h in range(2):
+            for j in range(hd // 2):
+                w = complex(x[r, h, j], x[r, h, j + hd // 2]) * complex(
+                    math.cos(p * theta ** (-2 * j / hd)), math.sin(p * theta ** (-2 * j / hd)))
+                assert abs(y[r, h, j] - w.real) < 1e-12
+                assert abs(y[r, h, j + hd // 2] - w.imag) < 1e-12
+
+
+def test_rope_scores_depend_on_relative_position_only(rng):
+    q = rng.standard_normal((1, 1, 8))
+    k = rng.standard_normal((1, 1, 8))
+    def score(m, n):
+        return float(np.sum(on.rope(q, np.array([m]), 10000.0) * on.rope(k, np.array([n]), 10000.0)))
+    for m, n, c in [(3, 1, 10), (0, 5, 77), (100, 100, 3)]:
+        assert abs(score(m, n) - score(m + c, n + c)) < 1e-12
+
+
+def test_rope_fixed_value():
+    # hd = 4: pairs (0, 2) rotate by pos * 1, pairs (1, 3) by pos * theta^-0.5
+    x = np.array([[[1.0, 0.0, 0.0, 2.0]]])
+    y = on.rope(x, np.array([2]), 100.0)[0, 0]
+    a, b = 2.0, 2.0 * 100.0 ** -0.5
+    want = [math.cos(a), -2.0 * math.sin(b), math.sin(a), 2.0 * math.cos(b)]
+    np.testing.assert_allclose(y, want, atol=1e-15)
+
+
+# --- attention ----------------------------------------------------------------
+
+def _attention_loops(q, k, v):
+    nq, hd = q.shape
+    out = np.zeros((nq, v.shape[1]))
+    for i in range(nq):
+        s = [sum(q[i, c] * k[j, c] for c in range(hd)) / math.sqrt(hd) for j in range(k.shape[0])]
+        mx = max(s)
+        w = [math.exp(t - mx) for t in s]
+        tot = sum(w)
+        for j in range(k.shape[0]):
+            for c in range(v.shape[1]):
+                out[i, c] += w[j] / tot * v[j, c]
+    return out
+
+
+def test_attention_matches_triple_loop(rng):
+    q, k, v = rng.standard_normal((5, 4)), rng.standard_normal((7, 4)), rng.standard_normal((7, 4))
+    np.testing.assert_allclose(on.attention(q, k, v), _attention_loops(q, k, v), atol=1e-13)
+
+
+def test_attention_matches_torch_sdpa_noncausal(rng):
+    q, k, v = (rng.standard_normal((2, 3, n, 16)) * 2 for n in (9, 13, 13))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v), is_causal=False).numpy()
+    for b, h in product(range(2), range(3)):
+        np.testing.assert_allclose(on.attention(q[b, h], k[b, h], v[b, h]), ref[b, h], atol=1e-12)
+
+
+def test_attention_closed_forms(rng):
+    q = rng.standard_normal((3, 8))
+    v = rng.standard_normal((5, 8))
+    same = np.tile(rng.standard_normal(8), (5, 1))    # identical keys -> uniform weights
+    np.testing.assert_allclose(on.attention(q, same, v), np.tile(v.mean(0), (3, 1)), atol=1e-14)
+    np.testing.assert_allclose(on.attention(q, same[:1], v[:1]), np.tile(v[0], (3, 1)), atol=0)
