@@ -1,0 +1,66 @@
+/*
+ * archer_ops.h -- single-kernel entry points and timing of the Archer library.
+ *
+ * These calls run one kernel of the decoding path exactly as the model path
+ * launches it (same kernels, same tile and split choices for the same
+ * shapes), on caller-provided device buffers.  They exist so that the
+ * kernels can be checked element by element at full model sizes and timed in
+ * isolation.  Conventions as in archer.h: device pointers, caller-owned
+ * memory, asynchronous on the given stream, host-side argument checks.
+ */
+#ifndef ARCHER_OPS_H
+#define ARCHER_OPS_H
+
+#include "archer.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Y = A W^T (a projection of Sec. 4's transformer layer; the alpha_l work of
+ * Eq. theory-cost).  A: [M][K], W: [N][K], both of element type dtype,
+ * row-major; Y: fp32 [M][N].  M >= 1; N and K multiples of 64. */
+archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
+                             const void *W, float *Y, void *hip_stream);
+
+/* Non-causal attention of one sequence over two key segments, the anchored
+ * attention of Eq. archer-attention: every query of head h attends to the nk1
+ * keys of segment 1 followed by the nk2 keys of segment 2 of key/value head
+ * h / (Hq / Hkv), scale 1 / sqrt(hd).
+ *   Q   [Hq][Mq][hd]                    O  [Mq][Hq hd] (element type dtype)
+ *   K1  [Hkv][ld1][hd]   Vt1 [Hkv][hd][ld1]   (segment 1, keys 0..nk1-1)
+ *   K2  [Hkv][ld2][hd]   Vt2 [Hkv][hd][ld2]   (segment 2, keys 0..nk2-1)
+ * V is stored transposed (Vt[h][d][key]).  ld1, ld2 multiples of 64,
+ * nk1 <= ld1, nk2 <= ld2, head_dim 64 or 128.
+ * workspace: device scratch of archer_op_attention_ws_bytes(...) bytes. */
+size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32_t hd, int32_t nk);
+archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd,
+                                  const void *Q, const void *K1, const void *Vt1, int32_t nk1,
+                                  int32_t ld1, const void *K2, const void *Vt2, int32_t nk2,
+                                  int32_t ld2, void *O, void *workspace, size_t ws_bytes,
+                                  void *hip_stream);
+
+/* Kernel classes for timing. */
+enum {
+  ARCHER_K_EMBED = 0, ARCHER_K_NORM = 1, ARCHER_K_GEMM_QKV = 2, ARCHER_K_ATTN = 3,
+  ARCHER_K_ATTN_MERGE = 4, ARCHER_K_GEMM_O = 5, ARCHER_K_GEMM_GATEUP = 6,
+  ARCHER_K_GEMM_DOWN = 7, ARCHER_K_GEMM_HEAD = 8, ARCHER_K_DECIDE = 9,
+  ARCHER_K_COUNT = 10
+};
+
+/* Start recording HIP events around every launch of the classes in
+ * class_mask (bit c = class c) made by this context; stops and clears any
+ * earlier recording. */
+archer_status archer_timing_begin(archer_ctx *ctx, uint32_t class_mask);
+
+/* Synchronise, stop recording and return, per class c < ARCHER_K_COUNT:
+ * launches[c], total_ms[c] (sum of event-bracketed launch durations) and the
+ * algorithmic bytes[c] and flops[c] of those launches (minimum HBM traffic:
+ * operands read once and results written once).  Any output may be NULL. */
+archer_status archer_timing_end(archer_ctx *ctx, int64_t *launches, double *total_ms,
+                                double *bytes, double *flops);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ARCHER_OPS_H */

@@ -35,7 +35,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .numerics import attention, rms_norm, rope, round_bf16, silu, weights_f64
+from .numerics import attention, linear, rms_norm, rope, round_bf16, silu, weights_f64
 
 
 def _rnd(m, x):
@@ -72,7 +72,7 @@ def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
         Wl = W["layers"][l]
         # attention block
         a = _rnd(m, rms_norm(x, Wl["attn_norm"], m.rms_eps))
-        qkv = a @ weights_f64(Wl["w_qkv"]).T
+        qkv = linear(a, Wl["w_qkv"])
         q = qkv[:, : hq * hd].reshape(n, hq, hd)
         k = qkv[:, hq * hd: (hq + hkv) * hd].reshape(n, hkv, hd)
         v = qkv[:, (hq + hkv) * hd:].reshape(n, hkv, hd)
@@ -91,17 +91,17 @@ def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
         for h in range(hq):
             o[:, h, :] = attention(q[:, h, :], k_all[h // group], v_all[h // group])
         o = _rnd(m, o.reshape(n, hq * hd))
-        x = x + o @ weights_f64(Wl["w_o"]).T
+        x = x + linear(o, Wl["w_o"])
         # SwiGLU MLP block
         b = _rnd(m, rms_norm(x, Wl["mlp_norm"], m.rms_eps))
-        gate = b @ weights_f64(Wl["w_gate"]).T
-        up = b @ weights_f64(Wl["w_up"]).T
+        gate = linear(b, Wl["w_gate"])
+        up = linear(b, Wl["w_up"])
         hmid = _rnd(m, silu(gate) * up)
-        x = x + hmid @ weights_f64(Wl["w_down"]).T
+        x = x + linear(hmid, Wl["w_down"])
         if keep_hidden:
             hidden.append(x.copy())
     c = _rnd(m, rms_norm(x[out_rows], W["final_norm"], m.rms_eps))
-    z = c @ weights_f64(W["lm_head"]).T
+    z = linear(c, W["lm_head"])
     if keep_hidden:
         return z, kv, (np.stack(hidden), c)
     return z, kv, None

@@ -68,6 +68,11 @@ def rope(x: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray:
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
+def linear(a: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """A projection of the transformer: a W^T with W stored row-major [out][in]."""
+    return np.asarray(a, dtype=np.float64) @ weights_f64(w).T
+
+
 def silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 

@@ -1,0 +1,286 @@
+"""Python binding of libarcher.so (ctypes).  Argument marshalling only.
+
+Every computation runs in the library's HIP kernels; this module turns torch
+CUDA tensors into device pointers and the C structs of include/archer.h and
+include/archer_ops.h.  torch provides device memory and the stream.  If the
+shared library has not been built the import fails loudly -- there is no
+fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "libarcher.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2608_08086_amd.build`")
+lib = C.CDLL(_LIB_PATH)
+
+OK, E_ARG, E_SHAPE, E_STATE, E_HIP, E_WORKSPACE, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+BF16, FP32 = 0, 1
+HAMMING, AGE, ALWAYS = 0, 1, 2
+NEVER = 2**31 - 1
+K_EMBED, K_NORM, K_GEMM_QKV, K_ATTN, K_ATTN_MERGE, K_GEMM_O, K_GEMM_GATEUP, K_GEMM_DOWN, K_GEMM_HEAD, K_DECIDE = range(10)
+K_COUNT = 10
+K_NAMES = ["embed", "norm", "gemm_qkv", "attn", "attn_merge", "gemm_o", "gemm_gateup", "gemm_down",
+           "gemm_head", "decide"]
+
+EXPORTED = [
+    "archer_workspace_bytes", "archer_init", "archer_refresh_prompt", "archer_step", "archer_decide",
+    "archer_decode", "archer_sync", "archer_destroy", "archer_last_error", "archer_op_gemm",
+    "archer_op_attention_ws_bytes", "archer_op_attention", "archer_timing_begin", "archer_timing_end",
+]
+
+
+class ModelCfg(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ff", C.c_int32),
+                ("vocab", C.c_int32), ("mask_id", C.c_int32), ("rms_eps", C.c_float),
+                ("rope_theta", C.c_float), ("dtype", C.c_int32)]
+
+
+class Weights(C.Structure):
+    _fields_ = [("tok_emb", C.c_void_p), ("lm_head", C.c_void_p), ("final_norm", C.c_void_p),
+                ("attn_norm", C.POINTER(C.c_void_p)), ("w_qkv", C.POINTER(C.c_void_p)),
+                ("w_o", C.POINTER(C.c_void_p)), ("mlp_norm", C.POINTER(C.c_void_p)),
+                ("w_gate", C.POINTER(C.c_void_p)), ("w_up", C.POINTER(C.c_void_p)),
+                ("w_down", C.POINTER(C.c_void_p))]
+
+
+class Limits(C.Structure):
+    _fields_ = [("max_batch", C.c_int32), ("max_prompt_len", C.c_int32),
+                ("max_prompt_total", C.c_int32), ("resp_len", C.c_int32)]
+
+
+class DecideCfg(C.Structure):
+    _fields_ = [("unmask_per_step", C.c_int32), ("remask_threshold", C.c_float),
+                ("max_remask", C.c_int32), ("final_step", C.c_int32)]
+
+
+class DecodeCfg(C.Structure):
+    _fields_ = [("policy", C.c_int32), ("K", C.c_int32), ("steps", C.c_int32),
+                ("unmask_per_step", C.c_int32), ("remask_threshold", C.c_float),
+                ("max_remask", C.c_int32)]
+
+
+class Trace(C.Structure):
+    _fields_ = [("refreshed", C.c_void_p), ("dist", C.c_void_p), ("age", C.c_void_p),
+                ("unmask_pos", C.c_void_p), ("unmask_tok", C.c_void_p), ("remask_pos", C.c_void_p)]
+
+
+P = C.c_void_p
+lib.archer_workspace_bytes.restype = C.c_size_t
+lib.archer_workspace_bytes.argtypes = [C.POINTER(ModelCfg), C.POINTER(Limits)]
+lib.archer_init.restype = C.c_int
+lib.archer_init.argtypes = [C.POINTER(ModelCfg), C.POINTER(Weights), C.POINTER(Limits), P, C.c_size_t, P,
+                            C.POINTER(P)]
+lib.archer_refresh_prompt.restype = C.c_int
+lib.archer_refresh_prompt.argtypes = [P, C.c_int32, P, C.POINTER(C.c_int32), P, P, P]
+lib.archer_step.restype = C.c_int
+lib.archer_step.argtypes = [P, P, P, P]
+lib.archer_decide.restype = C.c_int
+lib.archer_decide.argtypes = [P, P, P, P, C.POINTER(DecideCfg), P, P, P]
+lib.archer_decode.restype = C.c_int
+lib.archer_decode.argtypes = [P, C.c_int32, P, C.POINTER(C.c_int32), P, C.POINTER(DecodeCfg), C.POINTER(Trace)]
+lib.archer_sync.restype = C.c_int
+lib.archer_sync.argtypes = [P]
+lib.archer_destroy.restype = None
+lib.archer_destroy.argtypes = [P]
+lib.archer_last_error.restype = C.c_char_p
+lib.archer_last_error.argtypes = []
+lib.archer_op_gemm.restype = C.c_int
+lib.archer_op_gemm.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, P, P, P, P]
+lib.archer_op_attention_ws_bytes.restype = C.c_size_t
+lib.archer_op_attention_ws_bytes.argtypes = [C.c_int32] * 5
+lib.archer_op_attention.restype = C.c_int
+lib.archer_op_attention.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P, P, P, C.c_int32,
+                                    C.c_int32, P, P, C.c_int32, C.c_int32, P, P, C.c_size_t, P]
+lib.archer_timing_begin.restype = C.c_int
+lib.archer_timing_begin.argtypes = [P, C.c_uint32]
+lib.archer_timing_end.restype = C.c_int
+lib.archer_timing_end.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_double), C.POINTER(C.c_double),
+                                  C.POINTER(C.c_double)]
+
+
+class ArcherError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"archer status {status}: {msg}")
+        self.status = status
+
+
+def _check(status: int):
+    if status != OK:
+        raise ArcherError(status, lib.archer_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    assert t.is_cuda and t.is_contiguous(), "device tensors must be contiguous CUDA tensors"
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def torch_dtype(dtype: int):
+    return torch.bfloat16 if dtype == BF16 else torch.float32
+
+
+class Context:
+    """One archer_ctx: a model's weights (device tensors), limits and workspace."""
+
+    def __init__(self, shape, weights: dict, max_batch: int, max_prompt_len: int, max_prompt_total: int,
+                 resp_len: int):
+        self.shape = shape
+        self.dtype = BF16 if shape.dtype == "bf16" else FP32
+        self.cfg = ModelCfg(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
+                            shape.d_ff, shape.vocab, shape.mask_id, shape.rms_eps, shape.rope_theta, self.dtype)
+        self.lim = Limits(max_batch, max_prompt_len, max_prompt_total, resp_len)
+        self.G = resp_len
+        self.V = shape.vocab
+        self.weights = weights  # keep device tensors alive
+        L = shape.n_layers
+
+        def arr(key):
+            a = (C.c_void_p * L)(*[w[key].data_ptr() for w in weights["layers"]])
+            return C.cast(a, C.POINTER(C.c_void_p)), a
+
+        self._keep = []
+        fields = {}
+        for key in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate", "w_up", "w_down"):
+            p, a = arr(key)
+            self._keep.append(a)
+            fields[key] = p
+        self.cw = Weights(weights["tok_emb"].data_ptr(), weights["lm_head"].data_ptr(),
+                          weights["final_norm"].data_ptr(), **fields)
+        nbytes = lib.archer_workspace_bytes(C.byref(self.cfg), C.byref(self.lim))
+        if nbytes == 0:
+            raise ArcherError(E_ARG, lib.archer_last_error().decode())
+        self.ws_bytes = nbytes
+        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device="cuda")
+        off = (-self.workspace.data_ptr()) % 256
+        self._ws_ptr = self.workspace.data_ptr() + off
+        h = C.c_void_p()
+        _check(lib.archer_init(C.byref(self.cfg), C.byref(self.cw), C.byref(self.lim), C.c_void_p(self._ws_ptr),
+                               nbytes, _stream(), C.byref(h)))
+        self.h = h
+
+    def close(self):
+        if getattr(self, "h", None):
+            lib.archer_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- calls of archer.h -------------------------------------------------------------------
+    def new_logits(self, batch):
+        return torch.empty(batch, self.G, self.V, dtype=torch.float32, device="cuda")
+
+    def refresh_prompt(self, prompt, prompt_len, response, seq_sel=None, logits=None):
+        B = len(prompt_len)
+        logits = self.new_logits(B) if logits is None else logits
+        pl = (C.c_int32 * B)(*prompt_len)
+        sel = None if seq_sel is None else (C.c_uint8 * B)(*[1 if s else 0 for s in seq_sel])
+        _check(lib.archer_refresh_prompt(self.h, B, _ptr(prompt), pl, _ptr(response), sel, _ptr(logits)))
+        return logits
+
+    def step(self, response, seq_sel=None, logits=None):
+        B = response.shape[0]
+        logits = self.new_logits(B) if logits is None else logits
+        sel = None if seq_sel is None else (C.c_uint8 * B)(*[1 if s else 0 for s in seq_sel])
+        _check(lib.archer_step(self.h, _ptr(response), sel, _ptr(logits)))
+        return logits
+
+    def decide(self, logits, g_in, k=1, tau=0.1, max_remask=1, final=False):
+        B = g_in.shape[0]
+        g_out = torch.empty_like(g_in)
+        dist = torch.empty(B, dtype=torch.int32, device="cuda")
+        um = torch.empty(B, k, dtype=torch.int32, device="cuda")
+        rm = torch.empty(B, dtype=torch.int32, device="cuda")
+        dc = DecideCfg(k, tau, max_remask, 1 if final else 0)
+        _check(lib.archer_decide(self.h, _ptr(logits), _ptr(g_in), _ptr(g_out), C.byref(dc), _ptr(dist),
+                                 _ptr(um), _ptr(rm)))
+        return g_out, dist, um, rm
+
+    def decode(self, prompt, prompt_len, response, *, policy, K, steps, k=1, tau=0.1, max_remask=1,
+               trace=True):
+        B = len(prompt_len)
+        pl = (C.c_int32 * B)(*prompt_len)
+        dc = DecodeCfg(policy, int(min(K, NEVER)), steps, k, tau, max_remask)
+        tr = None
+        tens = None
+        if trace:
+            dev = dict(device="cuda", dtype=torch.int32)
+            tens = dict(refreshed=torch.zeros(steps, B, **dev), dist=torch.zeros(steps, B, **dev),
+                        age=torch.zeros(steps, B, **dev), unmask_pos=torch.full((steps, B, k), -1, **dev),
+                        unmask_tok=torch.full((steps, B, k), -1, **dev),
+                        remask_pos=torch.full((steps, B), -1, **dev))
+            tr = Trace(*[t.data_ptr() for t in tens.values()])
+        _check(lib.archer_decode(self.h, B, _ptr(prompt), pl, _ptr(response), C.byref(dc),
+                                 C.byref(tr) if tr is not None else None))
+        return response, tens
+
+    def sync(self):
+        _check(lib.archer_sync(self.h))
+
+    # -- timing of archer_ops.h ---------------------------------------------------------------
+    def timing_begin(self, classes):
+        mask = 0
+        for c in classes:
+            mask |= 1 << c
+        _check(lib.archer_timing_begin(self.h, mask))
+
+    def timing_end(self):
+        n = (C.c_int64 * K_COUNT)()
+        ms = (C.c_double * K_COUNT)()
+        by = (C.c_double * K_COUNT)()
+        fl = (C.c_double * K_COUNT)()
+        _check(lib.archer_timing_end(self.h, n, ms, by, fl))
+        return {K_NAMES[i]: dict(launches=n[i], ms=ms[i], bytes=by[i], flops=fl[i]) for i in range(K_COUNT)}
+
+
+def upload_weights(W: dict, dtype: str) -> dict:
+    """Host weights (synth layout: uint16 bf16 bits or float32) -> contiguous CUDA tensors."""
+    def dev(a):
+        if a.dtype.name == "uint16":
+            t = torch.from_numpy(a.view("int16")).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(a)
+        return t.to("cuda").contiguous()
+
+    out = {k: dev(W[k]) for k in ("tok_emb", "lm_head", "final_norm")}
+    out["layers"] = [{k: dev(v) for k, v in L.items()} for L in W["layers"]]
+    return out
+
+
+# -- single-kernel hooks of archer_ops.h --------------------------------------------------------
+def op_gemm(A, Wt, dtype=BF16):
+    M, K = A.shape
+    N = Wt.shape[0]
+    Y = torch.empty(M, N, dtype=torch.float32, device="cuda")
+    _check(lib.archer_op_gemm(dtype, M, N, K, _ptr(A), _ptr(Wt), _ptr(Y), _stream()))
+    return Y
+
+
+def op_attention(Q, K1, Vt1, nk1, K2, Vt2, nk2, dtype=BF16):
+    """Q [Hq][Mq][hd]; K1 [Hkv][ld1][hd], Vt1 [Hkv][hd][ld1]; same for segment 2.  Returns O [Mq][Hq*hd]."""
+    Hq, Mq, hd = Q.shape
+    Hkv, ld1, _ = K1.shape
+    ld2 = K2.shape[1]
+    O = torch.empty(Mq, Hq * hd, dtype=Q.dtype, device="cuda")
+    nbytes = lib.archer_op_attention_ws_bytes(dtype, Mq, Hq, hd, ((nk1 + 63) // 64) * 64 + nk2)
+    ws = torch.empty(max(nbytes, 1) + 256, dtype=torch.uint8, device="cuda")
+    wp = ws.data_ptr() + ((-ws.data_ptr()) % 256)
+    _check(lib.archer_op_attention(dtype, Mq, Hq, Hkv, hd, _ptr(Q), _ptr(K1), _ptr(Vt1), nk1, ld1, _ptr(K2),
+                                   _ptr(Vt2), nk2, ld2, _ptr(O), C.c_void_p(wp), nbytes, _stream()))
+    return O

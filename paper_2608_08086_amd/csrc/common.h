@@ -1,0 +1,80 @@
+// Shared device types and helpers of the Archer HIP library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define ARCHER_MAXB 64
+
+// Per-pass description of the rows a forward recomputes, passed to kernels
+// by value.  A full pass (FullForward) recomputes, for each selected
+// sequence, its prompt rows followed by its G response rows; a cached pass
+// (CachedForward) recomputes only the G response rows.  Key index space of
+// sequence s, shared by both passes: [0, ppad) are the cached prompt keys
+// (valid below p_len), [ppad, ppad + G) the fresh response keys, with
+// ppad = p_len rounded up to 64 so that every 64-key tile lies in one segment.
+struct SeqPlan {
+  int n;                          // sequences in this pass
+  int full;                       // 1 = rows are [prompt; response], 0 = response only
+  int G;                          // response length
+  int rows;                       // total rows of the pass
+  int seq[ARCHER_MAXB];           // batch index b of pass sequence s
+  int row_off[ARCHER_MAXB + 1];   // first pass row of sequence s (row_off[n] = rows)
+  int p_len[ARCHER_MAXB];         // prompt length P_b
+  int cache_off[ARCHER_MAXB];     // 64-aligned offset of b's prompt keys in a cache head plane
+  int tok_off[ARCHER_MAXB];       // offset of b's prompt tokens in the packed prompt array
+  int qt_off[ARCHER_MAXB + 1];    // prefix sum of attention query tiles per sequence
+  int nsplit[ARCHER_MAXB];        // split-KV count of sequence s (a function of its key count only)
+  int max_split;                  // max over s of nsplit
+};
+
+__device__ __forceinline__ int plan_find(const int* off, int n, int v) {
+  // largest s in [0, n) with off[s] <= v (off ascending, off[0] = 0)
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= v) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+
+template <class T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Block-wide sum for blockDim.x a multiple of 64 (<= 1024).  Uses 16 floats of LDS.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+// dst-row encoding of the K/V destination of a pass row: >= 0 is a row of the
+// fresh (response) K/V buffers, < 0 encodes prompt-cache row (-1 - v).
+__device__ __forceinline__ bool dst_is_fresh(int v) { return v >= 0; }
+__device__ __forceinline__ int dst_cache_row(int v) { return -1 - v; }

@@ -1,0 +1,689 @@
+// Host engine of the Archer library: the C ABI of archer.h / archer_ops.h.
+//
+// A context holds the model description, the weight pointers, the carved-up
+// caller workspace (prompt K/V cache of every layer, activations, logits and
+// decision scratch) and the per-batch session state (prompt lengths, cache
+// offsets, which sequences have a cache).  Each forward builds a SeqPlan on
+// the host (passed to kernels by value) and enqueues, per layer:
+//   RMSNorm -> QKV GEMM (+RoPE, K/V to cache or fresh buffers) -> attention
+//   [-> split-KV merge] -> O GEMM (+residual) -> RMSNorm -> gate/up GEMM
+//   (+SwiGLU) -> down GEMM (+residual),
+// then the final RMSNorm of the response rows and the LM head.
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "archer.h"
+#include "archer_ops.h"
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+archer_status fail(archer_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define HIPCHK(x)                                                                           \
+  do {                                                                                      \
+    hipError_t e_ = (x);                                                                    \
+    if (e_ != hipSuccess) return fail(ARCHER_E_HIP, std::string(#x) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Layout {
+  size_t rope, Kc, Vtc, Kf, Vtf, x, act, Q, O, H, Cn, logits, Opart, ML;
+  size_t row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
+  int ldcache, ldfresh, Mmax, Rmax, max_pos, ldq;
+  size_t cache_layer_elems;
+};
+
+constexpr int kMaxSplit = 8;
+
+std::string check_cfg(const archer_model_cfg* c, const archer_limits* l) {
+  if (!c || !l) return "null cfg or limits";
+  if (c->n_layers < 1 || c->d_model < 64 || c->n_heads < 1 || c->n_kv_heads < 1 || c->d_ff < 64 || c->vocab < 64)
+    return "model dimensions must be positive (d_model, d_ff, vocab >= 64)";
+  if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
+  if (c->n_heads % c->n_kv_heads) return "n_heads must be a multiple of n_kv_heads";
+  if (c->d_model % 64 || c->d_ff % 64 || c->vocab % 64) return "d_model, d_ff and vocab must be multiples of 64";
+  if (c->mask_id < 0 || c->mask_id >= c->vocab) return "mask_id outside the vocabulary";
+  if (c->dtype != ARCHER_BF16 && c->dtype != ARCHER_FP32) return "dtype must be ARCHER_BF16 or ARCHER_FP32";
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f)) return "rms_eps must be > 0 and rope_theta > 1";
+  if (l->max_batch < 1 || l->max_batch > ARCHER_MAXB) return "max_batch must be in [1, 64]";
+  if (l->max_prompt_len < 1 || l->max_prompt_total < l->max_prompt_len) return "bad prompt limits";
+  if (l->resp_len < 8 || l->resp_len % 8 || l->resp_len > 4096) return "resp_len must be a multiple of 8 in [8, 4096]";
+  if (c->dtype == ARCHER_FP32 && (size_t)c->head_dim + align_up(l->max_prompt_len, 64) + l->resp_len > 16000)
+    return "fp32 path supports at most ~16k keys per sequence";
+  return "";
+}
+
+Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
+  Layout L{};
+  const size_t esz = c->dtype == ARCHER_BF16 ? 2 : 4;
+  const int d = c->d_model, hq = c->n_heads, hkv = c->n_kv_heads, hd = c->head_dim;
+  L.Rmax = l->max_batch * l->resp_len;
+  L.ldcache = (int)align_up((size_t)l->max_prompt_total + 64 * (size_t)l->max_batch, 64);
+  L.ldfresh = (int)align_up((size_t)L.Rmax, 64);
+  L.Mmax = l->max_prompt_total + L.Rmax;
+  L.ldq = L.Mmax;
+  L.max_pos = l->max_prompt_len + l->resp_len;
+  L.cache_layer_elems = (size_t)hkv * L.ldcache * hd;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  L.rope = take((size_t)L.max_pos * (hd / 2) * sizeof(float2));
+  L.Kc = take((size_t)c->n_layers * L.cache_layer_elems * esz);
+  L.Vtc = take((size_t)c->n_layers * L.cache_layer_elems * esz);
+  L.Kf = take((size_t)hkv * L.ldfresh * hd * esz);
+  L.Vtf = take((size_t)hkv * L.ldfresh * hd * esz);
+  L.x = take((size_t)L.Mmax * d * 4);
+  L.act = take((size_t)L.Mmax * d * esz);
+  L.Q = take((size_t)hq * L.ldq * hd * esz);
+  L.O = take((size_t)L.Mmax * hq * hd * esz);
+  L.H = take((size_t)L.Mmax * c->d_ff * esz);
+  L.Cn = take((size_t)L.Rmax * d * esz);
+  L.logits = take((size_t)L.Rmax * c->vocab * 4);
+  const size_t part_rows = c->dtype == ARCHER_BF16 ? (size_t)L.Mmax : 1;
+  L.Opart = take((size_t)kMaxSplit * hq * part_rows * hd * 4);
+  L.ML = take((size_t)kMaxSplit * hq * part_rows * 2 * 4);
+  L.row_pos = take((size_t)L.Mmax * 4);
+  L.row_dst = take((size_t)L.Mmax * 4);
+  L.out_row = take((size_t)L.Rmax * 4);
+  L.g_anchor = take((size_t)L.Rmax * 4);
+  L.gbuf0 = take((size_t)L.Rmax * 4);
+  L.gbuf1 = take((size_t)L.Rmax * 4);
+  L.dist = take((size_t)ARCHER_MAXB * 4);
+  L.xhat = take((size_t)L.Rmax * 4);
+  L.ell = take((size_t)L.Rmax * 4);
+  L.qv = take((size_t)L.Rmax * 4);
+  L.err = take(256);
+  L.total = off;
+  return L;
+}
+
+struct TimerRec {
+  hipEvent_t a, b;
+  int cls;
+  double bytes, flops;
+};
+
+}  // namespace
+
+struct archer_ctx {
+  archer_model_cfg cfg;
+  archer_limits lim;
+  Layout L;
+  hipStream_t stream;
+  char* ws;
+  size_t esz;
+  // weights
+  const void* tok_emb;
+  const void* lm_head;
+  const float* final_norm;
+  std::vector<const float*> attn_norm, mlp_norm;
+  std::vector<const void*> w_qkv, w_o, w_gate, w_up, w_down;
+  // session
+  int batch = 0;
+  int plen[ARCHER_MAXB];
+  int cache_off[ARCHER_MAXB];
+  int tok_off[ARCHER_MAXB];
+  bool has_cache[ARCHER_MAXB];
+  // timing
+  bool t_on = false;
+  uint32_t t_mask = 0;
+  std::vector<TimerRec> t_recs;
+  size_t t_used = 0;
+
+  template <class P> P* at(size_t off) { return (P*)(ws + off); }
+};
+
+namespace {
+
+bool is_bf16(const archer_ctx* c) { return c->cfg.dtype == ARCHER_BF16; }
+
+template <class F>
+archer_status timed(archer_ctx* c, int cls, double bytes, double flops, F&& launch) {
+  const bool rec = c->t_on && ((c->t_mask >> cls) & 1u);
+  if (rec) {
+    if (c->t_used == c->t_recs.size()) {
+      TimerRec r{};
+      HIPCHK(hipEventCreate(&r.a));
+      HIPCHK(hipEventCreate(&r.b));
+      c->t_recs.push_back(r);
+    }
+    HIPCHK(hipEventRecord(c->t_recs[c->t_used].a, c->stream));
+  }
+  const int rc = launch();
+  if (rc) return fail(ARCHER_E_UNSUPPORTED, "kernel launch rejected the shape");
+  if (rec) {
+    TimerRec& r = c->t_recs[c->t_used++];
+    HIPCHK(hipEventRecord(r.b, c->stream));
+    r.cls = cls;
+    r.bytes = bytes;
+    r.flops = flops;
+  }
+  return ARCHER_OK;
+}
+
+int attn_qt(const archer_ctx* c) { return is_bf16(c) ? ATTN_QT_BF16 : ATTN_QT_F32; }
+
+SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) {
+  SeqPlan p;
+  memset(&p, 0, sizeof(p));
+  p.n = (int)sel.size();
+  p.full = full ? 1 : 0;
+  p.G = c->lim.resp_len;
+  const int qt = attn_qt(c);
+  int rows = 0, tiles = 0;
+  for (int s = 0; s < p.n; ++s) {
+    const int b = sel[s];
+    p.seq[s] = b;
+    p.p_len[s] = c->plen[b];
+    p.cache_off[s] = c->cache_off[b];
+    p.tok_off[s] = c->tok_off[b];
+    p.row_off[s] = rows;
+    p.qt_off[s] = tiles;
+    const int nr = full ? c->plen[b] + p.G : p.G;
+    rows += nr;
+    tiles += (nr + qt - 1) / qt;
+    p.nsplit[s] = is_bf16(c) ? attn_nsplit_for_keys(((c->plen[b] + 63) & ~63) + p.G) : 1;
+    p.max_split = std::max(p.max_split, p.nsplit[s]);
+  }
+  p.row_off[p.n] = rows;
+  p.qt_off[p.n] = tiles;
+  p.rows = rows;
+  return p;
+}
+
+archer_status gemm(archer_ctx* c, int cls, int epi, const GemmArgs& a) {
+  const double es = (double)c->esz;
+  double bytes = (double)a.M * a.K * es + (double)a.N * a.K * es;
+  if (epi == EPI_STORE) bytes += (double)a.M * a.N * 4;
+  else if (epi == EPI_RESID) bytes += 2.0 * a.M * a.N * 4;
+  else if (epi == EPI_SWIGLU) bytes += (double)a.M * (a.N / 2) * es;
+  else bytes += (double)a.M * a.N * es;
+  const double flops = 2.0 * a.M * a.N * a.K;
+  return timed(c, cls, bytes, flops, [&] {
+    return is_bf16(c) ? launch_gemm_bf16(epi, a, c->stream) : launch_gemm_f32(epi, a, c->stream);
+  });
+}
+
+GemmArgs gargs(const void* A, int lda, const void* W, int ldw, int M, int N, int K) {
+  GemmArgs a;
+  memset(&a, 0, sizeof(a));
+  a.A = A; a.lda = lda; a.W = W; a.ldw = ldw; a.M = M; a.N = N; a.K = K;
+  return a;
+}
+
+// One forward over the selected sequences (full = FullForward, else CachedForward).
+archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel, const int32_t* prompt,
+                          const int32_t* resp, float* logits) {
+  if (sel.empty()) return ARCHER_OK;
+  const archer_model_cfg& m = c->cfg;
+  const Layout& L = c->L;
+  const SeqPlan pl = build_plan(c, full, sel);
+  const int rows = pl.rows, d = m.d_model, hq = m.n_heads, hkv = m.n_kv_heads, hd = m.head_dim, F = m.d_ff;
+  const int qkv_n = (hq + 2 * hkv) * hd;
+  const size_t es = c->esz;
+  float* x = c->at<float>(L.x);
+  void* act = c->at<char>(L.act);
+  int* row_pos = c->at<int>(L.row_pos);
+  int* row_dst = c->at<int>(L.row_dst);
+  archer_status st;
+
+  st = timed(c, ARCHER_K_EMBED, (double)rows * d * (es + 4), 0.0, [&] {
+    if (is_bf16(c))
+      launch_embed<bf16>(pl, c->tok_emb, d, m.vocab, m.mask_id, prompt, resp, x, row_pos, row_dst,
+                         c->at<int>(L.g_anchor), c->at<int>(L.err), c->stream);
+    else
+      launch_embed<float>(pl, c->tok_emb, d, m.vocab, m.mask_id, prompt, resp, x, row_pos, row_dst,
+                          c->at<int>(L.g_anchor), c->at<int>(L.err), c->stream);
+    return 0;
+  });
+  if (st) return st;
+
+  auto norm = [&](const float* gain, int gather, int nrows, void* out) {
+    return timed(c, ARCHER_K_NORM, (double)nrows * d * (4 + es), 0.0, [&] {
+      if (is_bf16(c)) launch_rmsnorm<bf16>(pl, gather, nrows, x, gain, out, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
+      else launch_rmsnorm<float>(pl, gather, nrows, x, gain, out, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
+      return 0;
+    });
+  };
+
+  double kv_keys = 0;
+  for (int s = 0; s < pl.n; ++s) kv_keys += pl.p_len[s] + pl.G;
+  double attn_q_keys = 0;
+  for (int s = 0; s < pl.n; ++s)
+    attn_q_keys += (double)(pl.row_off[s + 1] - pl.row_off[s]) * (pl.p_len[s] + pl.G);
+
+  for (int l = 0; l < m.n_layers; ++l) {
+    if ((st = norm(c->attn_norm[l], 0, rows, act))) return st;
+    {
+      GemmArgs a = gargs(act, d, c->w_qkv[l], d, rows, qkv_n, d);
+      a.Qb = c->at<char>(L.Q); a.ldq = L.ldq;
+      a.Kc = c->at<char>(L.Kc) + (size_t)l * L.cache_layer_elems * es;
+      a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
+      a.ldcache = L.ldcache;
+      a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
+      a.hq = hq; a.hkv = hkv; a.hd = hd;
+      a.row_pos = row_pos; a.row_dst = row_dst; a.rope = c->at<float2>(L.rope);
+      if ((st = gemm(c, ARCHER_K_GEMM_QKV, EPI_QKV, a))) return st;
+    }
+    {
+      AttnArgs a;
+      memset(&a, 0, sizeof(a));
+      a.Q = c->at<char>(L.Q); a.ldq = L.ldq;
+      a.Kc = c->at<char>(L.Kc) + (size_t)l * L.cache_layer_elems * es;
+      a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
+      a.ldcache = L.ldcache;
+      a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
+      a.O = c->at<char>(L.O); a.ldo = hq * hd;
+      a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML);
+      a.hq = hq; a.hkv = hkv; a.hd = hd;
+      a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+      const double bytes = (double)rows * hq * hd * es * 2 + kv_keys * hkv * hd * es * 2;
+      const double flops = 4.0 * attn_q_keys * hq * hd;
+      int max_keys = 0;
+      for (int s = 0; s < pl.n; ++s) max_keys = std::max(max_keys, ((pl.p_len[s] + 63) & ~63) + pl.G);
+      st = timed(c, ARCHER_K_ATTN, bytes, flops, [&] {
+        return is_bf16(c) ? launch_attn_bf16(pl, a, c->stream) : launch_attn_f32(pl, a, max_keys, c->stream);
+      });
+      if (st) return st;
+      if (pl.max_split > 1) {
+        double mbytes = 0;
+        for (int s = 0; s < pl.n; ++s)
+          if (pl.nsplit[s] > 1)
+            mbytes += (double)(pl.row_off[s + 1] - pl.row_off[s]) * hq * ((hd + 2) * 4.0 * pl.nsplit[s] + hd * es);
+        st = timed(c, ARCHER_K_ATTN_MERGE, mbytes, 0.0, [&] {
+          launch_attn_merge<bf16>(pl, a.Opart, a.ML, a.O, hq, hd, a.ldo, c->stream);
+          return 0;
+        });
+        if (st) return st;
+      }
+    }
+    {
+      GemmArgs a = gargs(c->at<char>(L.O), hq * hd, c->w_o[l], hq * hd, rows, d, hq * hd);
+      a.X = x; a.ldx = d;
+      if ((st = gemm(c, ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
+    }
+    if ((st = norm(c->mlp_norm[l], 0, rows, act))) return st;
+    {
+      GemmArgs a = gargs(act, d, c->w_gate[l], d, rows, 2 * F, d);
+      a.W2 = c->w_up[l];
+      a.H = c->at<char>(L.H); a.ldh = F;
+      if ((st = gemm(c, ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
+    }
+    {
+      GemmArgs a = gargs(c->at<char>(L.H), F, c->w_down[l], F, rows, d, F);
+      a.X = x; a.ldx = d;
+      if ((st = gemm(c, ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
+    }
+  }
+  const int nresp = pl.n * pl.G;
+  if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn)))) return st;
+  {
+    GemmArgs a = gargs(c->at<char>(L.Cn), d, c->lm_head, d, nresp, m.vocab, d);
+    a.C = logits; a.ldc = m.vocab; a.out_row = c->at<int>(L.out_row);
+    if ((st = gemm(c, ARCHER_K_GEMM_HEAD, EPI_STORE, a))) return st;
+  }
+  HIPCHK(hipGetLastError());
+  return ARCHER_OK;
+}
+
+archer_status decide_impl(archer_ctx* c, const float* logits, const int32_t* g_in, int32_t* g_out, int k,
+                          float tau, int max_remask, int final_step, int32_t* dist, int32_t* unmask_pos,
+                          int32_t* remask_pos, int32_t* tr_dist, int32_t* tr_unmask, int32_t* tr_utok,
+                          int32_t* tr_remask) {
+  const int B = c->batch, G = c->lim.resp_len, V = c->cfg.vocab;
+  const int rows = B * G;
+  const float log_tau = (float)std::log((double)tau);
+  return timed(c, ARCHER_K_DECIDE, (double)rows * V * 4, 0.0, [&] {
+    launch_rowstats(rows, logits, V, c->cfg.mask_id, g_in, c->at<int>(c->L.xhat), c->at<float>(c->L.ell),
+                    c->at<float>(c->L.qv), c->stream);
+    launch_select(B, g_in, g_out, c->at<int>(c->L.g_anchor), c->at<int>(c->L.xhat), c->at<float>(c->L.ell),
+                  c->at<float>(c->L.qv), G, c->cfg.mask_id, k, log_tau, max_remask, final_step,
+                  dist ? dist : c->at<int>(c->L.dist), unmask_pos, remask_pos, tr_dist, tr_unmask, tr_utok,
+                  tr_remask, c->stream);
+    return 0;
+  });
+}
+
+archer_status set_batch(archer_ctx* c, int batch, const int32_t* prompt_len) {
+  if (batch < 1 || batch > c->lim.max_batch) return fail(ARCHER_E_SHAPE, "batch outside [1, max_batch]");
+  if (!prompt_len) return fail(ARCHER_E_ARG, "null prompt_len");
+  long total = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (prompt_len[b] < 1 || prompt_len[b] > c->lim.max_prompt_len)
+      return fail(ARCHER_E_SHAPE, "prompt length outside [1, max_prompt_len]");
+    total += prompt_len[b];
+  }
+  if (total > c->lim.max_prompt_total) return fail(ARCHER_E_SHAPE, "sum of prompt lengths exceeds max_prompt_total");
+  c->batch = batch;
+  int coff = 0, toff = 0;
+  for (int b = 0; b < batch; ++b) {
+    c->plen[b] = prompt_len[b];
+    c->cache_off[b] = coff;
+    c->tok_off[b] = toff;
+    c->has_cache[b] = false;
+    coff += (prompt_len[b] + 63) & ~63;
+    toff += prompt_len[b];
+  }
+  return ARCHER_OK;
+}
+
+archer_status check_same_batch(const archer_ctx* c, int batch, const int32_t* prompt_len) {
+  if (batch != c->batch) return fail(ARCHER_E_STATE, "batch differs from the current batch");
+  if (!prompt_len) return fail(ARCHER_E_ARG, "null prompt_len");
+  for (int b = 0; b < batch; ++b)
+    if (prompt_len[b] != c->plen[b]) return fail(ARCHER_E_STATE, "prompt_len differs from the current batch");
+  return ARCHER_OK;
+}
+
+archer_status read_err_flag(archer_ctx* c) {
+  int flag = 0;
+  HIPCHK(hipMemcpyAsync(&flag, c->at<int>(c->L.err), sizeof(int), hipMemcpyDeviceToHost, c->stream));
+  HIPCHK(hipStreamSynchronize(c->stream));
+  if (flag) {
+    int zero = 0;
+    HIPCHK(hipMemcpyAsync(c->at<int>(c->L.err), &zero, sizeof(int), hipMemcpyHostToDevice, c->stream));
+    HIPCHK(hipStreamSynchronize(c->stream));
+    return fail(ARCHER_E_ARG, "a token id was outside [0, vocab) or a prompt token was MASK");
+  }
+  return ARCHER_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+extern "C" {
+
+const char* archer_last_error(void) { return g_err.c_str(); }
+
+size_t archer_workspace_bytes(const archer_model_cfg* cfg, const archer_limits* lim) {
+  const std::string e = check_cfg(cfg, lim);
+  if (!e.empty()) { g_err = e; return 0; }
+  return make_layout(cfg, lim).total;
+}
+
+archer_status archer_init(const archer_model_cfg* cfg, const archer_weights* w, const archer_limits* lim,
+                          void* workspace, size_t ws_bytes, void* hip_stream, archer_ctx** out) {
+  if (!out) return fail(ARCHER_E_ARG, "null out");
+  *out = nullptr;
+  const std::string e = check_cfg(cfg, lim);
+  if (!e.empty()) return fail(ARCHER_E_UNSUPPORTED, e);
+  if (!w || !w->tok_emb || !w->lm_head || !w->final_norm || !w->attn_norm || !w->w_qkv || !w->w_o ||
+      !w->mlp_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return fail(ARCHER_E_ARG, "null weight pointer");
+  for (int l = 0; l < cfg->n_layers; ++l)
+    if (!w->attn_norm[l] || !w->w_qkv[l] || !w->w_o[l] || !w->mlp_norm[l] || !w->w_gate[l] || !w->w_up[l] ||
+        !w->w_down[l])
+      return fail(ARCHER_E_ARG, "null per-layer weight pointer");
+  if (!workspace || ((uintptr_t)workspace & 255)) return fail(ARCHER_E_ARG, "workspace null or not 256-byte aligned");
+  const Layout L = make_layout(cfg, lim);
+  if (ws_bytes < L.total) return fail(ARCHER_E_WORKSPACE, "workspace smaller than archer_workspace_bytes()");
+  archer_ctx* c = new archer_ctx();
+  c->cfg = *cfg;
+  c->lim = *lim;
+  c->L = L;
+  c->stream = (hipStream_t)hip_stream;
+  c->ws = (char*)workspace;
+  c->esz = cfg->dtype == ARCHER_BF16 ? 2 : 4;
+  c->tok_emb = w->tok_emb;
+  c->lm_head = w->lm_head;
+  c->final_norm = w->final_norm;
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    c->attn_norm.push_back(w->attn_norm[l]);
+    c->mlp_norm.push_back(w->mlp_norm[l]);
+    c->w_qkv.push_back(w->w_qkv[l]);
+    c->w_o.push_back(w->w_o[l]);
+    c->w_gate.push_back(w->w_gate[l]);
+    c->w_up.push_back(w->w_up[l]);
+    c->w_down.push_back(w->w_down[l]);
+  }
+  launch_rope_table(c->at<float2>(L.rope), L.max_pos, cfg->head_dim, (double)cfg->rope_theta, c->stream);
+  hipError_t he = hipMemsetAsync(c->at<int>(L.err), 0, 256, c->stream);
+  if (he == hipSuccess) he = hipGetLastError();
+  if (he == hipSuccess) he = hipStreamSynchronize(c->stream);
+  if (he != hipSuccess) {
+    delete c;
+    return fail(ARCHER_E_HIP, std::string("archer_init: ") + hipGetErrorString(he));
+  }
+  *out = c;
+  return ARCHER_OK;
+}
+
+archer_status archer_refresh_prompt(archer_ctx* c, int32_t batch, const int32_t* prompt, const int32_t* prompt_len,
+                                    const int32_t* response, const uint8_t* seq_sel, float* logits) {
+  if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  if (!prompt || !response || !logits) return fail(ARCHER_E_ARG, "null prompt, response or logits");
+  archer_status st = seq_sel ? check_same_batch(c, batch, prompt_len) : set_batch(c, batch, prompt_len);
+  if (st) return st;
+  std::vector<int> sel;
+  for (int b = 0; b < batch; ++b)
+    if (!seq_sel || seq_sel[b]) sel.push_back(b);
+  st = run_forward(c, true, sel, prompt, response, logits);
+  if (st) return st;
+  for (int b : sel) c->has_cache[b] = true;
+  return ARCHER_OK;
+}
+
+archer_status archer_step(archer_ctx* c, const int32_t* response, const uint8_t* seq_sel, float* logits) {
+  if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  if (!response || !logits) return fail(ARCHER_E_ARG, "null response or logits");
+  if (c->batch == 0) return fail(ARCHER_E_STATE, "archer_step before any archer_refresh_prompt");
+  std::vector<int> sel;
+  for (int b = 0; b < c->batch; ++b)
+    if (!seq_sel || seq_sel[b]) {
+      if (!c->has_cache[b]) return fail(ARCHER_E_STATE, "a selected sequence has no prompt cache");
+      sel.push_back(b);
+    }
+  return run_forward(c, false, sel, nullptr, response, logits);
+}
+
+archer_status archer_decide(archer_ctx* c, const float* logits, const int32_t* g_in, int32_t* g_out,
+                            const archer_decide_cfg* dc, int32_t* dist_out, int32_t* unmask_pos,
+                            int32_t* remask_pos) {
+  if (!c || !dc) return fail(ARCHER_E_ARG, "null ctx or cfg");
+  if (!logits || !g_in || !g_out) return fail(ARCHER_E_ARG, "null logits or token arrays");
+  if (g_in == g_out) return fail(ARCHER_E_ARG, "g_out must not alias g_in");
+  if (c->batch == 0) return fail(ARCHER_E_STATE, "archer_decide before any archer_refresh_prompt");
+  if (dc->unmask_per_step < 1 || dc->unmask_per_step > c->lim.resp_len) return fail(ARCHER_E_ARG, "unmask_per_step outside [1, G]");
+  if (!(dc->remask_threshold > 0.f && dc->remask_threshold < 1.f)) return fail(ARCHER_E_ARG, "remask_threshold outside (0, 1)");
+  if (dc->max_remask != 0 && dc->max_remask != 1) return fail(ARCHER_E_ARG, "max_remask must be 0 or 1");
+  archer_status st = decide_impl(c, logits, g_in, g_out, dc->unmask_per_step, dc->remask_threshold, dc->max_remask,
+                                 dc->final_step, dist_out, unmask_pos, remask_pos, nullptr, nullptr, nullptr,
+                                 nullptr);
+  if (st) return st;
+  HIPCHK(hipGetLastError());
+  return ARCHER_OK;
+}
+
+archer_status archer_decode(archer_ctx* c, int32_t batch, const int32_t* prompt, const int32_t* prompt_len,
+                            int32_t* response_inout, const archer_decode_cfg* dc, archer_trace* tr) {
+  if (!c || !dc) return fail(ARCHER_E_ARG, "null ctx or cfg");
+  if (!prompt || !response_inout) return fail(ARCHER_E_ARG, "null prompt or response");
+  if (dc->policy < ARCHER_REFRESH_HAMMING || dc->policy > ARCHER_REFRESH_ALWAYS) return fail(ARCHER_E_ARG, "bad policy");
+  if (dc->K < 0) return fail(ARCHER_E_ARG, "K must be >= 0");
+  if (dc->steps < 1) return fail(ARCHER_E_ARG, "steps must be >= 1");
+  if (dc->unmask_per_step < 1 || dc->unmask_per_step > c->lim.resp_len) return fail(ARCHER_E_ARG, "unmask_per_step outside [1, G]");
+  if (!(dc->remask_threshold > 0.f && dc->remask_threshold < 1.f)) return fail(ARCHER_E_ARG, "remask_threshold outside (0, 1)");
+  if (dc->max_remask != 0 && dc->max_remask != 1) return fail(ARCHER_E_ARG, "max_remask must be 0 or 1");
+  archer_status st = set_batch(c, batch, prompt_len);
+  if (st) return st;
+  const int B = batch, G = c->lim.resp_len, T = dc->steps, k = dc->unmask_per_step;
+  int* g[2] = {c->at<int>(c->L.gbuf0), c->at<int>(c->L.gbuf1)};
+  float* logits = c->at<float>(c->L.logits);
+  HIPCHK(hipMemcpyAsync(g[0], response_inout, (size_t)B * G * 4, hipMemcpyDeviceToDevice, c->stream));
+  std::vector<int> all(B);
+  for (int b = 0; b < B; ++b) all[b] = b;
+  std::vector<int> h_ref((size_t)T * B, 0), h_age((size_t)T * B, 0), r(B, 0);
+  std::vector<int> D(B, 0);
+
+  if ((st = run_forward(c, true, all, prompt, g[0], logits))) return st;
+  for (int b = 0; b < B; ++b) { c->has_cache[b] = true; h_ref[b] = 1; }
+  int cur = 0;
+  for (int t = 0; t < T; ++t) {
+    const bool final = t == T - 1;
+    int32_t* trd = (tr && tr->dist && !final) ? tr->dist + (size_t)(t + 1) * B : nullptr;
+    int32_t* tru = (tr && tr->unmask_pos) ? tr->unmask_pos + (size_t)t * B * k : nullptr;
+    int32_t* trt = (tr && tr->unmask_tok) ? tr->unmask_tok + (size_t)t * B * k : nullptr;
+    int32_t* trr = (tr && tr->remask_pos) ? tr->remask_pos + (size_t)t * B : nullptr;
+    st = decide_impl(c, logits, g[cur], g[cur ^ 1], k, dc->remask_threshold, dc->max_remask, final ? 1 : 0,
+                     nullptr, nullptr, nullptr, trd, tru, trt, trr);
+    if (st) return st;
+    cur ^= 1;
+    if (final) break;
+    const int s = t + 1;
+    if (dc->policy == ARCHER_REFRESH_HAMMING) {
+      HIPCHK(hipMemcpyAsync(D.data(), c->at<int>(c->L.dist), (size_t)B * 4, hipMemcpyDeviceToHost, c->stream));
+      HIPCHK(hipStreamSynchronize(c->stream));
+    }
+    std::vector<int> full, cached;
+    for (int b = 0; b < B; ++b) {
+      const int A = s - r[b];
+      h_age[(size_t)s * B + b] = A;
+      bool refresh;
+      if (dc->policy == ARCHER_REFRESH_ALWAYS) refresh = true;
+      else if (dc->policy == ARCHER_REFRESH_AGE) refresh = A >= dc->K;
+      else refresh = D[b] >= dc->K;
+      (refresh ? full : cached).push_back(b);
+      if (refresh) { r[b] = s; h_ref[(size_t)s * B + b] = 1; }
+    }
+    if ((st = run_forward(c, true, full, prompt, g[cur], logits))) return st;
+    if ((st = run_forward(c, false, cached, nullptr, g[cur], logits))) return st;
+  }
+  HIPCHK(hipMemcpyAsync(response_inout, g[cur], (size_t)B * G * 4, hipMemcpyDeviceToDevice, c->stream));
+  if (tr && tr->dist) HIPCHK(hipMemsetAsync(tr->dist, 0, (size_t)B * 4, c->stream));
+  if (tr && tr->refreshed)
+    HIPCHK(hipMemcpyAsync(tr->refreshed, h_ref.data(), h_ref.size() * 4, hipMemcpyHostToDevice, c->stream));
+  if (tr && tr->age)
+    HIPCHK(hipMemcpyAsync(tr->age, h_age.data(), h_age.size() * 4, hipMemcpyHostToDevice, c->stream));
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipStreamSynchronize(c->stream));
+  return read_err_flag(c);
+}
+
+archer_status archer_sync(archer_ctx* c) {
+  if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  HIPCHK(hipGetLastError());
+  return read_err_flag(c);
+}
+
+void archer_destroy(archer_ctx* c) {
+  if (!c) return;
+  for (auto& r : c->t_recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  delete c;
+}
+
+archer_status archer_timing_begin(archer_ctx* c, uint32_t mask) {
+  if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  c->t_on = mask != 0;
+  c->t_mask = mask;
+  c->t_used = 0;
+  return ARCHER_OK;
+}
+
+archer_status archer_timing_end(archer_ctx* c, int64_t* launches, double* total_ms, double* bytes, double* flops) {
+  if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  HIPCHK(hipStreamSynchronize(c->stream));
+  int64_t nl[ARCHER_K_COUNT] = {0};
+  double ms[ARCHER_K_COUNT] = {0}, by[ARCHER_K_COUNT] = {0}, fl[ARCHER_K_COUNT] = {0};
+  for (size_t i = 0; i < c->t_used; ++i) {
+    const TimerRec& r = c->t_recs[i];
+    float e = 0.f;
+    HIPCHK(hipEventElapsedTime(&e, r.a, r.b));
+    nl[r.cls] += 1;
+    ms[r.cls] += e;
+    by[r.cls] += r.bytes;
+    fl[r.cls] += r.flops;
+  }
+  for (int k = 0; k < ARCHER_K_COUNT; ++k) {
+    if (launches) launches[k] = nl[k];
+    if (total_ms) total_ms[k] = ms[k];
+    if (bytes) bytes[k] = by[k];
+    if (flops) flops[k] = fl[k];
+  }
+  c->t_on = false;
+  c->t_used = 0;
+  return ARCHER_OK;
+}
+
+// ---------------------------------------------------------------------------
+archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, const void* W, float* Y,
+                             void* hip_stream) {
+  if (!A || !W || !Y) return fail(ARCHER_E_ARG, "null operand");
+  if (M < 1 || N < 64 || K < 64 || N % 64 || K % 64) return fail(ARCHER_E_SHAPE, "need M >= 1 and N, K multiples of 64");
+  GemmArgs a = gargs(A, K, W, K, M, N, K);
+  a.C = Y; a.ldc = N;
+  int rc;
+  if (dtype == ARCHER_BF16) rc = launch_gemm_bf16(EPI_STORE, a, (hipStream_t)hip_stream);
+  else if (dtype == ARCHER_FP32) rc = launch_gemm_f32(EPI_STORE, a, (hipStream_t)hip_stream);
+  else return fail(ARCHER_E_ARG, "bad dtype");
+  if (rc) return fail(ARCHER_E_UNSUPPORTED, "gemm shape unsupported");
+  HIPCHK(hipGetLastError());
+  return ARCHER_OK;
+}
+
+static int op_attn_nsplit(int dtype, int nk) { return dtype == ARCHER_BF16 ? attn_nsplit_for_keys(nk) : 1; }
+
+size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32_t hd, int32_t nk) {
+  if (Mq < 1 || Hq < 1 || hd < 1 || nk < 1) return 0;
+  const int ns = op_attn_nsplit(dtype, nk);
+  return align_up((size_t)ns * Hq * Mq * hd * 4, 256) + (size_t)ns * Hq * Mq * 2 * 4 + 256;
+}
+
+archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd, const void* Q,
+                                  const void* K1, const void* Vt1, int32_t nk1, int32_t ld1, const void* K2,
+                                  const void* Vt2, int32_t nk2, int32_t ld2, void* O, void* workspace,
+                                  size_t ws_bytes, void* hip_stream) {
+  if (!Q || !K1 || !Vt1 || !K2 || !Vt2 || !O) return fail(ARCHER_E_ARG, "null operand");
+  if (Mq < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (hd != 64 && hd != 128)) return fail(ARCHER_E_SHAPE, "bad head shape");
+  if (nk1 < 1 || nk2 < 1 || ld1 % 64 || ld2 % 64 || nk1 > ld1 || nk2 > ld2) return fail(ARCHER_E_SHAPE, "bad key segments");
+  if (dtype != ARCHER_BF16 && dtype != ARCHER_FP32) return fail(ARCHER_E_ARG, "bad dtype");
+  const int ns = op_attn_nsplit(dtype, ((nk1 + 63) & ~63) + nk2);
+  const size_t need = archer_op_attention_ws_bytes(dtype, Mq, Hq, hd, ((nk1 + 63) & ~63) + nk2);
+  if (ns > 1 && (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255)))
+    return fail(ARCHER_E_WORKSPACE, "attention workspace too small or misaligned");
+  SeqPlan p;
+  memset(&p, 0, sizeof(p));
+  p.n = 1; p.full = 0; p.G = nk2; p.rows = Mq;
+  p.row_off[1] = Mq; p.p_len[0] = nk1;
+  const int qt = dtype == ARCHER_BF16 ? ATTN_QT_BF16 : ATTN_QT_F32;
+  p.qt_off[1] = (Mq + qt - 1) / qt;
+  p.nsplit[0] = ns;
+  p.max_split = ns;
+  AttnArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Q = Q; a.ldq = Mq;
+  a.Kc = K1; a.Vtc = Vt1; a.ldcache = ld1;
+  a.Kf = K2; a.Vtf = Vt2; a.ldfresh = ld2;
+  a.O = O; a.ldo = Hq * hd;
+  a.hq = Hq; a.hkv = Hkv; a.hd = hd;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+  if (ns > 1) {
+    a.Opart = (float*)workspace;
+    a.ML = (float*)((char*)workspace + align_up((size_t)ns * Hq * Mq * hd * 4, 256));
+  }
+  hipStream_t st = (hipStream_t)hip_stream;
+  int rc;
+  if (dtype == ARCHER_BF16) {
+    rc = launch_attn_bf16(p, a, st);
+    if (!rc && ns > 1) launch_attn_merge<bf16>(p, a.Opart, a.ML, O, Hq, hd, a.ldo, st);
+  } else {
+    rc = launch_attn_f32(p, a, ((nk1 + 63) & ~63) + nk2, st);
+  }
+  if (rc) return fail(ARCHER_E_UNSUPPORTED, "attention shape unsupported");
+  HIPCHK(hipGetLastError());
+  return ARCHER_OK;
+}
+
+}  // extern "C"

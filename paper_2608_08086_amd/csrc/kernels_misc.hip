@@ -1,0 +1,345 @@
+// Row-wise kernels of the Archer path: RoPE table, embedding gather, RMSNorm,
+// decision row statistics and selection, and the split-KV attention merge.
+#include "launch.h"
+
+// ---------------------------------------------------------------------------
+// RoPE table: tab[pos][j] = (cos, sin)(pos * theta^(-2j/hd)), computed in fp64.
+__global__ void rope_table_kernel(float2* tab, int max_pos, int half, int hd, double theta) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)max_pos * half) return;
+  const int pos = (int)(i / half), j = (int)(i % half);
+  const double ang = (double)pos * pow(theta, -2.0 * (double)j / (double)hd);
+  tab[i] = make_float2((float)cos(ang), (float)sin(ang));
+}
+
+void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st) {
+  const long n = (long)max_pos * (hd / 2);
+  rope_table_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(tab, max_pos, hd / 2, hd, theta);
+}
+
+// ---------------------------------------------------------------------------
+// Embedding gather.  One block per pass row: resolve (sequence, token,
+// position, K/V destination) from the plan, copy E[token] into the fp32
+// residual stream, and in a full pass record the response token as anchor g_r.
+template <class T>
+__global__ __launch_bounds__(256) void embed_kernel(SeqPlan pl, const T* __restrict__ emb, int d,
+                                                    int V, int mask_id, const int* __restrict__ prompt,
+                                                    const int* __restrict__ resp, float* __restrict__ x,
+                                                    int* __restrict__ row_pos, int* __restrict__ row_dst,
+                                                    int* __restrict__ g_anchor, int* __restrict__ err) {
+  const int i = blockIdx.x;
+  const int s = plan_find(pl.row_off, pl.n, i);
+  const int j = i - pl.row_off[s];
+  const int b = pl.seq[s], P = pl.p_len[s], G = pl.G;
+  int tok, pos, dst;
+  bool is_prompt = pl.full && j < P;
+  if (is_prompt) {
+    tok = prompt[pl.tok_off[s] + j];
+    pos = j;
+    dst = -1 - (pl.cache_off[s] + j);
+  } else {
+    const int r = pl.full ? j - P : j;
+    tok = resp[b * G + r];
+    pos = P + r;
+    dst = b * G + r;
+    if (pl.full && threadIdx.x == 0) g_anchor[b * G + r] = tok;
+  }
+  const bool bad = tok < 0 || tok >= V || (is_prompt && tok == mask_id);
+  if (bad) {
+    if (threadIdx.x == 0) atomicOr(err, 1);
+    tok = 0;
+  }
+  if (threadIdx.x == 0) {
+    row_pos[i] = pos;
+    row_dst[i] = dst;
+  }
+  const T* e = emb + (size_t)tok * d;
+  float* xr = x + (size_t)i * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) xr[c] = to_f32(e[c]);
+}
+
+template <class T>
+void launch_embed(const SeqPlan& pl, const void* emb, int d, int V, int mask_id, const int* prompt,
+                  const int* resp, float* x, int* row_pos, int* row_dst, int* g_anchor, int* err,
+                  hipStream_t st) {
+  embed_kernel<T><<<pl.rows, 256, 0, st>>>(pl, (const T*)emb, d, V, mask_id, prompt, resp, x, row_pos,
+                                           row_dst, g_anchor, err);
+}
+template void launch_embed<float>(const SeqPlan&, const void*, int, int, int, const int*, const int*,
+                                  float*, int*, int*, int*, int*, hipStream_t);
+template void launch_embed<bf16>(const SeqPlan&, const void*, int, int, int, const int*, const int*,
+                                 float*, int*, int*, int*, int*, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// RMSNorm: out[r] = round_T(x[r] / sqrt(mean(x[r]^2) + eps) * gain), fp32 math.
+// gather = 1 (final norm): output row ri in [0, n*G) is response row ri % G of
+// pass sequence ri / G; its logits row b*G + (ri % G) is written to out_row.
+template <class T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, const float* __restrict__ x,
+                                                      const float* __restrict__ gain, T* __restrict__ out,
+                                                      int d, float eps, int* __restrict__ out_row) {
+  __shared__ float red[16];
+  const int ro = blockIdx.x;
+  int ri = ro;
+  if (gather) {
+    const int s = ro / pl.G, r = ro % pl.G;
+    ri = pl.row_off[s] + (pl.full ? pl.p_len[s] : 0) + r;
+    if (threadIdx.x == 0) out_row[ro] = pl.seq[s] * pl.G + r;
+  }
+  const float* xr = x + (size_t)ri * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    const float4 v = *(const float4*)(xr + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  T* orow = out + (size_t)ro * d;
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    const float4 v = *(const float4*)(xr + c);
+    const float4 g = *(const float4*)(gain + c);
+    orow[c + 0] = from_f32<T>(v.x * inv * g.x);
+    orow[c + 1] = from_f32<T>(v.y * inv * g.y);
+    orow[c + 2] = from_f32<T>(v.z * inv * g.z);
+    orow[c + 3] = from_f32<T>(v.w * inv * g.w);
+  }
+}
+
+template <class T>
+void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
+                    int d, float eps, int* out_row, hipStream_t st) {
+  rmsnorm_kernel<T><<<nrows, 256, 0, st>>>(pl, gather, x, gain, (T*)out, d, eps, out_row);
+}
+template void launch_rmsnorm<float>(const SeqPlan&, int, int, const float*, const float*, void*, int, float,
+                                    int*, hipStream_t);
+template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const float*, void*, int, float,
+                                   int*, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Decision pass 1: per response row, over the non-MASK vocabulary:
+//   m = max z, xhat = smallest id attaining m, s = sum exp(z - m),
+//   ell = -log s (= m - lse, log top probability),
+//   q = z[g] - m - log s (log probability of the current token; decided rows).
+// One block per row; each thread scans a strided slice with an online
+// (max, sum) pair, then a fixed-order tree combines the threads.
+__device__ __forceinline__ void stat_combine(float& m, float& s, int& id, float m2, float s2, int id2) {
+  if (s2 == 0.f) return;
+  if (s == 0.f) { m = m2; s = s2; id = id2; return; }
+  if (m2 > m) {
+    s = s * expf(m - m2) + s2;
+    m = m2;
+    id = id2;
+  } else if (m2 < m) {
+    s = s + s2 * expf(m2 - m);
+  } else {
+    s = s + s2;
+    id = min(id, id2);
+  }
+}
+
+__global__ __launch_bounds__(256) void rowstats_kernel(const float* __restrict__ logits, int V, int mask_id,
+                                                       const int* __restrict__ g, int* __restrict__ xhat,
+                                                       float* __restrict__ ell, float* __restrict__ qv) {
+  __shared__ float sm[256], ss[256];
+  __shared__ int sid[256];
+  const int row = blockIdx.x;
+  const float* z = logits + (size_t)row * V;
+  float m = -INFINITY, s = 0.f;
+  int id = 0x7fffffff;
+  for (int v0 = threadIdx.x * 4; v0 < V; v0 += blockDim.x * 4) {
+    const float4 t = *(const float4*)(z + v0);
+    const float e[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int v = v0 + k;
+      if (v == mask_id) continue;
+      const float zv = e[k];
+      if (zv > m) {
+        s = s * expf(m - zv) + 1.f;
+        m = zv;
+        id = v;
+      } else {
+        s += expf(zv - m);
+      }
+    }
+  }
+  sm[threadIdx.x] = m;
+  ss[threadIdx.x] = s;
+  sid[threadIdx.x] = id;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      float a = sm[threadIdx.x], b = ss[threadIdx.x];
+      int c = sid[threadIdx.x];
+      stat_combine(a, b, c, sm[threadIdx.x + w], ss[threadIdx.x + w], sid[threadIdx.x + w]);
+      sm[threadIdx.x] = a;
+      ss[threadIdx.x] = b;
+      sid[threadIdx.x] = c;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float M = sm[0], S = ss[0];
+    const float logs = logf(S);
+    xhat[row] = sid[0];
+    ell[row] = -logs;
+    const int cur = g[row];
+    qv[row] = (cur != mask_id && cur >= 0 && cur < V) ? (z[cur] - M) - logs : 0.f;
+  }
+}
+
+void launch_rowstats(int rows, const float* logits, int V, int mask_id, const int* g, int* xhat, float* ell,
+                     float* qv, hipStream_t st) {
+  rowstats_kernel<<<rows, 256, 0, st>>>(logits, V, mask_id, g, xhat, ell, qv);
+}
+
+// ---------------------------------------------------------------------------
+// Decision pass 2 (one block per sequence): unmask the top-k masked rows by
+// ell (ties: smaller position) to xhat, remask the decided row of smallest q
+// (ties: smaller position) when q < log(tau), then D = d_H(g_out, g_anchor).
+__global__ __launch_bounds__(512) void select_kernel(const int* __restrict__ g_in, int* __restrict__ g_out,
+                                                     const int* __restrict__ g_anchor,
+                                                     const int* __restrict__ xhat, const float* __restrict__ ell,
+                                                     const float* __restrict__ qv, int G, int mask_id, int k,
+                                                     float log_tau, int max_remask, int final_step,
+                                                     int* __restrict__ dist, int* __restrict__ unmask_pos,
+                                                     int* __restrict__ remask_pos, int* __restrict__ tr_dist,
+                                                     int* __restrict__ tr_unmask, int* __restrict__ tr_utok,
+                                                     int* __restrict__ tr_remask) {
+  extern __shared__ unsigned char smem_raw[];
+  float* sell = (float*)smem_raw;               // [G]
+  int* smask = (int*)(sell + G);                // [G]
+  int* ssel = smask + G;                        // [G]
+  __shared__ float rq[512];
+  __shared__ int ri[512];
+  __shared__ int rcnt[512];
+  const int b = blockIdx.x;
+  const int* gi = g_in + (size_t)b * G;
+  for (int i = threadIdx.x; i < G; i += blockDim.x) {
+    const int msk = gi[i] == mask_id;
+    smask[i] = msk;
+    sell[i] = ell[(size_t)b * G + i];
+  }
+  __syncthreads();
+  // unmask selection by rank
+  for (int i = threadIdx.x; i < G; i += blockDim.x) {
+    int sel = 0;
+    if (smask[i]) {
+      if (final_step) {
+        sel = 1;
+      } else {
+        const float ei = sell[i];
+        int rank = 0;
+        for (int j = 0; j < G; ++j)
+          rank += smask[j] && (sell[j] > ei || (sell[j] == ei && j < i));
+        sel = rank < k;
+      }
+    }
+    ssel[i] = sel;
+  }
+  // remask candidate: argmin (q, position) over decided rows
+  float bq = INFINITY;
+  int bi = 0x7fffffff;
+  for (int i = threadIdx.x; i < G; i += blockDim.x) {
+    if (!smask[i]) {
+      const float q = qv[(size_t)b * G + i];
+      if (q < bq || (q == bq && i < bi)) { bq = q; bi = i; }
+    }
+  }
+  rq[threadIdx.x] = bq;
+  ri[threadIdx.x] = bi;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      const float q2 = rq[threadIdx.x + w];
+      const int i2 = ri[threadIdx.x + w];
+      if (q2 < rq[threadIdx.x] || (q2 == rq[threadIdx.x] && i2 < ri[threadIdx.x])) {
+        rq[threadIdx.x] = q2;
+        ri[threadIdx.x] = i2;
+      }
+    }
+    __syncthreads();
+  }
+  const int rm = (!final_step && max_remask > 0 && ri[0] < G && rq[0] < log_tau) ? ri[0] : -1;
+  // write g_out, count distance to the anchor, list unmasked positions
+  int cnt = 0;
+  for (int i = threadIdx.x; i < G; i += blockDim.x) {
+    int v = gi[i];
+    if (ssel[i]) v = xhat[(size_t)b * G + i];
+    if (i == rm) v = mask_id;
+    g_out[(size_t)b * G + i] = v;
+    cnt += v != g_anchor[(size_t)b * G + i];
+    if (ssel[i] && (unmask_pos || tr_unmask || tr_utok)) {
+      int order = 0;
+      for (int j = 0; j < i; ++j) order += ssel[j];
+      if (order < k) {
+        if (unmask_pos) unmask_pos[(size_t)b * k + order] = i;
+        if (tr_unmask) tr_unmask[(size_t)b * k + order] = i;
+        if (tr_utok) tr_utok[(size_t)b * k + order] = v;
+      }
+    }
+  }
+  rcnt[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) rcnt[threadIdx.x] += rcnt[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    int nsel = 0;
+    for (int j = 0; j < G; ++j) nsel += ssel[j];
+    for (int o = nsel; o < k; ++o) {
+      if (unmask_pos) unmask_pos[(size_t)b * k + o] = -1;
+      if (tr_unmask) tr_unmask[(size_t)b * k + o] = -1;
+      if (tr_utok) tr_utok[(size_t)b * k + o] = -1;
+    }
+    if (dist) dist[b] = rcnt[0];
+    if (tr_dist) tr_dist[b] = rcnt[0];
+    if (remask_pos) remask_pos[b] = rm;
+    if (tr_remask) tr_remask[b] = rm;
+  }
+}
+
+void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, const int* xhat, const float* ell,
+                   const float* qv, int G, int mask_id, int k, float log_tau, int max_remask, int final_step,
+                   int* dist, int* unmask_pos, int* remask_pos, int* tr_dist, int* tr_unmask, int* tr_utok,
+                   int* tr_remask, hipStream_t st) {
+  const size_t shm = (size_t)G * 12;
+  select_kernel<<<B, 512, shm, st>>>(g_in, g_out, g_anchor, xhat, ell, qv, G, mask_id, k, log_tau, max_remask,
+                                     final_step, dist, unmask_pos, remask_pos, tr_dist, tr_unmask, tr_utok,
+                                     tr_remask);
+}
+
+// ---------------------------------------------------------------------------
+// Split-KV merge: O[row][h*hd + d] = sum_s w_s O_s / sum_s w_s l_s with
+// w_s = 2^(m_s - max_s m_s); partials are unnormalised, m in log2 units.
+// Rows of sequences attended in one split were written directly and are skipped.
+template <class T>
+__global__ void attn_merge_kernel(SeqPlan pl, const float* __restrict__ Op, const float* __restrict__ ML,
+                                  T* __restrict__ O, int hq, int hd, int ldo) {
+  const int row = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
+  const int nsplit = pl.nsplit[plan_find(pl.row_off, pl.n, row)];
+  if (nsplit <= 1) return;
+  const int rows = pl.rows;
+  float M = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ML[(((size_t)s * hq + h) * rows + row) * 2]);
+  float num = 0.f, den = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const size_t base = ((size_t)s * hq + h) * rows + row;
+    const float m = ML[base * 2], l = ML[base * 2 + 1];
+    const float w = (l > 0.f) ? exp2f(m - M) : 0.f;
+    den += w * l;
+    if (d < hd) num += w * Op[base * hd + d];
+  }
+  if (d < hd) O[(size_t)row * ldo + h * hd + d] = from_f32<T>(num / den);
+}
+
+template <class T>
+void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, int hq, int hd, int ldo,
+                       hipStream_t st) {
+  attn_merge_kernel<T><<<dim3(pl.rows, hq), hd, 0, st>>>(pl, Op, ML, (T*)O, hq, hd, ldo);
+}
+template void launch_attn_merge<float>(const SeqPlan&, const float*, const float*, void*, int, int, int,
+                                       hipStream_t);
+template void launch_attn_merge<bf16>(const SeqPlan&, const float*, const float*, void*, int, int, int,
+                                      hipStream_t);

@@ -1,0 +1,71 @@
+// Kernel launchers of the Archer HIP library (internal interface between the
+// host engine and the kernels).
+#pragma once
+
+#include "common.h"
+
+// Epilogues of the projection GEMM Y = A W^T.
+enum GemmEpi {
+  EPI_STORE = 0,   // C[out_row ? out_row[r] : r][c] = y (fp32; LM-head logits, op hook)
+  EPI_RESID = 1,   // X[r][c] += y (fp32 residual stream; O and down projections)
+  EPI_SWIGLU = 2,  // H[r][f] = silu(y_gate) * y_up (W = gate rows, W2 = up rows)
+  EPI_QKV = 3,     // RoPE on q/k, then scatter q -> Q, k/v -> prompt cache or fresh buffers
+};
+
+struct GemmArgs {
+  const void* A; int lda;               // [M][K]
+  const void* W; const void* W2; int ldw; // [N][K] (SWIGLU: W = gate [F][K], W2 = up [F][K], N = 2F)
+  int M, N, K;
+  float* C; int ldc; const int* out_row; // EPI_STORE
+  float* X; int ldx;                     // EPI_RESID
+  void* H; int ldh;                      // EPI_SWIGLU
+  // EPI_QKV
+  void* Qb; int ldq;                     // Q [Hq][ldq][hd]
+  void* Kc; void* Vtc; int ldcache;      // prompt cache of this layer: K [Hkv][ldcache][hd], Vt [Hkv][hd][ldcache]
+  void* Kf; void* Vtf; int ldfresh;      // fresh response K/V: K [Hkv][ldfresh][hd], Vt [Hkv][hd][ldfresh]
+  int hq, hkv, hd;
+  const int* row_pos; const int* row_dst; const float2* rope;
+};
+
+struct AttnArgs {
+  const void* Q; int ldq;                // [Hq][ldq][hd]
+  const void* Kc; const void* Vtc; int ldcache;
+  const void* Kf; const void* Vtf; int ldfresh;
+  void* O; int ldo;                      // [rows][ldo]
+  float* Opart; float* ML;               // split partials [max_split][Hq][rows][hd], [max_split][Hq][rows][2]
+  int hq, hkv, hd;
+  float scale_log2;                      // log2(e) / sqrt(hd)
+};
+
+// query tile (rows per attention workgroup) of each attention kernel
+constexpr int ATTN_QT_BF16 = 64;
+constexpr int ATTN_QT_F32 = 1;
+
+void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
+template <class T>
+void launch_embed(const SeqPlan& pl, const void* emb, int d, int V, int mask_id, const int* prompt,
+                  const int* resp, float* x, int* row_pos, int* row_dst, int* g_anchor, int* err,
+                  hipStream_t st);
+template <class T>
+void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
+                    int d, float eps, int* out_row, hipStream_t st);
+void launch_rowstats(int rows, const float* logits, int V, int mask_id, const int* g, int* xhat, float* ell,
+                     float* qv, hipStream_t st);
+void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, const int* xhat, const float* ell,
+                   const float* qv, int G, int mask_id, int k, float log_tau, int max_remask, int final_step,
+                   int* dist, int* unmask_pos, int* remask_pos, int* tr_dist, int* tr_unmask, int* tr_utok,
+                   int* tr_remask, hipStream_t st);
+template <class T>
+void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, int hq, int hd, int ldo,
+                       hipStream_t st);
+
+// GEMM: returns 0 on success, nonzero if the shape is unsupported.
+int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);
+int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st);
+
+// Split-KV count for a sequence with nkeys keys (padded key space); the same
+// function is used by every pass so results do not depend on the batch or pass.
+int attn_nsplit_for_keys(int nkeys);
+// Attention over the plan's sequences; sequences with nsplit > 1 write partials (merge separately).
+int launch_attn_bf16(const SeqPlan& pl, const AttnArgs& a, hipStream_t st);
+int launch_attn_f32(const SeqPlan& pl, const AttnArgs& a, int max_keys, hipStream_t st);

@@ -1,0 +1,121 @@
+"""GPU parity of single kernels (through archer_ops.h) against the oracle.
+
+Small shapes span several tiles with ragged tails; full-size shapes are those
+of the LLaDA-8B-shaped cached step and of the long-prompt / GQA attention, in
+the same launch configuration the model path uses, checked on sampled rows
+the oracle computes one by one.
+"""
+
+import numpy as np
+import pytest
+
+from gpu_util import archer, host, rand_bf16, rand_f32, say
+from oracle import numerics as on
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (37, 192, 320), (128, 128, 256), (300, 64, 1024),
+                                   (513, 320, 128)])
+def test_gemm_bf16_matches_oracle(M, N, K):
+    say(f"gemm bf16 M={M} N={N} K={K}")
+    a = archer()
+    A, A64 = rand_bf16((M, K), 5, 1)
+    W, W64 = rand_bf16((N, K), 5, 2)
+    Y = host(a.op_gemm(A, W, a.BF16))
+    ref = on.linear(A64, W64)
+    # fp32 accumulation of exact bf16 products: error ~ sqrt(K) * 2^-24 * |a||w|
+    np.testing.assert_allclose(Y, ref, rtol=0, atol=2e-5 * np.sqrt(K) * 4)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (70, 128, 320), (200, 192, 64)])
+def test_gemm_f32_matches_oracle(M, N, K):
+    say(f"gemm fp32 M={M} N={N} K={K}")
+    a = archer()
+    A, A64 = rand_f32((M, K), 6, 1)
+    W, W64 = rand_f32((N, K), 6, 2)
+    Y = host(a.op_gemm(A, W, a.FP32))
+    np.testing.assert_allclose(Y, on.linear(A64, W64), rtol=0, atol=1e-4)
+
+
+def test_gemm_deterministic():
+    a = archer()
+    A, _ = rand_bf16((256, 4096), 7, 1)
+    W, _ = rand_bf16((512, 4096), 7, 2)
+    Y1 = a.op_gemm(A, W)
+    Y2 = a.op_gemm(A, W)
+    assert bool((Y1 == Y2).all())
+
+
+@pytest.mark.parametrize("N,K", [(12288, 4096), (4096, 12288), (126464, 4096)])
+def test_gemm_full_size_sampled(N, K):
+    """LLaDA-8B-shaped cached-step projections (M = 256 response rows)."""
+    say(f"gemm full size M=256 N={N} K={K}")
+    a = archer()
+    M = 256
+    A, A64 = rand_bf16((M, K), 8, 1)
+    W, W64 = rand_bf16((N, K), 8, 2, scale=0.02)
+    Y = a.op_gemm(A, W)
+    rng = np.random.default_rng(0)
+    rows = np.sort(rng.choice(M, 12, replace=False))
+    cols = np.sort(rng.choice(N, 1024, replace=False))
+    got = host(Y[rows][:, cols])
+    ref = on.linear(A64[rows], W64[cols])
+    np.testing.assert_allclose(got, ref, rtol=0, atol=2e-5 * np.sqrt(K) * 4 * 0.02)
+
+
+def _attn_case(dtype, Mq, Hq, Hkv, hd, nk1, nk2, seed, rows=None, heads=None):
+    a = archer()
+    rand = rand_bf16 if dtype == a.BF16 else rand_f32
+    ld1 = (nk1 + 63) // 64 * 64
+    ld2 = (nk2 + 63) // 64 * 64
+    Q, Q64 = rand((Hq, Mq, hd), seed, 1)
+    K1, K164 = rand((Hkv, ld1, hd), seed, 2)
+    V1, V164 = rand((Hkv, hd, ld1), seed, 3)
+    K2, K264 = rand((Hkv, ld2, hd), seed, 4)
+    V2, V264 = rand((Hkv, hd, ld2), seed, 5)
+    O = host(a.op_attention(Q, K1, V1, nk1, K2, V2, nk2, dtype))
+    rows = np.arange(Mq) if rows is None else rows
+    heads = range(Hq) if heads is None else heads
+    worst = 0.0
+    for h in heads:
+        kh = h // (Hq // Hkv)
+        k = np.concatenate([K164[kh, :nk1], K264[kh, :nk2]])
+        v = np.concatenate([V164[kh, :, :nk1].T, V264[kh, :, :nk2].T])
+        ref = on.attention(Q64[h, rows], k, v)
+        worst = max(worst, float(np.max(np.abs(O[rows, h * hd:(h + 1) * hd] - ref))))
+    return worst
+
+
+@pytest.mark.parametrize("Mq,Hq,Hkv,hd,nk1,nk2", [
+    (70, 4, 2, 64, 100, 40),       # GQA, ragged prompt keys, one split
+    (256, 2, 2, 128, 513, 256),    # several splits, ragged prompt
+    (16, 7, 1, 128, 1024, 512),    # GQA 7:1, many splits, few queries
+    (130, 3, 3, 64, 1, 8),         # a single prompt key
+])
+def test_attention_bf16_matches_oracle(Mq, Hq, Hkv, hd, nk1, nk2):
+    say(f"attention bf16 Mq={Mq} Hq={Hq} Hkv={Hkv} hd={hd} nk1={nk1} nk2={nk2}")
+    a = archer()
+    # bf16 probabilities in the P.V product and a bf16 output: |err| <~ 2^-8 max|v|
+    assert _attn_case(a.BF16, Mq, Hq, Hkv, hd, nk1, nk2, 11) < 2e-2
+
+
+@pytest.mark.parametrize("Mq,Hq,Hkv,hd,nk1,nk2", [(33, 4, 2, 64, 100, 40), (8, 2, 1, 128, 300, 64)])
+def test_attention_f32_matches_oracle(Mq, Hq, Hkv, hd, nk1, nk2):
+    say(f"attention fp32 Mq={Mq} Hq={Hq} Hkv={Hkv} hd={hd} nk1={nk1} nk2={nk2}")
+    a = archer()
+    assert _attn_case(a.FP32, Mq, Hq, Hkv, hd, nk1, nk2, 12) < 1e-5
+
+
+@pytest.mark.parametrize("Mq,Hq,Hkv,nk1,nk2", [
+    (256, 32, 32, 4096, 256),   # LLaDA-8B-shaped long-prompt cached step
+    (256, 32, 32, 512, 256),    # LLaDA-8B-shaped cached step
+    (512, 28, 4, 1024, 512),    # Dream-7B-shaped GQA cached step
+])
+def test_attention_full_size_sampled(Mq, Hq, Hkv, nk1, nk2):
+    say(f"attention full size Mq={Mq} Hq={Hq} Hkv={Hkv} nk1={nk1} nk2={nk2}")
+    a = archer()
+    rng = np.random.default_rng(1)
+    rows = np.sort(rng.choice(Mq, 24, replace=False))
+    heads = sorted(rng.choice(Hq, 4, replace=False).tolist())
+    assert _attn_case(a.BF16, Mq, Hq, Hkv, 128, nk1, nk2, 13, rows=rows, heads=heads) < 2e-2
