@@ -17,11 +17,14 @@
 extern "C" {
 #endif
 
-/* Y = A W^T (a projection of Sec. 4's transformer layer; the alpha_l work of
+/* Y = A W^T (a projection of the transformer layer; the alpha_l work of
  * Eq. theory-cost).  A: [M][K], W: [N][K], both of element type dtype,
- * row-major; Y: fp32 [M][N].  M >= 1; N and K multiples of 64. */
+ * row-major; Y: fp32 [M][N].  M >= 1; N and K multiples of 64.
+ * A_lo (bf16 only, may be NULL): low part of a two-term activation, so that
+ * A + A_lo carries about 16 significant bits; the product is then
+ * (A + A_lo) W^T, as in every projection of the bf16 model path. */
 archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void *A,
-                             const void *W, float *Y, void *hip_stream);
+                             const void *A_lo, const void *W, float *Y, void *hip_stream);
 
 /* Non-causal attention of one sequence over two key segments, the anchored
  * attention of Eq. archer-attention: every query of head h attends to the nk1

@@ -24,11 +24,14 @@ attention with query head h reading key/value head h // (Hq/Hkv); RoPE at
 absolute positions (prompt 0..P-1, response P..P+G-1).  The prompt K is
 cached after RoPE (positions never change, so this equals caching it before).
 
-bf16 models: the oracle rounds to bf16 where the bf16 path stores bf16
-operands -- the normalised activations entering each projection, the
-post-RoPE Q/K/V (hence the prompt cache), the attention output, the SwiGLU
-product and the final normalised hidden state.  The residual stream and the
-logits are not rounded.  fp32 models round nowhere.
+Precision (the paper fixes none).  bf16 models: weights are bf16, and the
+oracle rounds to bf16 exactly where the bf16 path stores single-bf16 values:
+the post-RoPE queries and keys and the values (hence the prompt cache).  The
+bf16 path carries every other activation (normalised inputs of the
+projections, attention output, SwiGLU product, final normalised hidden
+state) at about 16 significant bits, so the oracle keeps those unrounded;
+the residual stream and the logits are not rounded either.  fp32 models
+round nowhere.
 """
 
 from __future__ import annotations
@@ -71,7 +74,7 @@ def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
     for l in range(m.n_layers):
         Wl = W["layers"][l]
         # attention block
-        a = _rnd(m, rms_norm(x, Wl["attn_norm"], m.rms_eps))
+        a = rms_norm(x, Wl["attn_norm"], m.rms_eps)
         qkv = linear(a, Wl["w_qkv"])
         q = qkv[:, : hq * hd].reshape(n, hq, hd)
         k = qkv[:, hq * hd: (hq + hkv) * hd].reshape(n, hkv, hd)
@@ -90,17 +93,17 @@ def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
         o = np.empty((n, hq, hd))
         for h in range(hq):
             o[:, h, :] = attention(q[:, h, :], k_all[h // group], v_all[h // group])
-        o = _rnd(m, o.reshape(n, hq * hd))
+        o = o.reshape(n, hq * hd)
         x = x + linear(o, Wl["w_o"])
         # SwiGLU MLP block
-        b = _rnd(m, rms_norm(x, Wl["mlp_norm"], m.rms_eps))
+        b = rms_norm(x, Wl["mlp_norm"], m.rms_eps)
         gate = linear(b, Wl["w_gate"])
         up = linear(b, Wl["w_up"])
-        hmid = _rnd(m, silu(gate) * up)
+        hmid = silu(gate) * up
         x = x + linear(hmid, Wl["w_down"])
         if keep_hidden:
             hidden.append(x.copy())
-    c = _rnd(m, rms_norm(x[out_rows], W["final_norm"], m.rms_eps))
+    c = rms_norm(x[out_rows], W["final_norm"], m.rms_eps)
     z = linear(c, W["lm_head"])
     if keep_hidden:
         return z, kv, (np.stack(hidden), c)

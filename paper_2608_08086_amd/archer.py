@@ -93,7 +93,7 @@ lib.archer_destroy.argtypes = [P]
 lib.archer_last_error.restype = C.c_char_p
 lib.archer_last_error.argtypes = []
 lib.archer_op_gemm.restype = C.c_int
-lib.archer_op_gemm.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, P, P, P, P]
+lib.archer_op_gemm.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, P, P, P, P, P]
 lib.archer_op_attention_ws_bytes.restype = C.c_size_t
 lib.archer_op_attention_ws_bytes.argtypes = [C.c_int32] * 5
 lib.archer_op_attention.restype = C.c_int
@@ -264,11 +264,11 @@ def upload_weights(W: dict, dtype: str) -> dict:
 
 
 # -- single-kernel hooks of archer_ops.h --------------------------------------------------------
-def op_gemm(A, Wt, dtype=BF16):
+def op_gemm(A, Wt, dtype=BF16, A_lo=None):
     M, K = A.shape
     N = Wt.shape[0]
     Y = torch.empty(M, N, dtype=torch.float32, device="cuda")
-    _check(lib.archer_op_gemm(dtype, M, N, K, _ptr(A), _ptr(Wt), _ptr(Y), _stream()))
+    _check(lib.archer_op_gemm(dtype, M, N, K, _ptr(A), _ptr(A_lo), _ptr(Wt), _ptr(Y), _stream()))
     return Y
 
 

@@ -157,12 +157,13 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(SeqPlan pl, AttnArgs a) 
   if (!qval) return;
   // o[db][i]: dimension db*16 + 4*lg + i of query lc
   if (nsplit == 1) {
-    bf16* op = (bf16*)a.O + (size_t)qrow * a.ldo + h * HD;
+    const size_t ob = (size_t)qrow * a.ldo + h * HD;
     const float inv = 1.0f / l;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) op[db * 16 + lg * 4 + i] = (bf16)(o[db][i] * inv);
+      for (int i = 0; i < 4; ++i)
+        store_act<bf16>((bf16*)a.O, (bf16*)a.O2, ob + db * 16 + lg * 4 + i, o[db][i] * inv);
   } else {
     const size_t base = ((size_t)split * a.hq + h) * pl.rows + qrow;
     float* op = a.Opart + base * HD;

@@ -50,6 +50,17 @@ template <class T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
 
+// Two-term bf16 representation of an fp32 activation: v ~= hi + lo with
+// hi = bf16(v) and lo = bf16(v - hi), about 16 significant bits.  The bf16
+// GEMMs multiply both terms by the weights (two MFMAs), so activations keep
+// near-fp32 precision while every MFMA operand is bf16.
+template <class T>
+__device__ __forceinline__ void store_act(T* hi, T* lo, size_t i, float v) {
+  const T h = from_f32<T>(v);
+  hi[i] = h;
+  if (lo) lo[i] = from_f32<T>(v - to_f32(h));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);

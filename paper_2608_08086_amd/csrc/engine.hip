@@ -38,7 +38,7 @@ archer_status fail(archer_status s, const std::string& msg) {
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
-  size_t rope, Kc, Vtc, Kf, Vtf, x, act, Q, O, H, Cn, logits, Opart, ML;
+  size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML;
   size_t row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
   int ldcache, ldfresh, Mmax, Rmax, max_pos, ldq;
   size_t cache_layer_elems;
@@ -83,11 +83,17 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
   L.Kf = take((size_t)hkv * L.ldfresh * hd * esz);
   L.Vtf = take((size_t)hkv * L.ldfresh * hd * esz);
   L.x = take((size_t)L.Mmax * d * 4);
+  // bf16 activations feeding a GEMM are two-term (hi, lo); fp32 ones are single
+  const size_t lo = c->dtype == ARCHER_BF16 ? 1 : 0;
   L.act = take((size_t)L.Mmax * d * esz);
+  L.act2 = take(lo * L.Mmax * d * esz);
   L.Q = take((size_t)hq * L.ldq * hd * esz);
   L.O = take((size_t)L.Mmax * hq * hd * esz);
+  L.O2 = take(lo * L.Mmax * hq * hd * esz);
   L.H = take((size_t)L.Mmax * c->d_ff * esz);
+  L.H2 = take(lo * L.Mmax * c->d_ff * esz);
   L.Cn = take((size_t)L.Rmax * d * esz);
+  L.Cn2 = take(lo * L.Rmax * d * esz);
   L.logits = take((size_t)L.Rmax * c->vocab * 4);
   const size_t part_rows = c->dtype == ARCHER_BF16 ? (size_t)L.Mmax : 1;
   L.Opart = take((size_t)kMaxSplit * hq * part_rows * hd * 4);
@@ -147,6 +153,9 @@ namespace {
 
 bool is_bf16(const archer_ctx* c) { return c->cfg.dtype == ARCHER_BF16; }
 
+// low part of a two-term activation buffer (bf16 path only)
+void* lo_part(archer_ctx* c, size_t off) { return is_bf16(c) ? (void*)(c->ws + off) : nullptr; }
+
 template <class F>
 archer_status timed(archer_ctx* c, int cls, double bytes, double flops, F&& launch) {
   const bool rec = c->t_on && ((c->t_mask >> cls) & 1u);
@@ -203,10 +212,10 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
 
 archer_status gemm(archer_ctx* c, int cls, int epi, const GemmArgs& a) {
   const double es = (double)c->esz;
-  double bytes = (double)a.M * a.K * es + (double)a.N * a.K * es;
+  double bytes = (double)a.M * a.K * es * (a.A2 ? 2 : 1) + (double)a.N * a.K * es;
   if (epi == EPI_STORE) bytes += (double)a.M * a.N * 4;
   else if (epi == EPI_RESID) bytes += 2.0 * a.M * a.N * 4;
-  else if (epi == EPI_SWIGLU) bytes += (double)a.M * (a.N / 2) * es;
+  else if (epi == EPI_SWIGLU) bytes += (double)a.M * (a.N / 2) * es * (a.H2 ? 2 : 1);
   else bytes += (double)a.M * a.N * es;
   const double flops = 2.0 * a.M * a.N * a.K;
   return timed(c, cls, bytes, flops, [&] {
@@ -233,6 +242,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   const size_t es = c->esz;
   float* x = c->at<float>(L.x);
   void* act = c->at<char>(L.act);
+  void* act2 = lo_part(c, L.act2);
   int* row_pos = c->at<int>(L.row_pos);
   int* row_dst = c->at<int>(L.row_dst);
   archer_status st;
@@ -248,10 +258,12 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   });
   if (st) return st;
 
-  auto norm = [&](const float* gain, int gather, int nrows, void* out) {
-    return timed(c, ARCHER_K_NORM, (double)nrows * d * (4 + es), 0.0, [&] {
-      if (is_bf16(c)) launch_rmsnorm<bf16>(pl, gather, nrows, x, gain, out, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
-      else launch_rmsnorm<float>(pl, gather, nrows, x, gain, out, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
+  auto norm = [&](const float* gain, int gather, int nrows, void* out, void* out2) {
+    return timed(c, ARCHER_K_NORM, (double)nrows * d * (4 + es * (out2 ? 2 : 1)), 0.0, [&] {
+      if (is_bf16(c))
+        launch_rmsnorm<bf16>(pl, gather, nrows, x, gain, out, out2, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
+      else
+        launch_rmsnorm<float>(pl, gather, nrows, x, gain, out, out2, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
       return 0;
     });
   };
@@ -263,9 +275,10 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
     attn_q_keys += (double)(pl.row_off[s + 1] - pl.row_off[s]) * (pl.p_len[s] + pl.G);
 
   for (int l = 0; l < m.n_layers; ++l) {
-    if ((st = norm(c->attn_norm[l], 0, rows, act))) return st;
+    if ((st = norm(c->attn_norm[l], 0, rows, act, act2))) return st;
     {
       GemmArgs a = gargs(act, d, c->w_qkv[l], d, rows, qkv_n, d);
+      a.A2 = act2;
       a.Qb = c->at<char>(L.Q); a.ldq = L.ldq;
       a.Kc = c->at<char>(L.Kc) + (size_t)l * L.cache_layer_elems * es;
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
@@ -283,7 +296,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
       a.ldcache = L.ldcache;
       a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
-      a.O = c->at<char>(L.O); a.ldo = hq * hd;
+      a.O = c->at<char>(L.O); a.O2 = lo_part(c, L.O2); a.ldo = hq * hd;
       a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML);
       a.hq = hq; a.hkv = hkv; a.hd = hd;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
@@ -301,7 +314,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
           if (pl.nsplit[s] > 1)
             mbytes += (double)(pl.row_off[s + 1] - pl.row_off[s]) * hq * ((hd + 2) * 4.0 * pl.nsplit[s] + hd * es);
         st = timed(c, ARCHER_K_ATTN_MERGE, mbytes, 0.0, [&] {
-          launch_attn_merge<bf16>(pl, a.Opart, a.ML, a.O, hq, hd, a.ldo, c->stream);
+          launch_attn_merge<bf16>(pl, a.Opart, a.ML, a.O, a.O2, hq, hd, a.ldo, c->stream);
           return 0;
         });
         if (st) return st;
@@ -309,26 +322,30 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
     }
     {
       GemmArgs a = gargs(c->at<char>(L.O), hq * hd, c->w_o[l], hq * hd, rows, d, hq * hd);
+      a.A2 = lo_part(c, L.O2);
       a.X = x; a.ldx = d;
       if ((st = gemm(c, ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
     }
-    if ((st = norm(c->mlp_norm[l], 0, rows, act))) return st;
+    if ((st = norm(c->mlp_norm[l], 0, rows, act, act2))) return st;
     {
       GemmArgs a = gargs(act, d, c->w_gate[l], d, rows, 2 * F, d);
+      a.A2 = act2;
       a.W2 = c->w_up[l];
-      a.H = c->at<char>(L.H); a.ldh = F;
+      a.H = c->at<char>(L.H); a.H2 = lo_part(c, L.H2); a.ldh = F;
       if ((st = gemm(c, ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
     }
     {
       GemmArgs a = gargs(c->at<char>(L.H), F, c->w_down[l], F, rows, d, F);
+      a.A2 = lo_part(c, L.H2);
       a.X = x; a.ldx = d;
       if ((st = gemm(c, ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
     }
   }
   const int nresp = pl.n * pl.G;
-  if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn)))) return st;
+  if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn), lo_part(c, L.Cn2)))) return st;
   {
     GemmArgs a = gargs(c->at<char>(L.Cn), d, c->lm_head, d, nresp, m.vocab, d);
+    a.A2 = lo_part(c, L.Cn2);
     a.C = logits; a.ldc = m.vocab; a.out_row = c->at<int>(L.out_row);
     if ((st = gemm(c, ARCHER_K_GEMM_HEAD, EPI_STORE, a))) return st;
   }
@@ -618,11 +635,13 @@ archer_status archer_timing_end(archer_ctx* c, int64_t* launches, double* total_
 }
 
 // ---------------------------------------------------------------------------
-archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, const void* W, float* Y,
-                             void* hip_stream) {
+archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, const void* A_lo,
+                             const void* W, float* Y, void* hip_stream) {
   if (!A || !W || !Y) return fail(ARCHER_E_ARG, "null operand");
   if (M < 1 || N < 64 || K < 64 || N % 64 || K % 64) return fail(ARCHER_E_SHAPE, "need M >= 1 and N, K multiples of 64");
+  if (A_lo && dtype != ARCHER_BF16) return fail(ARCHER_E_ARG, "A_lo is only meaningful for bf16");
   GemmArgs a = gargs(A, K, W, K, M, N, K);
+  a.A2 = A_lo;
   a.C = Y; a.ldc = N;
   int rc;
   if (dtype == ARCHER_BF16) rc = launch_gemm_bf16(EPI_STORE, a, (hipStream_t)hip_stream);
@@ -677,7 +696,7 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
   int rc;
   if (dtype == ARCHER_BF16) {
     rc = launch_attn_bf16(p, a, st);
-    if (!rc && ns > 1) launch_attn_merge<bf16>(p, a.Opart, a.ML, O, Hq, hd, a.ldo, st);
+    if (!rc && ns > 1) launch_attn_merge<bf16>(p, a.Opart, a.ML, O, nullptr, Hq, hd, a.ldo, st);
   } else {
     rc = launch_attn_f32(p, a, ((nk1 + 63) & ~63) + nk2, st);
   }

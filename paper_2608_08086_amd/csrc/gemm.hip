@@ -39,7 +39,7 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int tile_n, int r, i
   if constexpr (EPI == EPI_SWIGLU) {
     const int f = tile_n * (BN / 2) + r;
     const float s = v1 / (1.0f + expf(-v1));
-    ((T*)a.H)[(size_t)row * a.ldh + f] = from_f32<T>(s * v2);
+    store_act<T>((T*)a.H, (T*)a.H2, (size_t)row * a.ldh + f, s * v2);
   } else if constexpr (EPI == EPI_QKV) {
     const int col0 = tile_n * BN;
     const int hd = a.hd;
@@ -86,22 +86,25 @@ __device__ __forceinline__ void epi_single(const GemmArgs& a, int row, int col, 
 constexpr bool epi_paired(int epi) { return epi == EPI_SWIGLU || epi == EPI_QKV; }
 
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int EPI>
+// SPLIT: A is the two-term activation (A = hi, A2 = lo); every fragment
+// product is issued twice, hi x W and lo x W, into the same fp32 accumulator.
+template <int BM, int BN, int EPI, bool SPLIT>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int BK = 64, LDK = BK + 8;
   constexpr int WM = BM / 4;
   constexpr int RB = WM / 16, CB = BN / 16;
   constexpr int A_CH = BM * BK / 8 / 256;
   constexpr int B_CH = BN * BK / 8 / 256;
+  constexpr int NA = SPLIT ? 2 : 1;
   static_assert(A_CH >= 1 && B_CH >= 1, "tile too small for 256 threads");
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) bf16 As[2][NA][BM * LDK];
   __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LDK];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int tile_n = blockIdx.x, m0 = blockIdx.y * BM;
-  const bf16* A = (const bf16*)a.A;
+  const bf16* Ap[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
 
-  const bf16* asrc[A_CH];
+  size_t aoffg[A_CH];
   bool aval[A_CH];
   int aoff[A_CH];
 #pragma unroll
@@ -109,7 +112,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     const int c = tid + 256 * j, r = c >> 3, kc = (c & 7) * 8;
     const int row = m0 + r;
     aval[j] = row < a.M;
-    asrc[j] = A + (size_t)(aval[j] ? row : 0) * a.lda + kc;
+    aoffg[j] = (size_t)(aval[j] ? row : 0) * a.lda + kc;
     aoff[j] = r * LDK + kc;
   }
   const bf16* bsrc[B_CH];
@@ -124,7 +127,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     boff[j] = r * LDK + kc;
   }
 
-  uint4 ra[A_CH], rbv[B_CH];
+  uint4 ra[NA][A_CH], rbv[B_CH];
   f32x4 acc[RB][CB];
 #pragma unroll
   for (int i = 0; i < RB; ++i)
@@ -133,13 +136,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
 
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int j = 0; j < A_CH; ++j) ra[j] = aval[j] ? *(const uint4*)(asrc[j] + k0) : make_uint4(0, 0, 0, 0);
+    for (int t = 0; t < NA; ++t)
+#pragma unroll
+      for (int j = 0; j < A_CH; ++j)
+        ra[t][j] = aval[j] ? *(const uint4*)(Ap[t] + aoffg[j] + k0) : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < B_CH; ++j) rbv[j] = *(const uint4*)(bsrc[j] + k0);
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int j = 0; j < A_CH; ++j) *(uint4*)&As[buf][aoff[j]] = ra[j];
+    for (int t = 0; t < NA; ++t)
+#pragma unroll
+      for (int j = 0; j < A_CH; ++j) *(uint4*)&As[buf][t][aoff[j]] = ra[t][j];
 #pragma unroll
     for (int j = 0; j < B_CH; ++j) *(uint4*)&Bs[buf][boff[j]] = rbv[j];
   };
@@ -153,18 +161,22 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
     if (kt + 1 < nk) gload((kt + 1) * BK);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 af[RB], bfr[CB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        af[rb] = *(const bf16x8*)&As[cur][(w * WM + rb * 16 + (lane & 15)) * LDK + ks * 32 + (lane >> 4) * 8];
+      bf16x8 bfr[CB];
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
         bfr[cb] = *(const bf16x8*)&Bs[cur][(cb * 16 + (lane & 15)) * LDK + ks * 32 + (lane >> 4) * 8];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
+      for (int t = 0; t < NA; ++t) {
+        bf16x8 af[RB];
 #pragma unroll
-        for (int cb = 0; cb < CB; ++cb)
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bfr[cb], acc[rb][cb], 0, 0, 0);
+        for (int rb = 0; rb < RB; ++rb)
+          af[rb] = *(const bf16x8*)&As[cur][t][(w * WM + rb * 16 + (lane & 15)) * LDK + ks * 32 + (lane >> 4) * 8];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bfr[cb], acc[rb][cb], 0, 0, 0);
+      }
     }
     if (kt + 1 < nk) sstore(cur ^ 1);
     __syncthreads();
@@ -193,7 +205,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
 template <int BM, int BN, int EPI>
 static void run_bf16(const GemmArgs& a, hipStream_t st) {
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM);
-  gemm_bf16_kernel<BM, BN, EPI><<<grid, 256, 0, st>>>(a);
+  if (a.A2) gemm_bf16_kernel<BM, BN, EPI, true><<<grid, 256, 0, st>>>(a);
+  else gemm_bf16_kernel<BM, BN, EPI, false><<<grid, 256, 0, st>>>(a);
 }
 
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st) {

@@ -77,7 +77,8 @@ template void launch_embed<bf16>(const SeqPlan&, const void*, int, int, int, con
 template <class T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, const float* __restrict__ x,
                                                       const float* __restrict__ gain, T* __restrict__ out,
-                                                      int d, float eps, int* __restrict__ out_row) {
+                                                      T* __restrict__ out2, int d, float eps,
+                                                      int* __restrict__ out_row) {
   __shared__ float red[16];
   const int ro = blockIdx.x;
   int ri = ro;
@@ -95,25 +96,26 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, co
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
   T* orow = out + (size_t)ro * d;
+  T* orow2 = out2 ? out2 + (size_t)ro * d : nullptr;
   for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
     const float4 v = *(const float4*)(xr + c);
     const float4 g = *(const float4*)(gain + c);
-    orow[c + 0] = from_f32<T>(v.x * inv * g.x);
-    orow[c + 1] = from_f32<T>(v.y * inv * g.y);
-    orow[c + 2] = from_f32<T>(v.z * inv * g.z);
-    orow[c + 3] = from_f32<T>(v.w * inv * g.w);
+    store_act<T>(orow, orow2, c + 0, v.x * inv * g.x);
+    store_act<T>(orow, orow2, c + 1, v.y * inv * g.y);
+    store_act<T>(orow, orow2, c + 2, v.z * inv * g.z);
+    store_act<T>(orow, orow2, c + 3, v.w * inv * g.w);
   }
 }
 
 template <class T>
 void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
-                    int d, float eps, int* out_row, hipStream_t st) {
-  rmsnorm_kernel<T><<<nrows, 256, 0, st>>>(pl, gather, x, gain, (T*)out, d, eps, out_row);
+                    void* out2, int d, float eps, int* out_row, hipStream_t st) {
+  rmsnorm_kernel<T><<<nrows, 256, 0, st>>>(pl, gather, x, gain, (T*)out, (T*)out2, d, eps, out_row);
 }
-template void launch_rmsnorm<float>(const SeqPlan&, int, int, const float*, const float*, void*, int, float,
-                                    int*, hipStream_t);
-template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const float*, void*, int, float,
-                                   int*, hipStream_t);
+template void launch_rmsnorm<float>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int,
+                                    float, int*, hipStream_t);
+template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int,
+                                   float, int*, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Decision pass 1: per response row, over the non-MASK vocabulary:
@@ -316,7 +318,7 @@ void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, cons
 // Rows of sequences attended in one split were written directly and are skipped.
 template <class T>
 __global__ void attn_merge_kernel(SeqPlan pl, const float* __restrict__ Op, const float* __restrict__ ML,
-                                  T* __restrict__ O, int hq, int hd, int ldo) {
+                                  T* __restrict__ O, T* __restrict__ O2, int hq, int hd, int ldo) {
   const int row = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
   const int nsplit = pl.nsplit[plan_find(pl.row_off, pl.n, row)];
   if (nsplit <= 1) return;
@@ -331,15 +333,15 @@ __global__ void attn_merge_kernel(SeqPlan pl, const float* __restrict__ Op, cons
     den += w * l;
     if (d < hd) num += w * Op[base * hd + d];
   }
-  if (d < hd) O[(size_t)row * ldo + h * hd + d] = from_f32<T>(num / den);
+  if (d < hd) store_act<T>(O, O2, (size_t)row * ldo + h * hd + d, num / den);
 }
 
 template <class T>
-void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, int hq, int hd, int ldo,
-                       hipStream_t st) {
-  attn_merge_kernel<T><<<dim3(pl.rows, hq), hd, 0, st>>>(pl, Op, ML, (T*)O, hq, hd, ldo);
+void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, void* O2, int hq, int hd,
+                       int ldo, hipStream_t st) {
+  attn_merge_kernel<T><<<dim3(pl.rows, hq), hd, 0, st>>>(pl, Op, ML, (T*)O, (T*)O2, hq, hd, ldo);
 }
-template void launch_attn_merge<float>(const SeqPlan&, const float*, const float*, void*, int, int, int,
+template void launch_attn_merge<float>(const SeqPlan&, const float*, const float*, void*, void*, int, int, int,
                                        hipStream_t);
-template void launch_attn_merge<bf16>(const SeqPlan&, const float*, const float*, void*, int, int, int,
+template void launch_attn_merge<bf16>(const SeqPlan&, const float*, const float*, void*, void*, int, int, int,
                                       hipStream_t);

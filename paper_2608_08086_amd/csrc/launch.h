@@ -14,11 +14,12 @@ enum GemmEpi {
 
 struct GemmArgs {
   const void* A; int lda;               // [M][K]
+  const void* A2;                       // optional low part of a two-term A (same layout), or null
   const void* W; const void* W2; int ldw; // [N][K] (SWIGLU: W = gate [F][K], W2 = up [F][K], N = 2F)
   int M, N, K;
   float* C; int ldc; const int* out_row; // EPI_STORE
   float* X; int ldx;                     // EPI_RESID
-  void* H; int ldh;                      // EPI_SWIGLU
+  void* H; void* H2; int ldh;            // EPI_SWIGLU: H = hi part, H2 = lo part (or null)
   // EPI_QKV
   void* Qb; int ldq;                     // Q [Hq][ldq][hd]
   void* Kc; void* Vtc; int ldcache;      // prompt cache of this layer: K [Hkv][ldcache][hd], Vt [Hkv][hd][ldcache]
@@ -31,7 +32,7 @@ struct AttnArgs {
   const void* Q; int ldq;                // [Hq][ldq][hd]
   const void* Kc; const void* Vtc; int ldcache;
   const void* Kf; const void* Vtf; int ldfresh;
-  void* O; int ldo;                      // [rows][ldo]
+  void* O; void* O2; int ldo;            // [rows][ldo]: hi part, lo part (or null)
   float* Opart; float* ML;               // split partials [max_split][Hq][rows][hd], [max_split][Hq][rows][2]
   int hq, hkv, hd;
   float scale_log2;                      // log2(e) / sqrt(hd)
@@ -48,7 +49,7 @@ void launch_embed(const SeqPlan& pl, const void* emb, int d, int V, int mask_id,
                   hipStream_t st);
 template <class T>
 void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
-                    int d, float eps, int* out_row, hipStream_t st);
+                    void* out2, int d, float eps, int* out_row, hipStream_t st);
 void launch_rowstats(int rows, const float* logits, int V, int mask_id, const int* g, int* xhat, float* ell,
                      float* qv, hipStream_t st);
 void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, const int* xhat, const float* ell,
@@ -56,8 +57,8 @@ void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, cons
                    int* dist, int* unmask_pos, int* remask_pos, int* tr_dist, int* tr_unmask, int* tr_utok,
                    int* tr_remask, hipStream_t st);
 template <class T>
-void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, int hq, int hd, int ldo,
-                       hipStream_t st);
+void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, void* O2, int hq, int hd,
+                       int ldo, hipStream_t st);
 
 // GEMM: returns 0 on success, nonzero if the shape is unsupported.
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);

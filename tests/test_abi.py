@@ -70,7 +70,7 @@ def test_workspace_bytes_and_host_side_errors():
     assert archer.lib.archer_init(None, None, None, None, 0, None, C.byref(h)) != 0
     assert archer.lib.archer_step(None, None, None, None) == archer.E_ARG
     assert archer.lib.archer_decode(None, 1, None, None, None, None, None) == archer.E_ARG
-    assert archer.lib.archer_op_gemm(archer.BF16, 0, 64, 64, None, None, None, None) == archer.E_ARG
+    assert archer.lib.archer_op_gemm(archer.BF16, 0, 64, 64, None, None, None, None, None) == archer.E_ARG
     # shape checks happen on the host before any launch (N not a multiple of 64)
-    assert archer.lib.archer_op_gemm(archer.BF16, 8, 60, 64, C.c_void_p(16), C.c_void_p(16), C.c_void_p(16),
-                                     None) == archer.E_SHAPE
+    assert archer.lib.archer_op_gemm(archer.BF16, 8, 60, 64, C.c_void_p(16), None, C.c_void_p(16),
+                                     C.c_void_p(16), None) == archer.E_SHAPE

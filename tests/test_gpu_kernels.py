@@ -38,6 +38,24 @@ def test_gemm_f32_matches_oracle(M, N, K):
     np.testing.assert_allclose(Y, on.linear(A64, W64), rtol=0, atol=1e-4)
 
 
+@pytest.mark.parametrize("M,N,K", [(37, 192, 320), (256, 512, 4096)])
+def test_gemm_two_term_activation_matches_oracle(M, N, K):
+    """A = hi + lo (bf16 pair of an fp32 activation) against the unrounded activation."""
+    say(f"gemm two-term bf16 M={M} N={N} K={K}")
+    a = archer()
+    import torch
+    from synth.gen import bf16_bits_to_f32, f32_to_bf16_bits, normal_tensor
+    A32 = normal_tensor((M, K), 9, 1, 1.0, "fp32")
+    hi = f32_to_bf16_bits(A32)
+    lo = f32_to_bf16_bits(A32 - bf16_bits_to_f32(hi))
+    W, W64 = rand_bf16((N, K), 9, 2)
+    dev = lambda u: torch.from_numpy(u.view(np.int16)).view(torch.bfloat16).cuda()  # noqa: E731
+    Y = host(a.op_gemm(dev(hi), W, a.BF16, A_lo=dev(lo)))
+    ref = on.linear(A32.astype(np.float64), W64)
+    # two-term residual ~2^-17 relative per element plus fp32 accumulation
+    np.testing.assert_allclose(Y, ref, rtol=0, atol=4e-5 * np.sqrt(K) * 4)
+
+
 def test_gemm_deterministic():
     a = archer()
     A, _ = rand_bf16((256, 4096), 7, 1)

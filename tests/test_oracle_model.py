@@ -43,7 +43,7 @@ def _loop_model(W, m, tokens, positions, out_rows):
     def norm(row, gain):
         ms = sum(v * v for v in row) / d
         r = 1.0 / math.sqrt(ms + m.rms_eps)
-        return [rnd(row[c] * r * float(gain[c])) for c in range(d)]
+        return [row[c] * r * float(gain[c]) for c in range(d)]
 
     def matvec(Wm, a):
         return [sum(Wm[o][c] * a[c] for c in range(len(a))) for o in range(len(Wm))]
@@ -75,12 +75,12 @@ def _loop_model(W, m, tokens, positions, out_rows):
                 mx = max(s)
                 p = [math.exp(t - mx) for t in s]
                 tot = sum(p)
-                o += [rnd(sum(p[j] / tot * V[j][kh][c] for j in range(n))) for c in range(hd)]
+                o += [sum(p[j] / tot * V[j][kh][c] for j in range(n)) for c in range(hd)]
             proj = matvec(wo, o)
             xi = [x[i][c] + proj[c] for c in range(d)]
             b = norm(xi, L["mlp_norm"])
             gate, up = matvec(wg, b), matvec(wu, b)
-            hmid = [rnd(gate[f] / (1.0 + math.exp(-gate[f])) * up[f]) for f in range(F)]
+            hmid = [gate[f] / (1.0 + math.exp(-gate[f])) * up[f] for f in range(F)]
             down = matvec(wd, hmid)
             newx.append([xi[c] + down[c] for c in range(d)])
         x = newx
