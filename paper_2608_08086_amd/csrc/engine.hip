@@ -39,7 +39,7 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
   size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML;
-  size_t row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
+  size_t part, row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
   int ldcache, ldfresh, Mmax, Rmax, max_pos, ldq;
   size_t cache_layer_elems;
 };
@@ -98,6 +98,17 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
   const size_t part_rows = c->dtype == ARCHER_BF16 ? (size_t)L.Mmax : 1;
   L.Opart = take((size_t)kMaxSplit * hq * part_rows * hd * 4);
   L.ML = take((size_t)kMaxSplit * hq * part_rows * 2 * 4);
+  // split-K partials of response-row launches: max over the projections of ksplit * N
+  size_t sn = 0;
+  if (c->dtype == ARCHER_BF16) {
+    const int F = c->d_ff, qkv = (hq + 2 * hkv) * hd;
+    const int NK[5][2] = {{qkv, d}, {d, hq * hd}, {2 * F, d}, {d, F}, {c->vocab, d}};
+    for (auto& nk : NK) {
+      const int S = gemm_ksplit(nk[0], nk[1]);
+      if (S > 1) sn = std::max(sn, (size_t)S * nk[0]);
+    }
+  }
+  L.part = take(sn * L.Rmax * 4);
   L.row_pos = take((size_t)L.Mmax * 4);
   L.row_dst = take((size_t)L.Mmax * 4);
   L.out_row = take((size_t)L.Rmax * 4);
@@ -210,7 +221,11 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
   return p;
 }
 
-archer_status gemm(archer_ctx* c, int cls, int epi, const GemmArgs& a) {
+archer_status gemm(archer_ctx* c, int cls, int epi, GemmArgs a) {
+  if (is_bf16(c)) {
+    a.ksplit = gemm_ksplit(a.N, a.K);
+    if (a.M <= c->L.Rmax) a.part = c->at<float>(c->L.part);
+  }
   const double es = (double)c->esz;
   double bytes = (double)a.M * a.K * es * (a.A2 ? 2 : 1) + (double)a.N * a.K * es;
   if (epi == EPI_STORE) bytes += (double)a.M * a.N * 4;
@@ -227,6 +242,7 @@ GemmArgs gargs(const void* A, int lda, const void* W, int ldw, int M, int N, int
   GemmArgs a;
   memset(&a, 0, sizeof(a));
   a.A = A; a.lda = lda; a.W = W; a.ldw = ldw; a.M = M; a.N = N; a.K = K;
+  a.ksplit = 1;
   return a;
 }
 
@@ -642,6 +658,7 @@ archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, con
   if (A_lo && dtype != ARCHER_BF16) return fail(ARCHER_E_ARG, "A_lo is only meaningful for bf16");
   GemmArgs a = gargs(A, K, W, K, M, N, K);
   a.A2 = A_lo;
+  if (dtype == ARCHER_BF16) a.ksplit = gemm_ksplit(N, K);
   a.C = Y; a.ldc = N;
   int rc;
   if (dtype == ARCHER_BF16) rc = launch_gemm_bf16(EPI_STORE, a, (hipStream_t)hip_stream);

@@ -1,20 +1,44 @@
 // Projection GEMMs Y = A W^T of the Archer path with fused epilogues.
 //
-// bf16: LDS-tiled MFMA kernel (v_mfma_f32_16x16x32_bf16, fp32 accumulate),
-//       256 threads = 4 wave64s stacked along M, BK = 64, double-buffered LDS.
-// fp32: FMA kernel with a 64x64 tile (tiny fp32 model and fp32 checks).
+// bf16 kernel: LDS-tiled MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulate),
+// 256 threads = 4 wave64s in a WGM x WGN grid, double-buffered LDS tiles in
+// an XOR-swizzled layout (16-byte chunk c of row r is stored at chunk
+// c ^ (r mod chunks-per-row): conflict-free fragment reads, no padding), and a
+// one-tile-ahead register prefetch of the global loads.
 //
-// Column pairing.  Two epilogues need two output columns of the same row in
-// one thread: RoPE rotates dimension j with j + hd/2 of a head, and SwiGLU
+// Split-K.  The K range of a GEMM is cut into S slices, S chosen from (N, K)
+// only.  A launch either gives each slice its own workgroup, which writes an
+// fp32 partial, and a second kernel sums the partials in slice order and
+// applies the epilogue; or runs all slices in one workgroup, accumulating each
+// slice from zero and adding the slice sums in the same order.  Both give the
+// same bits, so a row's result never depends on how many rows are in the
+// launch (CachedForward on its own cache equals FullForward bitwise).
+//
+// Column pairing.  RoPE rotates dimension j with j + hd/2 of a head, SwiGLU
 // multiplies gate feature f with up feature f.  The B tile rows (weight rows)
-// are gathered so that tile column r and r + BN/2 form such a pair:
-//   QKV (q and k heads): columns {h*hd + j0 + c} and {h*hd + hd/2 + j0 + c},
-//                        c < BN/2, j0 = (tile offset within the head) * BN/2;
-//   SWIGLU:              gate rows f0 + c and up rows f0 + c, f0 = tile * BN/2.
+// are gathered so that tile column r and r + BN/2 form such a pair, and each
+// wave's columns are taken from both halves of the tile so that a pair sits in
+// one lane:
+//   QKV:    columns {h*hd + j0 + c} and {h*hd + hd/2 + j0 + c}, c < BN/2,
+//           j0 = (tile offset within the head) * BN/2  (all of q, k and v);
+//   SWIGLU: gate rows f0 + c and up rows f0 + c, f0 = tile * BN/2.
+//
+// Tile order.  Workgroups are dispatched round-robin over the 8 XCDs.  The
+// linear workgroup id is laid out so that all M tiles of one (N tile, slice)
+// group run on the same XCD back to back (the weight tile is read from HBM
+// once and then hits that XCD's L2) and, with 8 slices, each XCD owns one K
+// slice (its slice of A stays in its L2).
+#include <algorithm>
+
 #include "launch.h"
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+namespace {
+
+// weight row of tile column r; *second = the row is in W2 (SWIGLU up rows)
 template <int EPI, int BN>
-__device__ __forceinline__ int64_t brow_index(const GemmArgs& a, int tile_n, int r, bool* second) {
+__device__ __forceinline__ int brow_index(const GemmArgs& a, int tile_n, int r, bool* second) {
   *second = false;
   if constexpr (EPI == EPI_SWIGLU) {
     const int f0 = tile_n * (BN / 2);
@@ -23,207 +47,390 @@ __device__ __forceinline__ int64_t brow_index(const GemmArgs& a, int tile_n, int
     return f0 + r - BN / 2;
   } else if constexpr (EPI == EPI_QKV) {
     const int col0 = tile_n * BN;
-    if (col0 < (a.hq + a.hkv) * a.hd) {
-      const int base = (col0 / a.hd) * a.hd;
-      const int j0 = ((col0 % a.hd) / BN) * (BN / 2);
-      return r < BN / 2 ? base + j0 + r : base + a.hd / 2 + j0 + (r - BN / 2);
-    }
-    return col0 + r;
+    const int base = (col0 / a.hd) * a.hd;
+    const int j0 = ((col0 % a.hd) / BN) * (BN / 2);
+    return r < BN / 2 ? base + j0 + r : base + a.hd / 2 + j0 + (r - BN / 2);
   } else {
-    return (int64_t)tile_n * BN + r;
+    return tile_n * BN + r;
   }
 }
 
-template <int EPI, class T, int BN>
-__device__ __forceinline__ void epi_pair(const GemmArgs& a, int tile_n, int r, int row, float v1, float v2) {
-  if constexpr (EPI == EPI_SWIGLU) {
-    const int f = tile_n * (BN / 2) + r;
-    const float s = v1 / (1.0f + expf(-v1));
-    store_act<T>((T*)a.H, (T*)a.H2, (size_t)row * a.ldh + f, s * v2);
-  } else if constexpr (EPI == EPI_QKV) {
-    const int col0 = tile_n * BN;
-    const int hd = a.hd;
-    const int qk_end = (a.hq + a.hkv) * hd;
-    const int dst = a.row_dst[row];
-    if (col0 < qk_end) {
-      const int head = col0 / hd;
-      const int j = ((col0 % hd) / BN) * (BN / 2) + r;
-      const float2 cs = a.rope[(size_t)a.row_pos[row] * (hd / 2) + j];
-      const float o1 = v1 * cs.x - v2 * cs.y;
-      const float o2 = v2 * cs.x + v1 * cs.y;
-      T* p;
-      if (head < a.hq) {
-        p = (T*)a.Qb + ((size_t)head * a.ldq + row) * hd;
-      } else if (dst_is_fresh(dst)) {
-        p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * hd;
-      } else {
-        p = (T*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * hd;
-      }
-      p[j] = from_f32<T>(o1);
-      p[j + hd / 2] = from_f32<T>(o2);
-    } else {
-      const int c1 = col0 - qk_end + r, c2 = c1 + BN / 2;
-      T* vt;
-      int ld, col;
-      if (dst_is_fresh(dst)) { vt = (T*)a.Vtf; ld = a.ldfresh; col = dst; }
-      else { vt = (T*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
-      vt[(size_t)c1 * ld + col] = from_f32<T>(v1);   // (vh*hd + d) == c
-      vt[(size_t)c2 * ld + col] = from_f32<T>(v2);
-    }
-  }
+// ---- epilogues on logical (global) columns ----------------------------------
+__device__ __forceinline__ void epi_store(const GemmArgs& a, int row, int col, float v) {
+  const int orow = a.out_row ? a.out_row[row] : row;
+  a.C[(size_t)orow * a.ldc + col] = v;
 }
 
-template <int EPI>
-__device__ __forceinline__ void epi_single(const GemmArgs& a, int row, int col, float v) {
-  if constexpr (EPI == EPI_STORE) {
-    const int orow = a.out_row ? a.out_row[row] : row;
-    a.C[(size_t)orow * a.ldc + col] = v;
-  } else if constexpr (EPI == EPI_RESID) {
-    a.X[(size_t)row * a.ldx + col] += v;
+__device__ __forceinline__ void epi_resid(const GemmArgs& a, int row, int col, float v) {
+  a.X[(size_t)row * a.ldx + col] += v;
+}
+
+template <class T>
+__device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int f, float g, float u) {
+  const float s = g / (1.0f + expf(-g));
+  store_act<T>((T*)a.H, (T*)a.H2, (size_t)row * a.ldh + f, s * u);
+}
+
+// head in [0, hq + 2 hkv): q heads, k heads, v heads; v1 / v2 = dims j, j + hd/2
+template <class T>
+__device__ __forceinline__ void epi_qkv(const GemmArgs& a, int row, int head, int j, float v1, float v2) {
+  const int hd = a.hd;
+  const int dst = a.row_dst[row];
+  if (head < a.hq + a.hkv) {
+    const float2 cs = a.rope[(size_t)a.row_pos[row] * (hd / 2) + j];
+    const float o1 = v1 * cs.x - v2 * cs.y;
+    const float o2 = v2 * cs.x + v1 * cs.y;
+    T* p;
+    if (head < a.hq) p = (T*)a.Qb + ((size_t)head * a.ldq + row) * hd;
+    else if (dst_is_fresh(dst)) p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * hd;
+    else p = (T*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * hd;
+    p[j] = from_f32<T>(o1);
+    p[j + hd / 2] = from_f32<T>(o2);
+  } else {
+    const int vh = head - a.hq - a.hkv;
+    T* vt;
+    int ld, col;
+    if (dst_is_fresh(dst)) { vt = (T*)a.Vtf; ld = a.ldfresh; col = dst; }
+    else { vt = (T*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
+    vt[((size_t)vh * hd + j) * ld + col] = from_f32<T>(v1);
+    vt[((size_t)vh * hd + j + hd / 2) * ld + col] = from_f32<T>(v2);
   }
 }
 
 constexpr bool epi_paired(int epi) { return epi == EPI_SWIGLU || epi == EPI_QKV; }
 
+// Fused epilogue of one pair of tile columns (r, r + BN/2) or single column r.
+template <int EPI, class T, int BN>
+__device__ __forceinline__ void epi_tile_pair(const GemmArgs& a, int tile_n, int r, int row, float v1, float v2) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    epi_swiglu<T>(a, row, tile_n * (BN / 2) + r, v1, v2);
+  } else if constexpr (EPI == EPI_QKV) {
+    const int col0 = tile_n * BN;
+    epi_qkv<T>(a, row, col0 / a.hd, ((col0 % a.hd) / BN) * (BN / 2) + r, v1, v2);
+  }
+}
+
+// logical column of tile column r in the [S][M][N] partial buffer
+template <int EPI, int BN>
+__device__ __forceinline__ int logical_col(const GemmArgs& a, int tile_n, int r) {
+  bool second;
+  const int w = brow_index<EPI, BN>(a, tile_n, r, &second);
+  return second ? w + a.N / 2 : w;
+}
+
+// XCD-aware decomposition of the linear workgroup id (see the file comment).
+__device__ __forceinline__ bool tile_of(int id, int n_tiles, int m_tiles, int S, int* tn, int* tm, int* z) {
+  const int groups = n_tiles * S;
+  const int g8 = id % 8, rest = id / 8;
+  const int gblk = rest / m_tiles, m = rest % m_tiles;
+  const int group = gblk * 8 + g8;
+  if (group >= groups) return false;
+  *tn = group / S;
+  *z = group % S;
+  *tm = m;
+  return true;
+}
+
+}  // namespace
+
+int gemm_grid_size(int n_tiles, int m_tiles, int S) { return ((n_tiles * S + 7) / 8) * 8 * m_tiles; }
+
+#define GEMM_GLOAD(slot, k0)                                                             \
+  do {                                                                                   \
+    _Pragma("unroll") for (int t = 0; t < NA; ++t)                                       \
+      _Pragma("unroll") for (int j = 0; j < A_CH; ++j)                                   \
+        RA##slot[t][j] = *(const u32x4*)(Ap[t] + aoffg[j] + (k0));                       \
+    _Pragma("unroll") for (int j = 0; j < B_CH; ++j) RB##slot[j] = *(const u32x4*)(bsrc[j] + (k0)); \
+  } while (0)
+#define GEMM_SSTORE(slot, buf)                                                           \
+  do {                                                                                   \
+    _Pragma("unroll") for (int t = 0; t < NA; ++t)                                       \
+      _Pragma("unroll") for (int j = 0; j < A_CH; ++j) *(u32x4*)&As[buf][t][aoff[j]] = RA##slot[t][j]; \
+    _Pragma("unroll") for (int j = 0; j < B_CH; ++j) *(u32x4*)&Bs[buf][boff[j]] = RB##slot[j]; \
+  } while (0)
+#define GEMM_COMPUTE(cur)                                                                \
+  do {                                                                                   \
+    _Pragma("unroll") for (int ks = 0; ks < BK / 32; ++ks) {                             \
+      const int ch = ks * 4 + lg;                                                        \
+      bf16x8 bfr[CB];                                                                    \
+      _Pragma("unroll") for (int cb = 0; cb < CB; ++cb)                                  \
+        bfr[cb] = *(const bf16x8*)&Bs[cur][tc[cb] * BK + ((ch ^ (tc[cb] % CPR)) * 8)];  \
+      _Pragma("unroll") for (int t = 0; t < NA; ++t) {                                   \
+        bf16x8 af[RB];                                                                   \
+        _Pragma("unroll") for (int rb = 0; rb < RB; ++rb) {                              \
+          const int r_ = wm * WM + rb * 16 + lc;                                         \
+          af[rb] = *(const bf16x8*)&As[cur][t][r_ * BK + ((ch ^ (r_ % CPR)) * 8)];       \
+        }                                                                                \
+        _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                                \
+          _Pragma("unroll") for (int cb = 0; cb < CB; ++cb)                              \
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bfr[cb], acc[rb][cb], 0, 0, 0); \
+      }                                                                                  \
+    }                                                                                    \
+  } while (0)
+
 // ---------------------------------------------------------------------------
 // SPLIT: A is the two-term activation (A = hi, A2 = lo); every fragment
-// product is issued twice, hi x W and lo x W, into the same fp32 accumulator.
-template <int BM, int BN, int EPI, bool SPLIT>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a) {
-  constexpr int BK = 64, LDK = BK + 8;
-  constexpr int WM = BM / 4;
-  constexpr int RB = WM / 16, CB = BN / 16;
-  constexpr int A_CH = BM * BK / 8 / 256;
-  constexpr int B_CH = BN * BK / 8 / 256;
+// product is issued twice, hi x W and lo x W, into the same accumulator.
+// MODE 0: one workgroup covers all of K in one accumulation (ksplit == 1).
+// MODE 1: one workgroup covers all ksplit slices, each accumulated from zero
+//         and added to the running total in slice order.
+// MODE 2: one workgroup per slice, writing an fp32 partial.
+template <int BM, int BN, int BK, int WGM, int WGN, int EPI, bool SPLIT, int MODE>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
+  constexpr int WM = BM / WGM, WN = BN / WGN;
+  constexpr int RB = WM / 16, CB = WN / 16;
+  constexpr int CPR = BK / 8;                       // 16-byte chunks per tile row
+  constexpr int A_CH = BM * CPR / 256, B_CH = BN * CPR / 256;
   constexpr int NA = SPLIT ? 2 : 1;
-  static_assert(A_CH >= 1 && B_CH >= 1, "tile too small for 256 threads");
-  __shared__ __attribute__((aligned(16))) bf16 As[2][NA][BM * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LDK];
+  constexpr bool PARTIAL = MODE == 2, FOLD = MODE == 1;
+  static_assert(WGM * WGN == 4 && A_CH >= 1 && B_CH >= 1 && CB % 2 == 0 && RB >= 1, "bad tile");
+  static_assert(BN % (32 * WGN) == 0, "each wave takes 16-column blocks from both tile halves");
+  __shared__ __attribute__((aligned(16))) bf16 As[2][NA][BM * BK];
+  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * BK];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int tile_n = blockIdx.x, m0 = blockIdx.y * BM;
+  const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
+  int tile_n, tile_m, z;
+  if (!tile_of(blockIdx.x, n_tiles, m_tiles, PARTIAL ? a.ksplit : 1, &tile_n, &tile_m, &z)) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int wm = w / WGN, wn = w % WGN;
+  const int m0 = tile_m * BM;
+  const int kslice = a.K / a.ksplit;
+  const int kbeg = PARTIAL ? z * kslice : 0;
+  const int nslices = FOLD ? a.ksplit : 1;
+  const int kt_slice = (PARTIAL || FOLD ? kslice : a.K) / BK;   // k tiles per accumulation
   const bf16* Ap[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
 
-  size_t aoffg[A_CH];
-  bool aval[A_CH];
-  int aoff[A_CH];
+  // rows past M load row M-1 (finite data; those output rows are never stored)
+  uint32_t aoffg[A_CH], aoff[A_CH];
 #pragma unroll
   for (int j = 0; j < A_CH; ++j) {
-    const int c = tid + 256 * j, r = c >> 3, kc = (c & 7) * 8;
-    const int row = m0 + r;
-    aval[j] = row < a.M;
-    aoffg[j] = (size_t)(aval[j] ? row : 0) * a.lda + kc;
-    aoff[j] = r * LDK + kc;
+    const int c = tid + 256 * j, r = c / CPR, kc = c % CPR;
+    const int row = min(m0 + r, a.M - 1);
+    aoffg[j] = (uint32_t)row * a.lda + kc * 8;
+    aoff[j] = r * BK + ((kc ^ (r % CPR)) * 8);
   }
   const bf16* bsrc[B_CH];
-  int boff[B_CH];
+  uint32_t boff[B_CH];
 #pragma unroll
   for (int j = 0; j < B_CH; ++j) {
-    const int c = tid + 256 * j, r = c >> 3, kc = (c & 7) * 8;
+    const int c = tid + 256 * j, r = c / CPR, kc = c % CPR;
     bool second;
-    const int64_t wr = brow_index<EPI, BN>(a, tile_n, r, &second);
-    const bf16* base = (const bf16*)(second ? a.W2 : a.W);
-    bsrc[j] = base + wr * a.ldw + kc;
-    boff[j] = r * LDK + kc;
+    const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
+    bsrc[j] = (const bf16*)(second ? a.W2 : a.W) + (size_t)wr * a.ldw + kc * 8;
+    boff[j] = r * BK + ((kc ^ (r % CPR)) * 8);
   }
+  // tile column of accumulator block cb: blocks 0..CB/2-1 from the first tile
+  // half, CB/2..CB-1 the partner columns from the second half
+  int tc[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) tc[cb] = (cb / (CB / 2)) * (BN / 2) + wn * (WN / 2) + (cb % (CB / 2)) * 16 + lc;
 
-  uint4 ra[NA][A_CH], rbv[B_CH];
+  u32x4 RA0[NA][A_CH], RB0[B_CH], RA1[NA][A_CH], RB1[B_CH];   // two tiles of prefetch in flight
   f32x4 acc[RB][CB];
+  f32x4 tot[FOLD ? RB : 1][FOLD ? CB : 1];
+  if constexpr (FOLD) {
 #pragma unroll
-  for (int i = 0; i < RB; ++i)
+    for (int i = 0; i < RB; ++i)
 #pragma unroll
-    for (int j = 0; j < CB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int t = 0; t < NA; ++t)
-#pragma unroll
-      for (int j = 0; j < A_CH; ++j)
-        ra[t][j] = aval[j] ? *(const uint4*)(Ap[t] + aoffg[j] + k0) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int j = 0; j < B_CH; ++j) rbv[j] = *(const uint4*)(bsrc[j] + k0);
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int t = 0; t < NA; ++t)
-#pragma unroll
-      for (int j = 0; j < A_CH; ++j) *(uint4*)&As[buf][t][aoff[j]] = ra[t][j];
-#pragma unroll
-    for (int j = 0; j < B_CH; ++j) *(uint4*)&Bs[buf][boff[j]] = rbv[j];
-  };
-
-  const int nk = a.K / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 bfr[CB];
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb)
-        bfr[cb] = *(const bf16x8*)&Bs[cur][(cb * 16 + (lane & 15)) * LDK + ks * 32 + (lane >> 4) * 8];
-#pragma unroll
-      for (int t = 0; t < NA; ++t) {
-        bf16x8 af[RB];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          af[rb] = *(const bf16x8*)&As[cur][t][(w * WM + rb * 16 + (lane & 15)) * LDK + ks * 32 + (lane >> 4) * 8];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-          for (int cb = 0; cb < CB; ++cb)
-            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bfr[cb], acc[rb][cb], 0, 0, 0);
-      }
-    }
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
+      for (int j = 0; j < CB; ++j) tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // accumulator (rb, cb)[i] holds row 16*rb + 4*(lane/16) + i, column 16*cb + lane%16
+  // Pipeline: LDS buffer b holds tile g (b = g & 1), register slot (g + 1) & 1
+  // holds tile g + 1 in flight; iteration g issues tile g + 2 into slot g & 1,
+  // computes tile g, then moves tile g + 1 from its slot into LDS buffer b ^ 1.
+  // Tile indices past the last tile are clamped (a redundant load whose LDS
+  // copy is never read).  Tiles per accumulation are even (host-checked), so
+  // the parity of g is static in the two unrolled halves.
+  const int ntot = nslices * kt_slice;
+#define kof(g) (kbeg + min((g), ntot - 1) * BK)
+  GEMM_GLOAD(0, kof(0));
+  GEMM_GLOAD(1, kof(1));
+  GEMM_SSTORE(0, 0);
+  __syncthreads();
+  for (int sl = 0; sl < nslices; ++sl) {
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < CB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kt = 0; kt < kt_slice; kt += 2) {
+      const int g = sl * kt_slice + kt;             // even
+      GEMM_GLOAD(0, kof(g + 2));
+      GEMM_COMPUTE(0);
+      GEMM_SSTORE(1, 1);
+      __syncthreads();
+      GEMM_GLOAD(1, kof(g + 3));
+      GEMM_COMPUTE(1);
+      GEMM_SSTORE(0, 0);
+      __syncthreads();
+    }
+    if constexpr (FOLD) {
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < CB; ++j) tot[i][j] += acc[i][j];
+    }
+  }
+
+  // accumulator (rb, cb)[i]: row wm*WM + 16*rb + 4*lg + i, tile column tc[cb]
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = m0 + w * WM + rb * 16 + (lane >> 4) * 4 + i;
+      const int row = m0 + wm * WM + rb * 16 + lg * 4 + i;
       if (row >= a.M) continue;
-      if constexpr (epi_paired(EPI)) {
+      if constexpr (PARTIAL) {
+        float* pr = a.part + ((size_t)z * a.M + row) * a.N;
 #pragma unroll
-        for (int cb = 0; cb < CB / 2; ++cb)
-          epi_pair<EPI, bf16, BN>(a, tile_n, cb * 16 + (lane & 15), row, acc[rb][cb][i], acc[rb][cb + CB / 2][i]);
+        for (int cb = 0; cb < CB; ++cb) pr[logical_col<EPI, BN>(a, tile_n, tc[cb])] = acc[rb][cb][i];
+      } else if constexpr (epi_paired(EPI)) {
+#pragma unroll
+        for (int cb = 0; cb < CB / 2; ++cb) epi_tile_pair<EPI, bf16, BN>(a, tile_n, tc[cb], row, FOLD ? tot[rb % (FOLD ? RB : 1)][cb % (FOLD ? CB : 1)][i] : acc[rb][cb][i],
+                                         FOLD ? tot[rb % (FOLD ? RB : 1)][(cb + CB / 2) % (FOLD ? CB : 1)][i] : acc[rb][cb + CB / 2][i]);
       } else {
 #pragma unroll
-        for (int cb = 0; cb < CB; ++cb)
-          epi_single<EPI>(a, row, tile_n * BN + cb * 16 + (lane & 15), acc[rb][cb][i]);
+        for (int cb = 0; cb < CB; ++cb) {
+          const int col = tile_n * BN + tc[cb];
+          const float v = FOLD ? tot[rb % (FOLD ? RB : 1)][cb % (FOLD ? CB : 1)][i] : acc[rb][cb][i];
+          if constexpr (EPI == EPI_STORE) epi_store(a, row, col, v);
+          else epi_resid(a, row, col, v);
+        }
       }
     }
   }
 }
 
-template <int BM, int BN, int EPI>
-static void run_bf16(const GemmArgs& a, hipStream_t st) {
-  dim3 grid(a.N / BN, (a.M + BM - 1) / BM);
-  if (a.A2) gemm_bf16_kernel<BM, BN, EPI, true><<<grid, 256, 0, st>>>(a);
-  else gemm_bf16_kernel<BM, BN, EPI, false><<<grid, 256, 0, st>>>(a);
+// Sum of the S partials in slice order, then the epilogue.  One thread per
+// (row, logical pair) for SWIGLU / QKV, per (row, column) otherwise.
+template <int EPI, class T>
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
+  const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)a.M * npair) return;
+  const int row = (int)(idx / npair), p = (int)(idx % npair);
+  const size_t plane = (size_t)a.M * a.N;
+  const float* pr = a.part + (size_t)row * a.N;
+  if constexpr (EPI == EPI_SWIGLU) {
+    const int F = a.N / 2;
+    float g = pr[p], u = pr[F + p];
+    for (int s = 1; s < a.ksplit; ++s) { g += pr[s * plane + p]; u += pr[s * plane + F + p]; }
+    epi_swiglu<T>(a, row, p, g, u);
+  } else if constexpr (EPI == EPI_QKV) {
+    const int half = a.hd / 2, head = p / half, j = p % half;
+    const int c1 = head * a.hd + j, c2 = c1 + half;
+    float v1 = pr[c1], v2 = pr[c2];
+    for (int s = 1; s < a.ksplit; ++s) { v1 += pr[s * plane + c1]; v2 += pr[s * plane + c2]; }
+    epi_qkv<T>(a, row, head, j, v1, v2);
+  } else {
+    float v = pr[p];
+    for (int s = 1; s < a.ksplit; ++s) v += pr[s * plane + p];
+    if constexpr (EPI == EPI_STORE) epi_store(a, row, p, v);
+    else epi_resid(a, row, p, v);
+  }
 }
 
-int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st) {
-  constexpr int BM = 128, BN = 64;
-  if (a.M <= 0 || a.N % BN || a.K % 64) return 1;
-  if (epi == EPI_QKV && (a.hd % BN)) return 1;
+// ---------------------------------------------------------------------------
+namespace {
+
+template <int BM, int BN, int BK, int WGM, int WGN, int EPI, int MODE>
+void run_mode(const GemmArgs& a, int grid, hipStream_t st) {
+  if (a.A2) gemm_bf16_kernel<BM, BN, BK, WGM, WGN, EPI, true, MODE><<<grid, 256, 0, st>>>(a);
+  else gemm_bf16_kernel<BM, BN, BK, WGM, WGN, EPI, false, MODE><<<grid, 256, 0, st>>>(a);
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, int EPI>
+void run_cfg(const GemmArgs& a, bool partial, hipStream_t st) {
+  const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
+  const int grid = gemm_grid_size(n_tiles, m_tiles, partial ? a.ksplit : 1);
+  if (partial) {
+    run_mode<BM, BN, BK, WGM, WGN, EPI, 2>(a, grid, st);
+    const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
+    const long total = (long)a.M * npair;
+    gemm_reduce_kernel<EPI, bf16><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(a);
+  } else if (a.ksplit > 1) {
+    run_mode<BM, BN, BK, WGM, WGN, EPI, 1>(a, grid, st);
+  } else {
+    run_mode<BM, BN, BK, WGM, WGN, EPI, 0>(a, grid, st);
+  }
+}
+
+template <int EPI>
+void run_epi(int cfg, const GemmArgs& a, bool partial, hipStream_t st) {
+  switch (cfg) {
+    case 0: run_cfg<128, 128, 64, 2, 2, EPI>(a, partial, st); break;
+    case 1: run_cfg<256, 128, 32, 2, 2, EPI>(a, partial, st); break;
+    case 2: run_cfg<128, 64, 64, 4, 1, EPI>(a, partial, st); break;
+    case 3: run_cfg<256, 64, 64, 4, 1, EPI>(a, partial, st); break;
+    case 4: run_cfg<64, 128, 64, 1, 4, EPI>(a, partial, st); break;
+    case 5: run_cfg<64, 128, 32, 1, 4, EPI>(a, partial, st); break;
+    default: run_cfg<128, 64, 32, 4, 1, EPI>(a, partial, st); break;
+  }
+}
+
+const int kCfgBN[GEMM_NCFG] = {128, 128, 64, 64, 128, 128, 64};
+const int kCfgBK[GEMM_NCFG] = {64, 32, 64, 64, 64, 32, 32};
+const int kCfgBM[GEMM_NCFG] = {128, 256, 128, 256, 64, 64, 128};
+
+}  // namespace
+
+int gemm_ksplit(int N, int K) {
+  // slice count from (N, K) only: enough slices that a 256-row launch of
+  // 128 x 128 tiles fills the 256 CUs, within the K granularity
+  const int tiles = 2 * std::max(N / 128, 1);
+  int S = 1;
+  while (S < 8 && tiles * S < 256 && K % (2 * S * 64) == 0) S *= 2;
+  return S;
+}
+
+int gemm_pick_cfg(const GemmArgs& a, int epi) {
+  // measured on MI355X (LLaDA-8B cached step and refresh shapes): the 64 x 128
+  // tile with four waves side by side is fastest up to M = 1024 rows
+  const bool bn128 = a.N % 128 == 0 && (epi != EPI_QKV || a.hd % 128 == 0) &&
+                     (epi != EPI_SWIGLU || (a.N / 2) % 64 == 0);
+  const bool bk64 = a.K % (2 * a.ksplit * 64) == 0;   // even number of 64-wide k tiles per slice
+  if (bn128) {
+    if (!bk64) return 5;
+    return a.M <= 1024 ? 4 : 0;
+  }
+  if (!bk64) return 6;
+  return a.M <= 1024 ? 2 : 3;
+}
+
+bool gemm_cfg_ok(int cfg, const GemmArgs& a, int epi) {
+  if (cfg < 0 || cfg >= GEMM_NCFG) return false;
+  const int BN = kCfgBN[cfg];
+  if (a.M <= 0 || a.N % BN || a.ksplit < 1 || a.K % (2 * a.ksplit * kCfgBK[cfg])) return false;
+  if (epi == EPI_QKV && (a.hd % BN)) return false;
+  if (epi == EPI_SWIGLU && ((a.N / 2) % (BN / 2))) return false;
+  return true;
+}
+
+int gemm_partial_wanted(int cfg, const GemmArgs& a) {
+  const int tiles = (a.N / kCfgBN[cfg]) * ((a.M + kCfgBM[cfg] - 1) / kCfgBM[cfg]);
+  return a.ksplit > 1 && tiles < 512;
+}
+
+int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st) {
+  if (!gemm_cfg_ok(cfg, a, epi)) return 1;
+  if (partial && (!a.part || a.ksplit < 2)) return 1;
   switch (epi) {
-    case EPI_STORE: run_bf16<BM, BN, EPI_STORE>(a, st); break;
-    case EPI_RESID: run_bf16<BM, BN, EPI_RESID>(a, st); break;
-    case EPI_SWIGLU: run_bf16<BM, BN, EPI_SWIGLU>(a, st); break;
-    case EPI_QKV: run_bf16<BM, BN, EPI_QKV>(a, st); break;
+    case EPI_STORE: run_epi<EPI_STORE>(cfg, a, partial, st); break;
+    case EPI_RESID: run_epi<EPI_RESID>(cfg, a, partial, st); break;
+    case EPI_SWIGLU: run_epi<EPI_SWIGLU>(cfg, a, partial, st); break;
+    case EPI_QKV: run_epi<EPI_QKV>(cfg, a, partial, st); break;
     default: return 1;
   }
   return 0;
 }
 
+int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st) {
+  const int cfg = gemm_pick_cfg(a, epi);
+  const bool partial = a.part != nullptr && gemm_partial_wanted(cfg, a);
+  return launch_gemm_bf16_cfg(epi, cfg, partial, a, st);
+}
+
 // ---------------------------------------------------------------------------
+// fp32 kernel: 64 x 64 tile, BK 16; thread (tx, ty) owns columns tx and
+// tx + 32 (a pair) of rows ty + 8 i.
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   constexpr int BM = 64, BN = 64, BK = 16;
@@ -237,8 +444,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   const bool aval = arow < a.M;
   const float* asrc = A + (size_t)(aval ? arow : 0) * a.lda + lk;
   bool second;
-  const int64_t wr = brow_index<EPI, BN>(a, tile_n, lr, &second);
-  const float* bsrc = (const float*)(second ? a.W2 : a.W) + wr * a.ldw + lk;
+  const int wr = brow_index<EPI, BN>(a, tile_n, lr, &second);
+  const float* bsrc = (const float*)(second ? a.W2 : a.W) + (size_t)wr * a.ldw + lk;
   float acc0[8], acc1[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) { acc0[i] = 0.f; acc1[i] = 0.f; }
@@ -265,10 +472,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     const int row = m0 + ty + 8 * i;
     if (row >= a.M) continue;
     if constexpr (epi_paired(EPI)) {
-      epi_pair<EPI, float, BN>(a, tile_n, tx, row, acc0[i], acc1[i]);
+      epi_tile_pair<EPI, float, BN>(a, tile_n, tx, row, acc0[i], acc1[i]);
+    } else if constexpr (EPI == EPI_STORE) {
+      epi_store(a, row, tile_n * BN + tx, acc0[i]);
+      epi_store(a, row, tile_n * BN + tx + 32, acc1[i]);
     } else {
-      epi_single<EPI>(a, row, tile_n * BN + tx, acc0[i]);
-      epi_single<EPI>(a, row, tile_n * BN + tx + 32, acc1[i]);
+      epi_resid(a, row, tile_n * BN + tx, acc0[i]);
+      epi_resid(a, row, tile_n * BN + tx + 32, acc1[i]);
     }
   }
 }

@@ -17,6 +17,8 @@ struct GemmArgs {
   const void* A2;                       // optional low part of a two-term A (same layout), or null
   const void* W; const void* W2; int ldw; // [N][K] (SWIGLU: W = gate [F][K], W2 = up [F][K], N = 2F)
   int M, N, K;
+  int ksplit;                            // K slices (bf16): a function of (N, K) only, see gemm_ksplit
+  float* part;                           // fp32 partials [ksplit][M][N] for the per-slice launch, or null
   float* C; int ldc; const int* out_row; // EPI_STORE
   float* X; int ldx;                     // EPI_RESID
   void* H; void* H2; int ldh;            // EPI_SWIGLU: H = hi part, H2 = lo part (or null)
@@ -61,6 +63,10 @@ void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void
                        int ldo, hipStream_t st);
 
 // GEMM: returns 0 on success, nonzero if the shape is unsupported.
+constexpr int GEMM_NCFG = 7;
+int gemm_ksplit(int N, int K);
+int gemm_pick_cfg(const GemmArgs& a, int epi);
+int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st);
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);
 int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st);
 
