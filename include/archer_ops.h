@@ -34,8 +34,12 @@ archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, con
  *   K1  [Hkv][ld1][hd]   Vt1 [Hkv][hd][ld1]   (segment 1, keys 0..nk1-1)
  *   K2  [Hkv][ld2][hd]   Vt2 [Hkv][hd][ld2]   (segment 2, keys 0..nk2-1)
  * V is stored transposed (Vt[h][d][key]).  ld1, ld2 multiples of 64,
- * nk1 <= ld1, nk2 <= ld2, head_dim 64 or 128.
- * workspace: device scratch of archer_op_attention_ws_bytes(...) bytes. */
+ * nk1 <= ld1, nk2 <= ld2, head_dim 64 or 128.  Keys are read in tiles of
+ * 64, so segment 1 must be readable up to nk1 rounded up to 64 (the values
+ * there are ignored).
+ * workspace: device scratch of archer_op_attention_ws_bytes(...) bytes,
+ * 256-byte aligned (split-KV partial results and arrival counters; the call
+ * clears the counters itself).  Calls sharing a workspace must not overlap. */
 size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32_t hd, int32_t nk);
 archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd,
                                   const void *Q, const void *K1, const void *Vt1, int32_t nk1,
@@ -46,7 +50,8 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
 /* Kernel classes for timing. */
 enum {
   ARCHER_K_EMBED = 0, ARCHER_K_NORM = 1, ARCHER_K_GEMM_QKV = 2, ARCHER_K_ATTN = 3,
-  ARCHER_K_ATTN_MERGE = 4, ARCHER_K_GEMM_O = 5, ARCHER_K_GEMM_GATEUP = 6,
+  ARCHER_K_ATTN_MERGE = 4 /* no launches: the split-KV merge runs inside the attention kernel */,
+  ARCHER_K_GEMM_O = 5, ARCHER_K_GEMM_GATEUP = 6,
   ARCHER_K_GEMM_DOWN = 7, ARCHER_K_GEMM_HEAD = 8, ARCHER_K_DECIDE = 9,
   ARCHER_K_COUNT = 10
 };

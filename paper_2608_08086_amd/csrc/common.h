@@ -31,6 +31,7 @@ struct SeqPlan {
   int qt_off[ARCHER_MAXB + 1];    // prefix sum of attention query tiles per sequence
   int nsplit[ARCHER_MAXB];        // split-KV count of sequence s (a function of its key count only)
   int max_split;                  // max over s of nsplit
+  int qt;                         // attention query rows per workgroup (qt_off counts tiles of qt rows)
 };
 
 __device__ __forceinline__ int plan_find(const int* off, int n, int v) {

@@ -38,13 +38,14 @@ archer_status fail(archer_status s, const std::string& msg) {
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
-  size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML;
+  size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML, cnt;
   size_t part, row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
   int ldcache, ldfresh, Mmax, Rmax, max_pos, ldq;
+  size_t n_cnt;
   size_t cache_layer_elems;
 };
 
-constexpr int kMaxSplit = 8;
+constexpr int kMaxSplit = ATTN_MAX_SPLIT;
 
 std::string check_cfg(const archer_model_cfg* c, const archer_limits* l) {
   if (!c || !l) return "null cfg or limits";
@@ -98,6 +99,10 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
   const size_t part_rows = c->dtype == ARCHER_BF16 ? (size_t)L.Mmax : 1;
   L.Opart = take((size_t)kMaxSplit * hq * part_rows * hd * 4);
   L.ML = take((size_t)kMaxSplit * hq * part_rows * 2 * 4);
+  // split-KV arrival counters, one per (query tile, head); zeroed at init,
+  // and each launch leaves them zero again
+  L.n_cnt = ((size_t)L.Mmax + ATTN_QT_BF16_MIN - 1) / ATTN_QT_BF16_MIN + l->max_batch;
+  L.cnt = take(L.n_cnt * hq * 4);
   // split-K partials of response-row launches: max over the projections of ksplit * N
   size_t sn = 0;
   if (c->dtype == ARCHER_BF16) {
@@ -191,7 +196,6 @@ archer_status timed(archer_ctx* c, int cls, double bytes, double flops, F&& laun
   return ARCHER_OK;
 }
 
-int attn_qt(const archer_ctx* c) { return is_bf16(c) ? ATTN_QT_BF16 : ATTN_QT_F32; }
 
 SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) {
   SeqPlan p;
@@ -199,8 +203,11 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
   p.n = (int)sel.size();
   p.full = full ? 1 : 0;
   p.G = c->lim.resp_len;
-  const int qt = attn_qt(c);
   int rows = 0, tiles = 0;
+  for (int s = 0; s < p.n; ++s) rows += full ? c->plen[sel[s]] + p.G : p.G;
+  const int qt = is_bf16(c) ? attn_qt_bf16(rows) : ATTN_QT_F32;
+  p.qt = qt;
+  rows = 0;
   for (int s = 0; s < p.n; ++s) {
     const int b = sel[s];
     p.seq[s] = b;
@@ -313,7 +320,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.ldcache = L.ldcache;
       a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
       a.O = c->at<char>(L.O); a.O2 = lo_part(c, L.O2); a.ldo = hq * hd;
-      a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML);
+      a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML); a.cnt = c->at<int>(L.cnt);
       a.hq = hq; a.hkv = hkv; a.hd = hd;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       const double bytes = (double)rows * hq * hd * es * 2 + kv_keys * hkv * hd * es * 2;
@@ -324,17 +331,6 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
         return is_bf16(c) ? launch_attn_bf16(pl, a, c->stream) : launch_attn_f32(pl, a, max_keys, c->stream);
       });
       if (st) return st;
-      if (pl.max_split > 1) {
-        double mbytes = 0;
-        for (int s = 0; s < pl.n; ++s)
-          if (pl.nsplit[s] > 1)
-            mbytes += (double)(pl.row_off[s + 1] - pl.row_off[s]) * hq * ((hd + 2) * 4.0 * pl.nsplit[s] + hd * es);
-        st = timed(c, ARCHER_K_ATTN_MERGE, mbytes, 0.0, [&] {
-          launch_attn_merge<bf16>(pl, a.Opart, a.ML, a.O, a.O2, hq, hd, a.ldo, c->stream);
-          return 0;
-        });
-        if (st) return st;
-      }
     }
     {
       GemmArgs a = gargs(c->at<char>(L.O), hq * hd, c->w_o[l], hq * hd, rows, d, hq * hd);
@@ -481,6 +477,7 @@ archer_status archer_init(const archer_model_cfg* cfg, const archer_weights* w, 
   }
   launch_rope_table(c->at<float2>(L.rope), L.max_pos, cfg->head_dim, (double)cfg->rope_theta, c->stream);
   hipError_t he = hipMemsetAsync(c->at<int>(L.err), 0, 256, c->stream);
+  if (he == hipSuccess) he = hipMemsetAsync(c->at<int>(L.cnt), 0, L.n_cnt * cfg->n_heads * 4, c->stream);
   if (he == hipSuccess) he = hipGetLastError();
   if (he == hipSuccess) he = hipStreamSynchronize(c->stream);
   if (he != hipSuccess) {
@@ -674,7 +671,9 @@ static int op_attn_nsplit(int dtype, int nk) { return dtype == ARCHER_BF16 ? att
 size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32_t hd, int32_t nk) {
   if (Mq < 1 || Hq < 1 || hd < 1 || nk < 1) return 0;
   const int ns = op_attn_nsplit(dtype, nk);
-  return align_up((size_t)ns * Hq * Mq * hd * 4, 256) + (size_t)ns * Hq * Mq * 2 * 4 + 256;
+  const size_t qtiles = (size_t)(Mq + ATTN_QT_BF16_MIN - 1) / ATTN_QT_BF16_MIN;
+  return align_up((size_t)ns * Hq * Mq * hd * 4, 256) + align_up((size_t)ns * Hq * Mq * 2 * 4, 256) +
+         qtiles * Hq * 4 + 256;
 }
 
 archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd, const void* Q,
@@ -693,7 +692,8 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
   memset(&p, 0, sizeof(p));
   p.n = 1; p.full = 0; p.G = nk2; p.rows = Mq;
   p.row_off[1] = Mq; p.p_len[0] = nk1;
-  const int qt = dtype == ARCHER_BF16 ? ATTN_QT_BF16 : ATTN_QT_F32;
+  const int qt = dtype == ARCHER_BF16 ? attn_qt_bf16(Mq) : ATTN_QT_F32;
+  p.qt = qt;
   p.qt_off[1] = (Mq + qt - 1) / qt;
   p.nsplit[0] = ns;
   p.max_split = ns;
@@ -705,15 +705,19 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
   a.O = O; a.ldo = Hq * hd;
   a.hq = Hq; a.hkv = Hkv; a.hd = hd;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
-  if (ns > 1) {
-    a.Opart = (float*)workspace;
-    a.ML = (float*)((char*)workspace + align_up((size_t)ns * Hq * Mq * hd * 4, 256));
-  }
   hipStream_t st = (hipStream_t)hip_stream;
+  if (ns > 1) {
+    const size_t o1 = align_up((size_t)ns * Hq * Mq * hd * 4, 256);
+    const size_t o2 = o1 + align_up((size_t)ns * Hq * Mq * 2 * 4, 256);
+    a.Opart = (float*)workspace;
+    a.ML = (float*)((char*)workspace + o1);
+    a.cnt = (int*)((char*)workspace + o2);
+    // the counters are cleared by a kernel (not a memset node) on every call
+    launch_fill_i32(a.cnt, 0, (size_t)p.qt_off[1] * Hq, st);
+  }
   int rc;
   if (dtype == ARCHER_BF16) {
     rc = launch_attn_bf16(p, a, st);
-    if (!rc && ns > 1) launch_attn_merge<bf16>(p, a.Opart, a.ML, O, nullptr, Hq, hd, a.ldo, st);
   } else {
     rc = launch_attn_f32(p, a, ((nk1 + 63) & ~63) + nk2, st);
   }

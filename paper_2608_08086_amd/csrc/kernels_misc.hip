@@ -1,5 +1,7 @@
 // Row-wise kernels of the Archer path: RoPE table, embedding gather, RMSNorm,
 // decision row statistics and selection, and the split-KV attention merge.
+#include <algorithm>
+
 #include "launch.h"
 
 // ---------------------------------------------------------------------------
@@ -316,32 +318,12 @@ void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, cons
 // Split-KV merge: O[row][h*hd + d] = sum_s w_s O_s / sum_s w_s l_s with
 // w_s = 2^(m_s - max_s m_s); partials are unnormalised, m in log2 units.
 // Rows of sequences attended in one split were written directly and are skipped.
-template <class T>
-__global__ void attn_merge_kernel(SeqPlan pl, const float* __restrict__ Op, const float* __restrict__ ML,
-                                  T* __restrict__ O, T* __restrict__ O2, int hq, int hd, int ldo) {
-  const int row = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
-  const int nsplit = pl.nsplit[plan_find(pl.row_off, pl.n, row)];
-  if (nsplit <= 1) return;
-  const int rows = pl.rows;
-  float M = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ML[(((size_t)s * hq + h) * rows + row) * 2]);
-  float num = 0.f, den = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const size_t base = ((size_t)s * hq + h) * rows + row;
-    const float m = ML[base * 2], l = ML[base * 2 + 1];
-    const float w = (l > 0.f) ? exp2f(m - M) : 0.f;
-    den += w * l;
-    if (d < hd) num += w * Op[base * hd + d];
-  }
-  if (d < hd) store_act<T>(O, O2, (size_t)row * ldo + h * hd + d, num / den);
+__global__ void fill_i32_kernel(int* p, int v, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
-template <class T>
-void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, void* O2, int hq, int hd,
-                       int ldo, hipStream_t st) {
-  attn_merge_kernel<T><<<dim3(pl.rows, hq), hd, 0, st>>>(pl, Op, ML, (T*)O, (T*)O2, hq, hd, ldo);
+void launch_fill_i32(int* p, int v, size_t n, hipStream_t st) {
+  if (n == 0) return;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 1024);
+  fill_i32_kernel<<<blocks, 256, 0, st>>>(p, v, n);
 }
-template void launch_attn_merge<float>(const SeqPlan&, const float*, const float*, void*, void*, int, int, int,
-                                       hipStream_t);
-template void launch_attn_merge<bf16>(const SeqPlan&, const float*, const float*, void*, void*, int, int, int,
-                                      hipStream_t);

@@ -36,12 +36,21 @@ struct AttnArgs {
   const void* Kf; const void* Vtf; int ldfresh;
   void* O; void* O2; int ldo;            // [rows][ldo]: hi part, lo part (or null)
   float* Opart; float* ML;               // split partials [max_split][Hq][rows][hd], [max_split][Hq][rows][2]
+  int* cnt;                              // [query tiles][Hq] arrival counters, zero between launches
   int hq, hkv, hd;
   float scale_log2;                      // log2(e) / sqrt(hd)
 };
 
 // query tile (rows per attention workgroup) of each attention kernel
-constexpr int ATTN_QT_BF16 = 64;
+// bf16: 64 query rows per workgroup (one 16-row block per wave) for passes of
+// fewer than ATTN_QT_WIDE_ROWS rows, 128 (two blocks per wave) otherwise.  The
+// result of a query row does not depend on the tiling (every softmax decision
+// is per query).
+constexpr int ATTN_QT_BF16_MIN = 64;
+constexpr int ATTN_QT_WIDE_ROWS = 512;
+inline int attn_qt_bf16(int rows) { return rows >= ATTN_QT_WIDE_ROWS ? 128 : 64; }
+constexpr int ATTN_MAX_SPLIT = 8;          // split-KV bound (workspace is sized for it)
+constexpr int ATTN_TILES_PER_SPLIT = 16;   // 64-key tiles per split, at least
 constexpr int ATTN_QT_F32 = 1;
 
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
@@ -58,9 +67,7 @@ void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, cons
                    const float* qv, int G, int mask_id, int k, float log_tau, int max_remask, int final_step,
                    int* dist, int* unmask_pos, int* remask_pos, int* tr_dist, int* tr_unmask, int* tr_utok,
                    int* tr_remask, hipStream_t st);
-template <class T>
-void launch_attn_merge(const SeqPlan& pl, const float* Op, const float* ML, void* O, void* O2, int hq, int hd,
-                       int ldo, hipStream_t st);
+void launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
 
 // GEMM: returns 0 on success, nonzero if the shape is unsupported.
 constexpr int GEMM_NCFG = 7;
