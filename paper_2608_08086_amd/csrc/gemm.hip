@@ -14,14 +14,9 @@
 // same bits, so a row's result never depends on how many rows are in the
 // launch (CachedForward on its own cache equals FullForward bitwise).
 //
-// Column pairing.  RoPE rotates dimension j with j + hd/2 of a head, SwiGLU
-// multiplies gate feature f with up feature f.  The B tile rows (weight rows)
-// are gathered so that tile column r and r + BN/2 form such a pair, and each
-// wave's columns are taken from both halves of the tile so that a pair sits in
-// one lane:
-//   QKV:    columns {h*hd + j0 + c} and {h*hd + hd/2 + j0 + c}, c < BN/2,
-//           j0 = (tile offset within the head) * BN/2  (all of q, k and v);
-//   SWIGLU: gate rows f0 + c and up rows f0 + c, f0 = tile * BN/2.
+// Column pairing (gemm_common.h): tile column r and r + BN/2 are an RoPE or
+// SwiGLU pair, and each wave's columns are taken from both halves of the tile
+// so that a pair sits in one lane.
 //
 // Tile order.  Workgroups are dispatched round-robin over the 8 XCDs.  The
 // linear workgroup id is laid out so that all M tiles of one (N tile, slice)
@@ -34,104 +29,8 @@
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-namespace {
+#include "gemm_common.h"
 
-// weight row of tile column r; *second = the row is in W2 (SWIGLU up rows)
-template <int EPI, int BN>
-__device__ __forceinline__ int brow_index(const GemmArgs& a, int tile_n, int r, bool* second) {
-  *second = false;
-  if constexpr (EPI == EPI_SWIGLU) {
-    const int f0 = tile_n * (BN / 2);
-    if (r < BN / 2) return f0 + r;
-    *second = true;
-    return f0 + r - BN / 2;
-  } else if constexpr (EPI == EPI_QKV) {
-    const int col0 = tile_n * BN;
-    const int base = (col0 / a.hd) * a.hd;
-    const int j0 = ((col0 % a.hd) / BN) * (BN / 2);
-    return r < BN / 2 ? base + j0 + r : base + a.hd / 2 + j0 + (r - BN / 2);
-  } else {
-    return tile_n * BN + r;
-  }
-}
-
-// ---- epilogues on logical (global) columns ----------------------------------
-__device__ __forceinline__ void epi_store(const GemmArgs& a, int row, int col, float v) {
-  const int orow = a.out_row ? a.out_row[row] : row;
-  a.C[(size_t)orow * a.ldc + col] = v;
-}
-
-__device__ __forceinline__ void epi_resid(const GemmArgs& a, int row, int col, float v) {
-  a.X[(size_t)row * a.ldx + col] += v;
-}
-
-template <class T>
-__device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int f, float g, float u) {
-  const float s = g / (1.0f + expf(-g));
-  store_act<T>((T*)a.H, (T*)a.H2, (size_t)row * a.ldh + f, s * u);
-}
-
-// head in [0, hq + 2 hkv): q heads, k heads, v heads; v1 / v2 = dims j, j + hd/2
-template <class T>
-__device__ __forceinline__ void epi_qkv(const GemmArgs& a, int row, int head, int j, float v1, float v2) {
-  const int hd = a.hd;
-  const int dst = a.row_dst[row];
-  if (head < a.hq + a.hkv) {
-    const float2 cs = a.rope[(size_t)a.row_pos[row] * (hd / 2) + j];
-    const float o1 = v1 * cs.x - v2 * cs.y;
-    const float o2 = v2 * cs.x + v1 * cs.y;
-    T* p;
-    if (head < a.hq) p = (T*)a.Qb + ((size_t)head * a.ldq + row) * hd;
-    else if (dst_is_fresh(dst)) p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * hd;
-    else p = (T*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * hd;
-    p[j] = from_f32<T>(o1);
-    p[j + hd / 2] = from_f32<T>(o2);
-  } else {
-    const int vh = head - a.hq - a.hkv;
-    T* vt;
-    int ld, col;
-    if (dst_is_fresh(dst)) { vt = (T*)a.Vtf; ld = a.ldfresh; col = dst; }
-    else { vt = (T*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
-    vt[((size_t)vh * hd + j) * ld + col] = from_f32<T>(v1);
-    vt[((size_t)vh * hd + j + hd / 2) * ld + col] = from_f32<T>(v2);
-  }
-}
-
-constexpr bool epi_paired(int epi) { return epi == EPI_SWIGLU || epi == EPI_QKV; }
-
-// Fused epilogue of one pair of tile columns (r, r + BN/2) or single column r.
-template <int EPI, class T, int BN>
-__device__ __forceinline__ void epi_tile_pair(const GemmArgs& a, int tile_n, int r, int row, float v1, float v2) {
-  if constexpr (EPI == EPI_SWIGLU) {
-    epi_swiglu<T>(a, row, tile_n * (BN / 2) + r, v1, v2);
-  } else if constexpr (EPI == EPI_QKV) {
-    const int col0 = tile_n * BN;
-    epi_qkv<T>(a, row, col0 / a.hd, ((col0 % a.hd) / BN) * (BN / 2) + r, v1, v2);
-  }
-}
-
-// logical column of tile column r in the [S][M][N] partial buffer
-template <int EPI, int BN>
-__device__ __forceinline__ int logical_col(const GemmArgs& a, int tile_n, int r) {
-  bool second;
-  const int w = brow_index<EPI, BN>(a, tile_n, r, &second);
-  return second ? w + a.N / 2 : w;
-}
-
-// XCD-aware decomposition of the linear workgroup id (see the file comment).
-__device__ __forceinline__ bool tile_of(int id, int n_tiles, int m_tiles, int S, int* tn, int* tm, int* z) {
-  const int groups = n_tiles * S;
-  const int g8 = id % 8, rest = id / 8;
-  const int gblk = rest / m_tiles, m = rest % m_tiles;
-  const int group = gblk * 8 + g8;
-  if (group >= groups) return false;
-  *tn = group / S;
-  *z = group % S;
-  *tm = m;
-  return true;
-}
-
-}  // namespace
 
 int gemm_grid_size(int n_tiles, int m_tiles, int S) { return ((n_tiles * S + 7) / 8) * 8 * m_tiles; }
 
@@ -328,6 +227,22 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
   }
 }
 
+template <int EPI>
+static void reduce_epi(const GemmArgs& a, hipStream_t st) {
+  const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
+  const long total = (long)a.M * npair;
+  gemm_reduce_kernel<EPI, bf16><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(a);
+}
+
+void launch_gemm_reduce(int epi, const GemmArgs& a, hipStream_t st) {
+  switch (epi) {
+    case EPI_STORE: reduce_epi<EPI_STORE>(a, st); break;
+    case EPI_RESID: reduce_epi<EPI_RESID>(a, st); break;
+    case EPI_SWIGLU: reduce_epi<EPI_SWIGLU>(a, st); break;
+    default: reduce_epi<EPI_QKV>(a, st); break;
+  }
+}
+
 // ---------------------------------------------------------------------------
 namespace {
 
@@ -343,9 +258,7 @@ void run_cfg(const GemmArgs& a, bool partial, hipStream_t st) {
   const int grid = gemm_grid_size(n_tiles, m_tiles, partial ? a.ksplit : 1);
   if (partial) {
     run_mode<BM, BN, BK, WGM, WGN, EPI, 2>(a, grid, st);
-    const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
-    const long total = (long)a.M * npair;
-    gemm_reduce_kernel<EPI, bf16><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(a);
+    launch_gemm_reduce(EPI, a, st);
   } else if (a.ksplit > 1) {
     run_mode<BM, BN, BK, WGM, WGN, EPI, 1>(a, grid, st);
   } else {
@@ -382,8 +295,13 @@ int gemm_ksplit(int N, int K) {
 }
 
 int gemm_pick_cfg(const GemmArgs& a, int epi) {
-  // measured on MI355X (LLaDA-8B cached step and refresh shapes): the 64 x 128
-  // tile with four waves side by side is fastest up to M = 1024 rows
+  // Measured on MI355X (LLaDA-8B cached step M = 256 and refresh M = 768,
+  // two-term activations): the direct-to-LDS kernel with 128 x 192 tiles
+  // (BK 32, 4 stages) for N a multiple of 192 (gate/up: 128 column tiles, one
+  // round of 256 workgroups; QKV), else 128 x 128 tiles (BK 64, 3 stages).
+  if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a)) return GEMM_NCFG + 0;
+  if (a.N % 128 == 0 && gemm_lds_cfg_ok(1, a)) return GEMM_NCFG + 1;
+  // register-staged kernel for the remaining shapes
   const bool bn128 = a.N % 128 == 0 && (epi != EPI_QKV || a.hd % 128 == 0) &&
                      (epi != EPI_SWIGLU || (a.N / 2) % 64 == 0);
   const bool bk64 = a.K % (2 * a.ksplit * 64) == 0;   // even number of 64-wide k tiles per slice
@@ -405,11 +323,13 @@ bool gemm_cfg_ok(int cfg, const GemmArgs& a, int epi) {
 }
 
 int gemm_partial_wanted(int cfg, const GemmArgs& a) {
-  const int tiles = (a.N / kCfgBN[cfg]) * ((a.M + kCfgBM[cfg] - 1) / kCfgBM[cfg]);
+  const int tiles = cfg >= GEMM_NCFG ? gemm_lds_tiles(cfg - GEMM_NCFG, a)
+                                     : (a.N / kCfgBN[cfg]) * ((a.M + kCfgBM[cfg] - 1) / kCfgBM[cfg]);
   return a.ksplit > 1 && tiles < 512;
 }
 
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st) {
+  if (cfg >= GEMM_NCFG) return launch_gemm_lds_cfg(epi, cfg - GEMM_NCFG, partial, a, st);
   if (!gemm_cfg_ok(cfg, a, epi)) return 1;
   if (partial && (!a.part || a.ksplit < 2)) return 1;
   switch (epi) {

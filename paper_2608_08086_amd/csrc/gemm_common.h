@@ -1,0 +1,112 @@
+// Shared pieces of the bf16 / fp32 projection GEMMs: weight-row gathering for
+// paired epilogues, the fused epilogues, and the XCD-aware tile order.
+//
+// Column pairing.  RoPE rotates dimension j with j + hd/2 of a head, SwiGLU
+// multiplies gate feature f with up feature f.  The B tile rows (weight rows)
+// are gathered so that tile column r and r + BN/2 form such a pair:
+//   QKV:    pair p = tile * BN/2 + c (c < BN/2) is (head p / (hd/2), dim
+//           j = p mod (hd/2)); its columns are head*hd + j and head*hd + hd/2 + j
+//           (q, k and v heads alike);
+//   SWIGLU: gate row f and up row f, f = tile * BN/2 + c.
+#pragma once
+
+#include "launch.h"
+
+namespace {
+
+// weight row of tile column r; *second = the row is in W2 (SWIGLU up rows)
+template <int EPI, int BN>
+__device__ __forceinline__ int brow_index(const GemmArgs& a, int tile_n, int r, bool* second) {
+  *second = false;
+  if constexpr (EPI == EPI_SWIGLU) {
+    const int f0 = tile_n * (BN / 2);
+    if (r < BN / 2) return f0 + r;
+    *second = true;
+    return f0 + r - BN / 2;
+  } else if constexpr (EPI == EPI_QKV) {
+    // rotation pairs are numbered across heads: pair p = (head, j), j < hd/2
+    const int half = a.hd / 2;
+    const int p = tile_n * (BN / 2) + (r < BN / 2 ? r : r - BN / 2);
+    return (p / half) * a.hd + (r < BN / 2 ? 0 : half) + p % half;
+  } else {
+    return tile_n * BN + r;
+  }
+}
+
+// ---- epilogues on logical (global) columns ----------------------------------
+__device__ __forceinline__ void epi_store(const GemmArgs& a, int row, int col, float v) {
+  const int orow = a.out_row ? a.out_row[row] : row;
+  a.C[(size_t)orow * a.ldc + col] = v;
+}
+
+__device__ __forceinline__ void epi_resid(const GemmArgs& a, int row, int col, float v) {
+  a.X[(size_t)row * a.ldx + col] += v;
+}
+
+template <class T>
+__device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int f, float g, float u) {
+  const float s = g / (1.0f + expf(-g));
+  store_act<T>((T*)a.H, (T*)a.H2, (size_t)row * a.ldh + f, s * u);
+}
+
+// head in [0, hq + 2 hkv): q heads, k heads, v heads; v1 / v2 = dims j, j + hd/2
+template <class T>
+__device__ __forceinline__ void epi_qkv(const GemmArgs& a, int row, int head, int j, float v1, float v2) {
+  const int hd = a.hd;
+  const int dst = a.row_dst[row];
+  if (head < a.hq + a.hkv) {
+    const float2 cs = a.rope[(size_t)a.row_pos[row] * (hd / 2) + j];
+    const float o1 = v1 * cs.x - v2 * cs.y;
+    const float o2 = v2 * cs.x + v1 * cs.y;
+    T* p;
+    if (head < a.hq) p = (T*)a.Qb + ((size_t)head * a.ldq + row) * hd;
+    else if (dst_is_fresh(dst)) p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * hd;
+    else p = (T*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * hd;
+    p[j] = from_f32<T>(o1);
+    p[j + hd / 2] = from_f32<T>(o2);
+  } else {
+    const int vh = head - a.hq - a.hkv;
+    T* vt;
+    int ld, col;
+    if (dst_is_fresh(dst)) { vt = (T*)a.Vtf; ld = a.ldfresh; col = dst; }
+    else { vt = (T*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
+    vt[((size_t)vh * hd + j) * ld + col] = from_f32<T>(v1);
+    vt[((size_t)vh * hd + j + hd / 2) * ld + col] = from_f32<T>(v2);
+  }
+}
+
+constexpr bool epi_paired(int epi) { return epi == EPI_SWIGLU || epi == EPI_QKV; }
+
+// Fused epilogue of one pair of tile columns (r, r + BN/2) or single column r.
+template <int EPI, class T, int BN>
+__device__ __forceinline__ void epi_tile_pair(const GemmArgs& a, int tile_n, int r, int row, float v1, float v2) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    epi_swiglu<T>(a, row, tile_n * (BN / 2) + r, v1, v2);
+  } else if constexpr (EPI == EPI_QKV) {
+    const int half = a.hd / 2, p = tile_n * (BN / 2) + r;
+    epi_qkv<T>(a, row, p / half, p % half, v1, v2);
+  }
+}
+
+// logical column of tile column r in the [S][M][N] partial buffer
+template <int EPI, int BN>
+__device__ __forceinline__ int logical_col(const GemmArgs& a, int tile_n, int r) {
+  bool second;
+  const int w = brow_index<EPI, BN>(a, tile_n, r, &second);
+  return second ? w + a.N / 2 : w;
+}
+
+// XCD-aware decomposition of the linear workgroup id (see the file comment).
+__device__ __forceinline__ bool tile_of(int id, int n_tiles, int m_tiles, int S, int* tn, int* tm, int* z) {
+  const int groups = n_tiles * S;
+  const int g8 = id % 8, rest = id / 8;
+  const int gblk = rest / m_tiles, m = rest % m_tiles;
+  const int group = gblk * 8 + g8;
+  if (group >= groups) return false;
+  *tn = group / S;
+  *z = group % S;
+  *tm = m;
+  return true;
+}
+
+}  // namespace

@@ -1,0 +1,299 @@
+// Projection GEMMs, multistage version: the A (two-term) and W tiles are
+// loaded straight from global memory into LDS (global_load_lds_dwordx4, no
+// register staging) NST - 1 tiles ahead of the tile being multiplied.
+//
+// Addressing.  A direct load writes the 16 bytes of lane l at LDS address
+// M0 + 16 l, so the LDS layout is fixed by the slot order and each lane
+// fetches the global chunk that belongs in its slot.  Tiles are stored
+// row-major with 16-byte chunks XOR-swizzled inside a row (physical chunk =
+// logical chunk ^ swz(row)), which keeps the MFMA fragment reads free of bank
+// conflicts.  The global address of a slot is a per-lane 32-bit offset that
+// never changes plus a wave-uniform 64-bit base that advances by BK elements
+// per tile, so the k loop spends no vector instructions on addresses.
+//
+// Synchronisation.  The loads are issued from inline assembly, so the
+// compiler's wait insertion does not see them; each iteration waits
+// (s_waitcnt vmcnt) until only the tiles issued after the one it needs are in
+// flight, then a barrier publishes that tile to all waves and also certifies
+// that every wave is done with the stage the next load overwrites.
+//
+// Results are bitwise identical to the register-staged kernel in gemm.hip:
+// the same k order (32-wide chunks in order, hi then lo term per chunk), the
+// same split-K slices and the same epilogues.
+#include <algorithm>
+
+#include "gemm_common.h"
+
+namespace {
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// s_waitcnt immediates (gfx9 encoding)
+#define GL_VMCNT(n) (((n) & 15) | (7 << 4) | (15 << 8) | ((((n) >> 4) & 3) << 14))
+#define GL_LGKMCNT0 (15 | (7 << 4) | (0 << 8) | (3 << 14))
+
+// M0 is listed as clobbered; no other code of this file keeps a value in it.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void gl_dma16(const void* sbase, unsigned voff, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// chunk swizzle of a row of CPR 16-byte chunks: the 16 rows of a fragment
+// read land on distinct banks (a 256-byte bank period holds 16 / CPR rows)
+template <int CPR>
+__device__ __forceinline__ int gl_swz(int row) {
+  return CPR == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, int NST, int EPI, bool SPLIT, int MODE>
+__global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
+  constexpr int WM = BM / WGM, WN = BN / WGN;
+  constexpr int RB = WM / 16, CB = WN / 16;
+  constexpr int CPR = BK / 8;
+  constexpr int NA = SPLIT ? 2 : 1;
+  constexpr int A_SL = BM * CPR, B_SL = BN * CPR;          // 16-byte slots per tile
+  constexpr int AI = A_SL / 256, BI = B_SL / 256;          // load instructions per wave per tile
+  constexpr int IPT = NA * AI + BI;
+  constexpr int STAGE = (NA * A_SL + B_SL) * 16;           // bytes
+  constexpr bool PARTIAL = MODE == 2, FOLD = MODE == 1;
+  static_assert(WGM * WGN == 4 && CB % 2 == 0 && RB >= 1, "bad wave grid");
+  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(A_SL % 256 == 0 && B_SL % 256 == 0, "each wave issues whole load instructions");
+  static_assert(BN % (32 * WGN) == 0, "each wave takes 16-column blocks from both tile halves");
+  static_assert((NST - 2) * IPT <= 63 && NST >= 2, "vmcnt range");
+  // the W / W2 split of a SwiGLU tile falls on a wave-instruction boundary
+  static_assert((BN / 2) % (64 / CPR) == 0, "pair halves must not share a load instruction");
+  __shared__ __attribute__((aligned(1024))) char smem[NST * STAGE];
+
+  const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
+  int tile_n, tile_m, z;
+  if (!tile_of(blockIdx.x, n_tiles, m_tiles, PARTIAL ? a.ksplit : 1, &tile_n, &tile_m, &z)) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int wm = w / WGN, wn = w % WGN;
+  const int m0 = tile_m * BM;
+  const int kslice = a.K / a.ksplit;
+  const int kbeg = PARTIAL ? z * kslice : 0;
+  const int nslices = FOLD ? a.ksplit : 1;
+  const int kt_slice = (PARTIAL || FOLD ? kslice : a.K) / BK;
+  const int ntot = nslices * kt_slice;
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+
+  // per-lane global byte offsets of the slots this lane fills (rows past M
+  // load row M - 1: finite data, and those output rows are never stored)
+  unsigned a_go[AI], b_go[BI];
+  bool b_hi[BI];
+#pragma unroll
+  for (int j = 0; j < AI; ++j) {
+    const int q = j * 256 + w * 64 + lane, r = q / CPR, pc = q % CPR;
+    const int row = min(m0 + r, a.M - 1);
+    a_go[j] = ((unsigned)row * a.lda + (pc ^ gl_swz<CPR>(r)) * 8) * 2;
+  }
+#pragma unroll
+  for (int j = 0; j < BI; ++j) {
+    const int q = j * 256 + w * 64 + lane, r = q / CPR, pc = q % CPR;
+    bool second;
+    const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
+    b_go[j] = ((unsigned)wr * a.ldw + (pc ^ gl_swz<CPR>(r)) * 8) * 2;
+    // uniform over the wave's 64 slots (rows j*256/CPR + w*64/CPR + [0, 64/CPR))
+    b_hi[j] = __builtin_amdgcn_readfirstlane(second ? 1 : 0) != 0;
+  }
+  const bf16* Abase[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
+  const bf16* Wlo = (const bf16*)a.W;
+  const bf16* Whi = (const bf16*)(a.W2 ? a.W2 : a.W);
+
+  auto issue = [&](int g) {
+    const int gg = min(g, ntot - 1);
+    const int k0 = kbeg + gg * BK;
+    const unsigned st = lds0 + (unsigned)((g % NST) * STAGE);
+#pragma unroll
+    for (int t = 0; t < NA; ++t)
+#pragma unroll
+      for (int j = 0; j < AI; ++j)
+        gl_dma16(Abase[t] + k0, a_go[j], st + (unsigned)((t * A_SL + j * 256 + wu * 64) * 16));
+#pragma unroll
+    for (int j = 0; j < BI; ++j)
+      gl_dma16((b_hi[j] ? Whi : Wlo) + k0, b_go[j], st + (unsigned)((NA * A_SL + j * 256 + wu * 64) * 16));
+  };
+
+  // LDS byte offsets of this lane's fragment reads within a stage, per 32-wide k chunk
+  unsigned a_lo[BK / 32][RB], b_lo[BK / 32][CB];
+  int tc[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) tc[cb] = (cb / (CB / 2)) * (BN / 2) + wn * (WN / 2) + (cb % (CB / 2)) * 16 + lc;
+#pragma unroll
+  for (int ks = 0; ks < BK / 32; ++ks) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int r = wm * WM + rb * 16 + lc;
+      a_lo[ks][rb] = (unsigned)((r * CPR + ((ks * 4 + lg) ^ gl_swz<CPR>(r))) * 16);
+    }
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+      b_lo[ks][cb] = (unsigned)((NA * A_SL + tc[cb] * CPR + ((ks * 4 + lg) ^ gl_swz<CPR>(tc[cb]))) * 16);
+  }
+
+  f32x4 acc[RB][CB];
+  f32x4 tot[FOLD ? RB : 1][FOLD ? CB : 1];
+#pragma unroll
+  for (int i = 0; i < RB; ++i)
+#pragma unroll
+    for (int j = 0; j < CB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (FOLD) {
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < CB; ++j) tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s) issue(s);
+  for (int g = 0; g < ntot; ++g) {
+    // tile g has landed once at most the NST - 2 tiles issued after it are in flight
+    __builtin_amdgcn_s_waitcnt(GL_VMCNT((NST - 2) * IPT));
+    __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(g + NST - 1);                 // into the stage of tile g - 1, which every wave has left
+    const char* stg = smem + (g % NST) * STAGE;
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      bf16x8 bfr[CB];
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) bfr[cb] = *(const bf16x8*)(stg + b_lo[ks][cb]);
+#pragma unroll
+      for (int t = 0; t < NA; ++t) {
+        bf16x8 af[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) af[rb] = *(const bf16x8*)(stg + t * A_SL * 16 + a_lo[ks][rb]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bfr[cb], acc[rb][cb], 0, 0, 0);
+      }
+    }
+    if constexpr (FOLD) {
+      if ((g + 1) % kt_slice == 0) {
+#pragma unroll
+        for (int i = 0; i < RB; ++i)
+#pragma unroll
+          for (int j = 0; j < CB; ++j) {
+            tot[i][j] += acc[i][j];
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+      }
+    }
+  }
+  // the trailing (redundant) loads must land before the workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(GL_VMCNT(0));
+  asm volatile("" ::: "memory");
+
+  // accumulator (rb, cb)[i]: row wm*WM + 16*rb + 4*lg + i, tile column tc[cb]
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = m0 + wm * WM + rb * 16 + lg * 4 + i;
+      if (row >= a.M) continue;
+      if constexpr (PARTIAL) {
+        float* pr = a.part + ((size_t)z * a.M + row) * a.N;
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) pr[logical_col<EPI, BN>(a, tile_n, tc[cb])] = acc[rb][cb][i];
+      } else if constexpr (epi_paired(EPI)) {
+#pragma unroll
+        for (int cb = 0; cb < CB / 2; ++cb) {
+          const float v1 = FOLD ? tot[rb % (FOLD ? RB : 1)][cb % (FOLD ? CB : 1)][i] : acc[rb][cb][i];
+          const float v2 = FOLD ? tot[rb % (FOLD ? RB : 1)][(cb + CB / 2) % (FOLD ? CB : 1)][i] : acc[rb][cb + CB / 2][i];
+          epi_tile_pair<EPI, bf16, BN>(a, tile_n, tc[cb], row, v1, v2);
+        }
+      } else {
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+          const int col = tile_n * BN + tc[cb];
+          const float v = FOLD ? tot[rb % (FOLD ? RB : 1)][cb % (FOLD ? CB : 1)][i] : acc[rb][cb][i];
+          if constexpr (EPI == EPI_STORE) epi_store(a, row, col, v);
+          else epi_resid(a, row, col, v);
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, int NST, int EPI, int MODE>
+void lds_mode(const GemmArgs& a, int grid, hipStream_t st) {
+  if (a.A2) gemm_lds_kernel<BM, BN, BK, WGM, WGN, NST, EPI, true, MODE><<<grid, 256, 0, st>>>(a);
+  else gemm_lds_kernel<BM, BN, BK, WGM, WGN, NST, EPI, false, MODE><<<grid, 256, 0, st>>>(a);
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, int NST, int EPI>
+void lds_cfg(const GemmArgs& a, bool partial, hipStream_t st) {
+  const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
+  const int grid = gemm_grid_size(n_tiles, m_tiles, partial ? a.ksplit : 1);
+  if (partial) {
+    lds_mode<BM, BN, BK, WGM, WGN, NST, EPI, 2>(a, grid, st);
+    launch_gemm_reduce(EPI, a, st);
+  } else if (a.ksplit > 1) {
+    lds_mode<BM, BN, BK, WGM, WGN, NST, EPI, 1>(a, grid, st);
+  } else {
+    lds_mode<BM, BN, BK, WGM, WGN, NST, EPI, 0>(a, grid, st);
+  }
+}
+
+struct LdsCfg { int BM, BN, BK; };
+// configuration table (index = cfg - GEMM_NCFG_REG)
+const LdsCfg kLds[GEMM_NCFG_LDS] = {
+    {128, 192, 32},   // 0: 2 x 2 waves of 64 x 96, 4 stages
+    {128, 128, 64},   // 1: 2 x 2 waves of 64 x 64, 3 stages
+    {128, 128, 32},   // 2: 2 x 2 waves of 64 x 64, 4 stages
+    {64, 128, 64},    // 3: 1 x 4 waves of 64 x 32, 3 stages
+    {128, 96, 64},    // 4: 4 x 1 waves of 32 x 96, 3 stages
+    {256, 128, 32},   // 5: 2 x 2 waves of 128 x 64, 3 stages
+};
+
+template <int EPI>
+void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
+  switch (c) {
+    case 0: lds_cfg<128, 192, 32, 2, 2, 4, EPI>(a, partial, st); break;
+    case 1: lds_cfg<128, 128, 64, 2, 2, 3, EPI>(a, partial, st); break;
+    case 2: lds_cfg<128, 128, 32, 2, 2, 4, EPI>(a, partial, st); break;
+    case 3: lds_cfg<64, 128, 64, 1, 4, 3, EPI>(a, partial, st); break;
+    case 4: lds_cfg<128, 96, 64, 4, 1, 3, EPI>(a, partial, st); break;
+    default: lds_cfg<256, 128, 32, 2, 2, 3, EPI>(a, partial, st); break;
+  }
+}
+
+}  // namespace
+
+bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
+  if (c < 0 || c >= GEMM_NCFG_LDS) return false;
+  const LdsCfg& k = kLds[c];
+  if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * k.BK)) return false;
+  // 32-bit lane offsets
+  if ((size_t)a.N * a.ldw * 2 >= (1ull << 32) || (size_t)a.M * a.lda * 2 >= (1ull << 32)) return false;
+  return true;
+}
+
+int gemm_lds_tiles(int c, const GemmArgs& a) {
+  const LdsCfg& k = kLds[c];
+  return (a.N / k.BN) * ((a.M + k.BM - 1) / k.BM);
+}
+
+int launch_gemm_lds_cfg(int epi, int c, bool partial, const GemmArgs& a, hipStream_t st) {
+  if (!gemm_lds_cfg_ok(c, a)) return 1;
+  if (partial && (!a.part || a.ksplit < 2)) return 1;
+  switch (epi) {
+    case EPI_STORE: lds_epi<EPI_STORE>(c, a, partial, st); break;
+    case EPI_RESID: lds_epi<EPI_RESID>(c, a, partial, st); break;
+    case EPI_SWIGLU: lds_epi<EPI_SWIGLU>(c, a, partial, st); break;
+    case EPI_QKV: lds_epi<EPI_QKV>(c, a, partial, st); break;
+    default: return 1;
+  }
+  return 0;
+}

@@ -70,8 +70,17 @@ void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, cons
 void launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
 
 // GEMM: returns 0 on success, nonzero if the shape is unsupported.
+// Configurations 0 .. GEMM_NCFG-1: register-staged kernel (gemm.hip);
+// GEMM_NCFG .. GEMM_NCFG+GEMM_NCFG_LDS-1: direct-to-LDS multistage kernel
+// (gemm_lds.hip).  All give the same bits for the same (N, K) split.
 constexpr int GEMM_NCFG = 7;
+constexpr int GEMM_NCFG_LDS = 6;
 int gemm_ksplit(int N, int K);
+bool gemm_lds_cfg_ok(int c, const GemmArgs& a);
+int gemm_lds_tiles(int c, const GemmArgs& a);
+int launch_gemm_lds_cfg(int epi, int c, bool partial, const GemmArgs& a, hipStream_t st);
+void launch_gemm_reduce(int epi, const GemmArgs& a, hipStream_t st);
+int gemm_grid_size(int n_tiles, int m_tiles, int S);
 int gemm_pick_cfg(const GemmArgs& a, int epi);
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st);
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);
@@ -80,6 +89,6 @@ int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st);
 // Split-KV count for a sequence with nkeys keys (padded key space); the same
 // function is used by every pass so results do not depend on the batch or pass.
 int attn_nsplit_for_keys(int nkeys);
-// Attention over the plan's sequences; sequences with nsplit > 1 write partials (merge separately).
+// Attention over the plan's sequences; split-KV partials are merged inside the kernel.
 int launch_attn_bf16(const SeqPlan& pl, const AttnArgs& a, hipStream_t st);
 int launch_attn_f32(const SeqPlan& pl, const AttnArgs& a, int max_keys, hipStream_t st);
