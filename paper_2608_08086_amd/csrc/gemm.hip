@@ -296,10 +296,15 @@ int gemm_ksplit(int N, int K) {
 
 int gemm_pick_cfg(const GemmArgs& a, int epi) {
   // Measured on MI355X (LLaDA-8B cached step M = 256 and refresh M = 768,
-  // two-term activations): the direct-to-LDS kernel with 128 x 192 tiles
-  // (BK 32, 4 stages) for N a multiple of 192 (gate/up: 128 column tiles, one
-  // round of 256 workgroups; QKV), else 128 x 128 tiles (BK 64, 3 stages).
-  if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a)) return GEMM_NCFG + 0;
+  // two-term activations): the warp-specialised direct-to-LDS kernel with
+  // 128 x 192 tiles when N is a multiple of 192 (gate/up: 128 column tiles, one
+  // round of 256 workgroups; QKV), else with 128 x 128 tiles.  The 128 x 192
+  // tile is not used for slices folded in one workgroup (its second
+  // accumulator set does not fit the registers of two waves per SIMD).
+  if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a)) {
+    const bool fold = a.ksplit > 1 && !(a.part && gemm_partial_wanted(GEMM_NCFG + 0, a));
+    if (!fold) return GEMM_NCFG + 0;
+  }
   if (a.N % 128 == 0 && gemm_lds_cfg_ok(1, a)) return GEMM_NCFG + 1;
   // register-staged kernel for the remaining shapes
   const bool bn128 = a.N % 128 == 0 && (epi != EPI_QKV || a.hd % 128 == 0) &&

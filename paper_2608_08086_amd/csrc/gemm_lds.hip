@@ -1,6 +1,12 @@
-// Projection GEMMs, multistage version: the A (two-term) and W tiles are
-// loaded straight from global memory into LDS (global_load_lds_dwordx4, no
-// register staging) NST - 1 tiles ahead of the tile being multiplied.
+// Projection GEMMs, multistage warp-specialised version.
+//
+// A workgroup has 8 waves: waves 0-3 multiply (a 2 x 2 or 4 x 1 grid of
+// wave tiles, MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulate), waves 4-7 only
+// load.  The loaders move the A (two-term: hi and lo) and W tiles of 32-wide k
+// chunks straight from global memory into NST LDS stages
+// (global_load_lds_dwordx4, no register staging).  With one wave per SIMD
+// doing both jobs, a wave blocked issuing loads into a full memory queue also
+// stops issuing MFMAs; separate loader waves keep the MFMA pipes fed.
 //
 // Addressing.  A direct load writes the 16 bytes of lane l at LDS address
 // M0 + 16 l, so the LDS layout is fixed by the slot order and each lane
@@ -8,14 +14,17 @@
 // row-major with 16-byte chunks XOR-swizzled inside a row (physical chunk =
 // logical chunk ^ swz(row)), which keeps the MFMA fragment reads free of bank
 // conflicts.  The global address of a slot is a per-lane 32-bit offset that
-// never changes plus a wave-uniform 64-bit base that advances by BK elements
-// per tile, so the k loop spends no vector instructions on addresses.
+// never changes plus a wave-uniform 64-bit base that advances by 32 elements
+// per tile, so the loaders spend no vector instructions on addresses.
 //
-// Synchronisation.  The loads are issued from inline assembly, so the
-// compiler's wait insertion does not see them; each iteration waits
-// (s_waitcnt vmcnt) until only the tiles issued after the one it needs are in
-// flight, then a barrier publishes that tile to all waves and also certifies
-// that every wave is done with the stage the next load overwrites.
+// Synchronisation (one barrier per tile, all 8 waves).  The multiply waves
+// hold the fragments of tile g in registers (read during tile g - 1) and
+// place barrier X_g between the hi-term and lo-term MFMAs of tile g; after
+// X_g they read the fragments of tile g + 1, overlapping the lo-term MFMAs.
+// A loader arrives at X_g once its loads of tile g + 1 have landed
+// (s_waitcnt vmcnt; the loads are issued from inline assembly, outside the
+// compiler's own wait tracking) and after X_g loads tile g + NST into the
+// stage of tile g, which no wave reads any more.
 //
 // Results are bitwise identical to the register-staged kernel in gemm.hip:
 // the same k order (32-wide chunks in order, hi then lo term per chunk), the
@@ -25,8 +34,6 @@
 #include "gemm_common.h"
 
 namespace {
-
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // s_waitcnt immediates (gfx9 encoding)
 #define GL_VMCNT(n) (((n) & 15) | (7 << 4) | (15 << 8) | ((((n) >> 4) & 3) << 14))
@@ -43,29 +50,34 @@ __device__ __forceinline__ void gl_dma16(const void* sbase, unsigned voff, unsig
 }
 #pragma clang diagnostic pop
 
-// chunk swizzle of a row of CPR 16-byte chunks: the 16 rows of a fragment
-// read land on distinct banks (a 256-byte bank period holds 16 / CPR rows)
-template <int CPR>
-__device__ __forceinline__ int gl_swz(int row) {
-  return CPR == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+__device__ __forceinline__ void gl_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN, int NST, int EPI, bool SPLIT, int MODE>
-__global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
+// Chunk swizzle of a 64-byte row (four 16-byte chunks), chosen by measurement
+// (LDS bank-conflict counter of ds_read_b128 over 16 rows x one chunk): the
+// chunk index is XORed with (row / 2) mod 4.
+__device__ __forceinline__ int gl_swz(int row) { return (row >> 1) & 3; }
+
+constexpr int BK = 32;      // k chunk per tile (one MFMA k step)
+constexpr int CPR = BK / 8; // 16-byte chunks per tile row
+
+template <int BM, int BN, int WGM, int WGN, int NST, int EPI, bool SPLIT, int MODE>
+__global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int RB = WM / 16, CB = WN / 16;
-  constexpr int CPR = BK / 8;
   constexpr int NA = SPLIT ? 2 : 1;
   constexpr int A_SL = BM * CPR, B_SL = BN * CPR;          // 16-byte slots per tile
-  constexpr int AI = A_SL / 256, BI = B_SL / 256;          // load instructions per wave per tile
+  constexpr int AI = A_SL / 256, BI = B_SL / 256;          // load instructions per loader wave per tile
   constexpr int IPT = NA * AI + BI;
   constexpr int STAGE = (NA * A_SL + B_SL) * 16;           // bytes
   constexpr bool PARTIAL = MODE == 2, FOLD = MODE == 1;
   static_assert(WGM * WGN == 4 && CB % 2 == 0 && RB >= 1, "bad wave grid");
-  static_assert(BK == 32 || BK == 64, "BK");
-  static_assert(A_SL % 256 == 0 && B_SL % 256 == 0, "each wave issues whole load instructions");
+  static_assert(A_SL % 256 == 0 && B_SL % 256 == 0, "each loader wave issues whole load instructions");
   static_assert(BN % (32 * WGN) == 0, "each wave takes 16-column blocks from both tile halves");
-  static_assert((NST - 2) * IPT <= 63 && NST >= 2, "vmcnt range");
+  static_assert((NST - 1) * IPT <= 63 && NST >= 2, "vmcnt range");
   // the W / W2 split of a SwiGLU tile falls on a wave-instruction boundary
   static_assert((BN / 2) % (64 / CPR) == 0, "pair halves must not share a load instruction");
   __shared__ __attribute__((aligned(1024))) char smem[NST * STAGE];
@@ -73,70 +85,82 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
   const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
   int tile_n, tile_m, z;
   if (!tile_of(blockIdx.x, n_tiles, m_tiles, PARTIAL ? a.ksplit : 1, &tile_n, &tile_m, &z)) return;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lg = lane >> 4, lc = lane & 15;
-  const int wu = __builtin_amdgcn_readfirstlane(w);
-  const int wm = w / WGN, wn = w % WGN;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int m0 = tile_m * BM;
   const int kslice = a.K / a.ksplit;
   const int kbeg = PARTIAL ? z * kslice : 0;
   const int nslices = FOLD ? a.ksplit : 1;
   const int kt_slice = (PARTIAL || FOLD ? kslice : a.K) / BK;
   const int ntot = nslices * kt_slice;
-  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
 
-  // per-lane global byte offsets of the slots this lane fills (rows past M
-  // load row M - 1: finite data, and those output rows are never stored)
-  unsigned a_go[AI], b_go[BI];
-  bool b_hi[BI];
+  if (w >= 4) {
+    // ---- loader waves -------------------------------------------------------
+    const int wp = w - 4;
+    const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+    // per-lane global byte offsets of the slots this lane fills (rows past M
+    // load row M - 1: finite data, and those output rows are never stored)
+    unsigned a_go[AI], b_go[BI];
+    bool b_hi[BI];
 #pragma unroll
-  for (int j = 0; j < AI; ++j) {
-    const int q = j * 256 + w * 64 + lane, r = q / CPR, pc = q % CPR;
-    const int row = min(m0 + r, a.M - 1);
-    a_go[j] = ((unsigned)row * a.lda + (pc ^ gl_swz<CPR>(r)) * 8) * 2;
+    for (int j = 0; j < AI; ++j) {
+      const int q = j * 256 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
+      const int row = min(m0 + r, a.M - 1);
+      a_go[j] = ((unsigned)row * a.lda + (pc ^ gl_swz(r)) * 8) * 2;
+    }
+#pragma unroll
+    for (int j = 0; j < BI; ++j) {
+      const int q = j * 256 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
+      bool second;
+      const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
+      b_go[j] = ((unsigned)wr * a.ldw + (pc ^ gl_swz(r)) * 8) * 2;
+      // uniform over the wave's 64 slots (rows j*256/CPR + wp*64/CPR + [0, 64/CPR))
+      b_hi[j] = __builtin_amdgcn_readfirstlane(second ? 1 : 0) != 0;
+    }
+    const bf16* Abase[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
+    const bf16* Wlo = (const bf16*)a.W;
+    const bf16* Whi = (const bf16*)(a.W2 ? a.W2 : a.W);
+    // tiles past the last are clamped: redundant loads into stages no wave reads again
+    auto issue = [&](int g) {
+      const int k0 = kbeg + min(g, ntot - 1) * BK;
+      const unsigned st = lds0 + (unsigned)((g % NST) * STAGE);
+#pragma unroll
+      for (int t = 0; t < NA; ++t)
+#pragma unroll
+        for (int j = 0; j < AI; ++j)
+          gl_dma16(Abase[t] + k0, a_go[j], st + (unsigned)((t * A_SL + j * 256 + wp * 64) * 16));
+#pragma unroll
+      for (int j = 0; j < BI; ++j)
+        gl_dma16((b_hi[j] ? Whi : Wlo) + k0, b_go[j], st + (unsigned)((NA * A_SL + j * 256 + wp * 64) * 16));
+    };
+#pragma unroll
+    for (int s = 0; s < NST; ++s) issue(s);
+    __builtin_amdgcn_s_waitcnt(GL_VMCNT((NST - 1) * IPT));   // tile 0 landed
+    gl_barrier();                                             // X_-1
+    for (int g = 0; g + 1 < ntot; ++g) {
+      __builtin_amdgcn_s_waitcnt(GL_VMCNT((NST - 2) * IPT)); // tile g + 1 landed
+      gl_barrier();                                           // X_g
+      issue(g + NST);
+    }
+    // the trailing loads must land before the workgroup's LDS is released
+    __builtin_amdgcn_s_waitcnt(GL_VMCNT(0));
+    return;
   }
-#pragma unroll
-  for (int j = 0; j < BI; ++j) {
-    const int q = j * 256 + w * 64 + lane, r = q / CPR, pc = q % CPR;
-    bool second;
-    const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
-    b_go[j] = ((unsigned)wr * a.ldw + (pc ^ gl_swz<CPR>(r)) * 8) * 2;
-    // uniform over the wave's 64 slots (rows j*256/CPR + w*64/CPR + [0, 64/CPR))
-    b_hi[j] = __builtin_amdgcn_readfirstlane(second ? 1 : 0) != 0;
-  }
-  const bf16* Abase[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
-  const bf16* Wlo = (const bf16*)a.W;
-  const bf16* Whi = (const bf16*)(a.W2 ? a.W2 : a.W);
 
-  auto issue = [&](int g) {
-    const int gg = min(g, ntot - 1);
-    const int k0 = kbeg + gg * BK;
-    const unsigned st = lds0 + (unsigned)((g % NST) * STAGE);
-#pragma unroll
-    for (int t = 0; t < NA; ++t)
-#pragma unroll
-      for (int j = 0; j < AI; ++j)
-        gl_dma16(Abase[t] + k0, a_go[j], st + (unsigned)((t * A_SL + j * 256 + wu * 64) * 16));
-#pragma unroll
-    for (int j = 0; j < BI; ++j)
-      gl_dma16((b_hi[j] ? Whi : Wlo) + k0, b_go[j], st + (unsigned)((NA * A_SL + j * 256 + wu * 64) * 16));
-  };
-
-  // LDS byte offsets of this lane's fragment reads within a stage, per 32-wide k chunk
-  unsigned a_lo[BK / 32][RB], b_lo[BK / 32][CB];
+  // ---- multiply waves --------------------------------------------------------
+  const int lg = lane >> 4, lc = lane & 15;
+  const int wm = w / WGN, wn = w % WGN;
+  // LDS byte offsets of this lane's fragment reads within a stage
+  unsigned a_lo[RB], b_lo[CB];
   int tc[CB];
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) tc[cb] = (cb / (CB / 2)) * (BN / 2) + wn * (WN / 2) + (cb % (CB / 2)) * 16 + lc;
 #pragma unroll
-  for (int ks = 0; ks < BK / 32; ++ks) {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int r = wm * WM + rb * 16 + lc;
-      a_lo[ks][rb] = (unsigned)((r * CPR + ((ks * 4 + lg) ^ gl_swz<CPR>(r))) * 16);
-    }
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb)
-      b_lo[ks][cb] = (unsigned)((NA * A_SL + tc[cb] * CPR + ((ks * 4 + lg) ^ gl_swz<CPR>(tc[cb]))) * 16);
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = wm * WM + rb * 16 + lc;
+    a_lo[rb] = (unsigned)((r * CPR + (lg ^ gl_swz(r))) * 16);
   }
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) b_lo[cb] = (unsigned)((NA * A_SL + tc[cb] * CPR + (lg ^ gl_swz(tc[cb]))) * 16);
 
   f32x4 acc[RB][CB];
   f32x4 tot[FOLD ? RB : 1][FOLD ? CB : 1];
@@ -151,34 +175,31 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
       for (int j = 0; j < CB; ++j) tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-#pragma unroll
-  for (int s = 0; s < NST - 1; ++s) issue(s);
-  for (int g = 0; g < ntot; ++g) {
-    // tile g has landed once at most the NST - 2 tiles issued after it are in flight
-    __builtin_amdgcn_s_waitcnt(GL_VMCNT((NST - 2) * IPT));
-    __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    issue(g + NST - 1);                 // into the stage of tile g - 1, which every wave has left
+  bf16x8 fa[2][NA][RB], fb[2][CB];
+  auto read_frags = [&](int g, int buf) {
     const char* stg = smem + (g % NST) * STAGE;
 #pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8 bfr[CB];
+    for (int cb = 0; cb < CB; ++cb) fb[buf][cb] = *(const bf16x8*)(stg + b_lo[cb]);
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) bfr[cb] = *(const bf16x8*)(stg + b_lo[ks][cb]);
+    for (int t = 0; t < NA; ++t)
 #pragma unroll
-      for (int t = 0; t < NA; ++t) {
-        bf16x8 af[RB];
+      for (int rb = 0; rb < RB; ++rb) fa[buf][t][rb] = *(const bf16x8*)(stg + t * A_SL * 16 + a_lo[rb]);
+  };
+  auto mfma_term = [&](int buf, int t) {
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) af[rb] = *(const bf16x8*)(stg + t * A_SL * 16 + a_lo[ks][rb]);
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-          for (int cb = 0; cb < CB; ++cb)
-            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bfr[cb], acc[rb][cb], 0, 0, 0);
-      }
+      for (int cb = 0; cb < CB; ++cb)
+        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][t][rb], fb[buf][cb], acc[rb][cb], 0, 0, 0);
+  };
+  auto tile_body = [&](int g, int cur) {
+    mfma_term(cur, 0);
+    if (g + 1 < ntot) {
+      __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
+      gl_barrier();                               // X_g
+      read_frags(g + 1, cur ^ 1);
     }
+    if constexpr (NA == 2) mfma_term(cur, 1);
     if constexpr (FOLD) {
       if ((g + 1) % kt_slice == 0) {
 #pragma unroll
@@ -190,10 +211,13 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
           }
       }
     }
+  };
+  gl_barrier();                                   // X_-1: tile 0 landed
+  read_frags(0, 0);
+  for (int g = 0; g < ntot; g += 2) {             // fragment buffer parity static in the two halves
+    tile_body(g, 0);
+    if (g + 1 < ntot) tile_body(g + 1, 1);
   }
-  // the trailing (redundant) loads must land before the workgroup's LDS is released
-  __builtin_amdgcn_s_waitcnt(GL_VMCNT(0));
-  asm volatile("" ::: "memory");
 
   // accumulator (rb, cb)[i]: row wm*WM + 16*rb + 4*lg + i, tile column tc[cb]
 #pragma unroll
@@ -226,46 +250,43 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a) {
   }
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN, int NST, int EPI, int MODE>
+template <int BM, int BN, int WGM, int WGN, int NST, int EPI, int MODE>
 void lds_mode(const GemmArgs& a, int grid, hipStream_t st) {
-  if (a.A2) gemm_lds_kernel<BM, BN, BK, WGM, WGN, NST, EPI, true, MODE><<<grid, 256, 0, st>>>(a);
-  else gemm_lds_kernel<BM, BN, BK, WGM, WGN, NST, EPI, false, MODE><<<grid, 256, 0, st>>>(a);
+  if (a.A2) gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, true, MODE><<<grid, 512, 0, st>>>(a);
+  else gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, false, MODE><<<grid, 512, 0, st>>>(a);
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN, int NST, int EPI>
+template <int BM, int BN, int WGM, int WGN, int NST, int EPI>
 void lds_cfg(const GemmArgs& a, bool partial, hipStream_t st) {
   const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
   const int grid = gemm_grid_size(n_tiles, m_tiles, partial ? a.ksplit : 1);
   if (partial) {
-    lds_mode<BM, BN, BK, WGM, WGN, NST, EPI, 2>(a, grid, st);
+    lds_mode<BM, BN, WGM, WGN, NST, EPI, 2>(a, grid, st);
     launch_gemm_reduce(EPI, a, st);
   } else if (a.ksplit > 1) {
-    lds_mode<BM, BN, BK, WGM, WGN, NST, EPI, 1>(a, grid, st);
+    lds_mode<BM, BN, WGM, WGN, NST, EPI, 1>(a, grid, st);
   } else {
-    lds_mode<BM, BN, BK, WGM, WGN, NST, EPI, 0>(a, grid, st);
+    lds_mode<BM, BN, WGM, WGN, NST, EPI, 0>(a, grid, st);
   }
 }
 
-struct LdsCfg { int BM, BN, BK; };
-// configuration table (index = cfg - GEMM_NCFG_REG)
+struct LdsCfg { int BM, BN; };
 const LdsCfg kLds[GEMM_NCFG_LDS] = {
-    {128, 192, 32},   // 0: 2 x 2 waves of 64 x 96, 4 stages
-    {128, 128, 64},   // 1: 2 x 2 waves of 64 x 64, 3 stages
-    {128, 128, 32},   // 2: 2 x 2 waves of 64 x 64, 4 stages
-    {64, 128, 64},    // 3: 1 x 4 waves of 64 x 32, 3 stages
-    {128, 96, 64},    // 4: 4 x 1 waves of 32 x 96, 3 stages
-    {256, 128, 32},   // 5: 2 x 2 waves of 128 x 64, 3 stages
+    {128, 192},   // 0: 2 x 2 multiply waves of 64 x 96, 4 stages
+    {128, 128},   // 1: 2 x 2 multiply waves of 64 x 64, 4 stages
+    {128, 128},   // 2: as 1 with 6 stages
+    {64, 128},    // 3: 1 x 4 multiply waves of 64 x 32, 6 stages
+    {128, 192},   // 4: as 0 with 5 stages
 };
 
 template <int EPI>
 void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
   switch (c) {
-    case 0: lds_cfg<128, 192, 32, 2, 2, 4, EPI>(a, partial, st); break;
-    case 1: lds_cfg<128, 128, 64, 2, 2, 3, EPI>(a, partial, st); break;
-    case 2: lds_cfg<128, 128, 32, 2, 2, 4, EPI>(a, partial, st); break;
-    case 3: lds_cfg<64, 128, 64, 1, 4, 3, EPI>(a, partial, st); break;
-    case 4: lds_cfg<128, 96, 64, 4, 1, 3, EPI>(a, partial, st); break;
-    default: lds_cfg<256, 128, 32, 2, 2, 3, EPI>(a, partial, st); break;
+    case 0: lds_cfg<128, 192, 2, 2, 4, EPI>(a, partial, st); break;
+    case 1: lds_cfg<128, 128, 2, 2, 4, EPI>(a, partial, st); break;
+    case 2: lds_cfg<128, 128, 2, 2, 6, EPI>(a, partial, st); break;
+    case 3: lds_cfg<64, 128, 1, 4, 6, EPI>(a, partial, st); break;
+    default: lds_cfg<128, 192, 2, 2, 5, EPI>(a, partial, st); break;
   }
 }
 
@@ -274,7 +295,7 @@ void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
 bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
   if (c < 0 || c >= GEMM_NCFG_LDS) return false;
   const LdsCfg& k = kLds[c];
-  if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * k.BK)) return false;
+  if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * BK)) return false;
   // 32-bit lane offsets
   if ((size_t)a.N * a.ldw * 2 >= (1ull << 32) || (size_t)a.M * a.lda * 2 >= (1ull << 32)) return false;
   return true;

@@ -74,7 +74,7 @@ void launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
 // GEMM_NCFG .. GEMM_NCFG+GEMM_NCFG_LDS-1: direct-to-LDS multistage kernel
 // (gemm_lds.hip).  All give the same bits for the same (N, K) split.
 constexpr int GEMM_NCFG = 7;
-constexpr int GEMM_NCFG_LDS = 6;
+constexpr int GEMM_NCFG_LDS = 5;
 int gemm_ksplit(int N, int K);
 bool gemm_lds_cfg_ok(int c, const GemmArgs& a);
 int gemm_lds_tiles(int c, const GemmArgs& a);
@@ -82,6 +82,7 @@ int launch_gemm_lds_cfg(int epi, int c, bool partial, const GemmArgs& a, hipStre
 void launch_gemm_reduce(int epi, const GemmArgs& a, hipStream_t st);
 int gemm_grid_size(int n_tiles, int m_tiles, int S);
 int gemm_pick_cfg(const GemmArgs& a, int epi);
+int gemm_partial_wanted(int cfg, const GemmArgs& a);
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st);
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);
 int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st);
