@@ -35,41 +35,45 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_TFLOPS = 157.3
 
 # kernel symbol of each timed class for the LLaDA-8B shape as rocprofv3 names it
-# (template arguments: BM, BN, BK, wave grid, epilogue, two-term A, mode; see csrc/gemm.hip)
+# (gemm_lds_kernel template arguments: BM, BN, wave grid, stages, epilogue,
+# two-term A, split mode; see csrc/gemm_lds.hip)
 KERNEL_OF_CLASS = {
-    "gemm_qkv": "gemm_bf16_kernel<64, 128, 64, 1, 4, 3, true, 2> + gemm_reduce_kernel<3, bf16>",
-    "gemm_o": "gemm_bf16_kernel<64, 128, 64, 1, 4, 1, true, 2> + gemm_reduce_kernel<1, bf16>",
-    "gemm_gateup": "gemm_bf16_kernel<64, 128, 64, 1, 4, 2, true, 0>",
-    "gemm_down": "gemm_bf16_kernel<64, 128, 64, 1, 4, 1, true, 2> + gemm_reduce_kernel<1, bf16>",
-    "gemm_head": "gemm_bf16_kernel<64, 128, 64, 1, 4, 0, true, 0>", "attn": "attn_bf16_kernel<128>",
-    "attn_merge": "attn_merge_kernel<bf16>", "norm": "rmsnorm_kernel<bf16>", "embed": "embed_kernel<bf16>",
-    "decide": "rowstats_kernel + select_kernel",
+    "gemm_qkv": "gemm_lds_kernel<128, 192, 2, 2, 4, 3, true, 2> + gemm_reduce_kernel<3, bf16>",
+    "gemm_o": "gemm_lds_kernel<128, 128, 2, 2, 4, 1, true, 2> + gemm_reduce_kernel<1, bf16>",
+    "gemm_gateup": "gemm_lds_kernel<128, 192, 2, 2, 4, 2, true, 0>",
+    "gemm_down": "gemm_lds_kernel<128, 128, 2, 2, 4, 1, true, 2> + gemm_reduce_kernel<1, bf16>",
+    "gemm_head": "gemm_lds_kernel<128, 128, 2, 2, 4, 0, true, 0>",
+    "attn": "attn_bf16_kernel<128, 1> (cached passes), attn_bf16_kernel<128, 2> (refresh passes)",
+    "norm": "rmsnorm_kernel<bf16>", "embed": "embed_kernel<bf16>", "decide": "rowstats_kernel + select_kernel",
 }
 # classes whose bf16 launches multiply two-term activations (two MFMAs per fragment)
 TWO_TERM = {"gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "gemm_head"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_gateup_llada_p512.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_08086_amd", "csrc", "gemm.hip")
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def src_hash(path):
+def src_hash(paths):
+    """First 16 hex digits of the SHA-256 of the concatenated files."""
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def committed_traffic(cls):
     """HBM bytes per launch from the committed rocprofv3 PMC record, if it
-    was taken on the current kernel source; else None."""
+    was taken on the current kernel sources; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
-    except (OSError, ValueError):
-        return None
-    if rec.get("class") != cls or rec.get("kernel_source_sha256_16") != src_hash(KERNEL_SRC):
+        if rec.get("class") != cls or rec.get("kernel_sources_sha256_16") != src_hash(rec["kernel_sources"]):
+            return None
+    except (OSError, ValueError, KeyError):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -130,7 +134,7 @@ def cpu_baseline(w, lens, T, K_refresh, policy, sample_layers=9):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="llada_p512")
     ap.add_argument("--policy", default="age", choices=["age", "hamming", "always"])
