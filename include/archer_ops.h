@@ -38,8 +38,9 @@ archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, con
  * 64, so segment 1 must be readable up to nk1 rounded up to 64 (the values
  * there are ignored).
  * workspace: device scratch of archer_op_attention_ws_bytes(...) bytes,
- * 256-byte aligned (split-KV partial results and arrival counters; the call
- * clears the counters itself).  Calls sharing a workspace must not overlap. */
+ * 256-byte aligned (split-KV partial results; none is needed, and NULL is
+ * accepted, when the key count gives one split).  Calls sharing a workspace
+ * must not overlap. */
 size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32_t hd, int32_t nk);
 archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd,
                                   const void *Q, const void *K1, const void *Vt1, int32_t nk1,

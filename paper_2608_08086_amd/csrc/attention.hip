@@ -2,10 +2,12 @@
 // row of a sequence attends to that sequence's cached prompt keys followed by
 // its fresh response keys, with no mask other than key validity.
 //
-// bf16 kernel: flash-style online softmax with MFMA.  A workgroup (4 wave64s)
-// owns 64 * QB query rows of one (sequence, query head) and a contiguous
-// range of 64-key tiles (split-KV over blockIdx.z; the last split to finish
-// merges the partial results).  Per tile, K [64][hd] and V^T [hd][64] are
+// bf16 kernel: flash-style online softmax with MFMA.  A workgroup of NW
+// wave64s (two per SIMD, so that one wave's softmax overlaps the other's
+// MFMAs and LDS reads) owns 16 * QB * NW query rows of one (sequence, query
+// head) -- a whole 256-row response block -- and a contiguous range of 64-key
+// tiles (split-KV over blockIdx.z; the last split to finish merges the
+// partial results).  Every K/V tile staged in LDS serves all 256 queries.  Per tile, K [64][hd] and V^T [hd][64] are
 // loaded straight into one of three LDS stages, two tiles ahead of the one
 // being computed.  Scores are formed transposed, S^T = K Q^T, so
 // that a lane holds 4 keys x 1 query per 16x16 block; the probabilities of two
@@ -40,8 +42,9 @@ constexpr float ATT_RESCALE_LOG2 = 8.0f;
 // filled by direct global->LDS loads: the 16-byte slot a lane writes is fixed
 // (slot = instruction base + lane), so each lane loads the global chunk that
 // belongs in its slot.
-// One direct global->LDS load of 16 bytes per lane: lane l's bytes land at
-// LDS byte address lds_base + 16 * l (lds_base wave-uniform, held in M0).
+// One direct global->LDS load of 16 bytes per lane from sbase + voff (sbase
+// wave-uniform, voff a per-lane byte offset): lane l's bytes land at LDS byte
+// address lds_base + 16 * l (lds_base wave-uniform, held in M0).
 // Written as inline assembly so that the compiler's own wait insertion, which
 // cannot tell the stages apart, does not drain the loads in flight; the
 // kernel waits for them itself (ATT_VMCNT) before the barrier that publishes
@@ -49,15 +52,24 @@ constexpr float ATT_RESCALE_LOG2 = 8.0f;
 // M0 is listed as clobbered; no other code of this file keeps a value in it.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void att_dma16(const void* src, unsigned lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+__device__ __forceinline__ void att_dma16(const void* sbase, unsigned voff, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(src), "s"(lds_base)
+               : "v"(voff), "s"(sbase), "s"(lds_base)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
 
 __device__ __forceinline__ unsigned att_lds_addr(const void* p) { return (unsigned)(uintptr_t)(lds_void*)p; }
+
+// A pointer that is the same in every lane, moved to scalar registers (the
+// direct loads take their base address there).
+__device__ __forceinline__ const void* att_uniform(const void* p) {
+  const uintptr_t v = (uintptr_t)p;
+  const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)v);
+  const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(v >> 32));
+  return (const void*)(((uintptr_t)hi << 32) | lo);
+}
 
 // Four consecutive outputs of one query row as two-term bf16 (hi = bf16(v),
 // lo = bf16(v - hi)), one 8-byte store per term.
@@ -72,26 +84,58 @@ __device__ __forceinline__ void att_store4(const AttnArgs& a, size_t i, f32x4 v)
   if (a.O2) *(bf16x4*)((bf16*)a.O2 + i) = lo;
 }
 
+// K stage: row = key (CPR chunks of 8 dimensions).  The score MFMA reads the
+// 16 rows {b..b+3, b+8..b+11, b+16..b+19, b+24..b+27} at once (see
+// att_key_row), which the swizzle spreads over all banks.
 template <int CPR>
-__device__ __forceinline__ int att_swz(int row) {
-  return CPR == 16 ? (row & 15) : ((row >> 1) & 7);
+__device__ __forceinline__ int att_kswz(int row) {
+  return CPR == 16 ? ((row + 4 * (row >> 4)) & 15) : (((row >> 1) + 2 * (row >> 4)) & 7);
+}
+// V^T stage: row = dimension (8 chunks of 8 keys); 16 consecutive rows are
+// read at once.
+__device__ __forceinline__ int att_vswz(int d) { return (d >> 1) & 7; }
+
+// Instruction order of one MFMA phase of NR fragment reads from LDS, each
+// feeding MPR MFMAs: four reads ahead, then MPR MFMAs per further read, so
+// that the read latency is hidden (left to itself the scheduler waits for
+// each read right before its first MFMA).
+template <int NR, int MPR>
+__device__ __forceinline__ void att_mfma_pipeline() {
+  constexpr int AHEAD = 6;
+  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);       // DS reads
+#pragma unroll
+  for (int i = 0; i < NR - AHEAD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, MPR, 0);       // MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, MPR * AHEAD, 0);
 }
 
-template <int HD, int QB>
-__global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs a) {
-  constexpr int KT = 64, NST = 3;
+// Key (within a 64-key tile) of row r of the score MFMA's A operand for key
+// block kb.  The order makes the four scores a lane receives from blocks
+// 2 ks and 2 ks + 1 the keys 32 ks + 8 lg .. 32 ks + 8 lg + 7 in order, which
+// is exactly the B operand of the PV MFMA with k-step ks, and that operand's
+// partner (V^T row d, the same 8 keys) is one 16-byte chunk.
+__device__ __forceinline__ int att_key_row(int kb, int r) {
+  return 32 * (kb >> 1) + 4 * (kb & 1) + 8 * (r >> 2) + (r & 3);
+}
+
+template <int HD, int QB, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs a) {
+  constexpr int KT = 64, NST = 4;
+  constexpr int NT = 64 * NW;                      // threads
   constexpr int KCPR = HD / 8;                     // K chunks per row
   constexpr int KSL = KT * KCPR, VSL = HD * (KT / 8);   // 16-byte slots per stage
-  constexpr int KI = KSL / 256, VI = VSL / 256;    // load instructions per wave per stage
+  constexpr int KI = KSL / NT, VI = VSL / NT;      // load instructions per wave per stage
   constexpr int DS = HD / 32, DB = HD / 16;
-  constexpr int QT = 64 * QB;
-  // one LDS object per stage: the compiler can then tell a stage being read
-  // from the stages still being filled and does not wait for their loads
-  __shared__ __attribute__((aligned(1024))) u32x4 Ks0[KSL], Ks1[KSL], Ks2[KSL];
-  __shared__ __attribute__((aligned(1024))) u32x4 Vs0[VSL], Vs1[VSL], Vs2[VSL];
-  __shared__ int last_flag;
+  constexpr int QT = 16 * QB * NW;
+  static_assert(KSL % NT == 0 && VSL % NT == 0, "whole load instructions per wave");
+  __shared__ __attribute__((aligned(1024))) u32x4 Ks[NST * KSL];
+  __shared__ __attribute__((aligned(1024))) u32x4 Vs[NST * VSL];
+  __shared__ int simd_of[NW];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lg = lane >> 4, lc = lane & 15;
   const int gq = blockIdx.x, h = blockIdx.y, split = blockIdx.z;
   const int s = plan_find(pl.qt_off, pl.n, gq);
   const int nsplit = pl.nsplit[s];
@@ -109,50 +153,51 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
   const bf16* Kf = (const bf16*)a.Kf + (size_t)kvh * a.ldfresh * HD;
   const bf16* Vtf = (const bf16*)a.Vtf + (size_t)kvh * HD * a.ldfresh;
   const int coff = pl.cache_off[s], foff = b * G;
+  const unsigned k_lds = att_lds_addr(Ks), v_lds = att_lds_addr(Vs);
 
   // Issue the direct loads of local tile i into stage i % NST.  Keys past the
   // segment read a clamped valid key (in bounds; K rows then give scores that
   // are masked, V chunks are zeroed after arrival).
-  const int wu = __builtin_amdgcn_readfirstlane(w);
-  auto issue = [&](int i, unsigned kofs, unsigned vofs) {
+  auto issue = [&](int i, int st) __attribute__((always_inline)) {
     const int k0 = (t0 + i) * KT;
     const bool ct = k0 < ppad;
     const int kb0 = ct ? k0 : k0 - ppad;
     const int kvalid = ct ? P : G;
-    const bf16* Kseg = ct ? Kc + (size_t)coff * HD : Kf + (size_t)foff * HD;
-    const bf16* Vseg = ct ? Vtc + coff : Vtf + foff;
+    const bool part = kb0 + KT > kvalid;
+    const bf16* Kbase = (ct ? Kc + (size_t)coff * HD : Kf + (size_t)foff * HD) + (size_t)kb0 * HD;
+    const bf16* Vbase = (ct ? Vtc + coff : Vtf + foff) + kb0;
     const int vld = ct ? a.ldcache : a.ldfresh;
+    const unsigned kofs = k_lds + (unsigned)(st * KSL * 16), vofs = v_lds + (unsigned)(st * VSL * 16);
 #pragma unroll
     for (int j = 0; j < KI; ++j) {
-      const int q = j * 256 + w * 64 + lane;
+      const int q = j * NT + w * 64 + lane;
       const int r = q / KCPR, pc = q % KCPR;
-      const int key = min(kb0 + r, kvalid - 1);
-      const bf16* src = Kseg + (size_t)key * HD + (pc ^ att_swz<KCPR>(r)) * 8;
-      att_dma16(src, kofs + (j * 256 + wu * 64) * 16);
+      const int rr = part ? min(r, kvalid - 1 - kb0) : r;
+      att_dma16(att_uniform(Kbase), (unsigned)(rr * HD + (pc ^ att_kswz<KCPR>(r)) * 8) * 2, kofs + (j * NT + w * 64) * 16);
     }
 #pragma unroll
     for (int j = 0; j < VI; ++j) {
-      const int q = j * 256 + w * 64 + lane;
+      const int q = j * NT + w * 64 + lane;
       const int d = q / 8, pc = q % 8;
-      const int c = pc ^ att_swz<8>(d);
-      const int keyc = min(kb0 + c * 8, (kvalid - 1) & ~7);
-      const bf16* src = Vseg + (size_t)d * vld + keyc;
-      att_dma16(src, vofs + (j * 256 + wu * 64) * 16);
+      const int c = pc ^ att_vswz(d);
+      const int cc = part ? min(c * 8, ((kvalid - 1) & ~7) - kb0) : c * 8;
+      att_dma16(att_uniform(Vbase), (unsigned)(d * vld + cc) * 2, vofs + (j * NT + w * 64) * 16);
     }
   };
   // After local tile i has landed: zero the V entries of keys past the
   // segment in the slots this lane loaded (only partial tiles have any).
-  auto fix_tail = [&](int i, u32x4* Vd) {
+  auto fix_tail = [&](int i, int st) __attribute__((always_inline)) {
     const int k0 = (t0 + i) * KT;
     const bool ct = k0 < ppad;
     const int kb0 = ct ? k0 : k0 - ppad;
     const int kvalid = ct ? P : G;
     if (kb0 + KT <= kvalid) return;
+    u32x4* Vd = Vs + st * VSL;
 #pragma unroll
     for (int j = 0; j < VI; ++j) {
-      const int q = j * 256 + w * 64 + lane;
+      const int q = j * NT + w * 64 + lane;
       const int d = q / 8, pc = q % 8;
-      const int c = pc ^ att_swz<8>(d);
+      const int c = pc ^ att_vswz(d);
       const int nv = kvalid - (kb0 + c * 8);
       if (nv < 8) {
         u32x4 v = Vd[q];
@@ -163,10 +208,13 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
     }
   };
 
-  const unsigned k_ofs[NST] = {att_lds_addr(Ks0), att_lds_addr(Ks1), att_lds_addr(Ks2)};
-  const unsigned v_ofs[NST] = {att_lds_addr(Vs0), att_lds_addr(Vs1), att_lds_addr(Vs2)};
-  if (nt > 0) issue(0, k_ofs[0], v_ofs[0]);
-  if (nt > 1) issue(1, k_ofs[1], v_ofs[1]);
+  if (nt > 0) issue(0, 0);
+  if (nt > 1) issue(1, 1);
+
+  // Which of the two waves on this wave's SIMD it is: the first one (by wave
+  // index) runs group 0, the other group 1.  Only the schedule depends on it.
+  // s_getreg returns the 2-bit field SIMD_ID (bits 5:4 of HW_ID) already shifted down
+  if (lane == 0) simd_of[w] = __builtin_amdgcn_s_getreg((1 << 11) | (4 << 6) | 4) & 3;
 
   bf16x8 qf[QB][DS];
 #pragma unroll
@@ -177,11 +225,14 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) qf[qb][ds] = __builtin_bit_cast(bf16x8, *(const u32x4*)(Qp + ds * 32 + lg * 8));
   }
-  // the Q fragments were loaded after the first two stages were issued: wait
-  // for all of them here (the stages arrive about together), so that no wait
-  // the compiler places for Q inside the loop drains later stages
+  // wait for the Q fragments and the first two stages together, so that no
+  // wait the compiler places for Q inside the loop drains later stages
   __builtin_amdgcn_s_waitcnt(ATT_VMCNT(0));
-  asm volatile("" ::: "memory");
+  __syncthreads();
+  int grp = 0;
+  for (int v = 0; v < w; ++v) grp += simd_of[v] == simd_of[w];
+  grp = __builtin_amdgcn_readfirstlane(grp & 1);
+
   f32x4 o[QB][DB];
   float m_run[QB], l_run[QB];
 #pragma unroll
@@ -191,44 +242,43 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
 #pragma unroll
     for (int i = 0; i < DB; ++i) o[qb][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  f32x4 sc[QB][4];
+  bf16x8 pb[2][QB];
 
-  // local tile i from stage (Kcur, Vcur); tile i + 2 goes into stage nxt,
-  // the one computed at i - 1, which every wave has left at the barrier
-  auto tile = [&](int i, const u32x4* Kcur, u32x4* Vcur, int nxt) {
-    if (i + 1 < nt) __builtin_amdgcn_s_waitcnt(ATT_VMCNT(KI + VI));
-    else __builtin_amdgcn_s_waitcnt(ATT_VMCNT(0));
-    asm volatile("" ::: "memory");    // no LDS access moves above the wait
-    fix_tail(i, Vcur);
-    // a plain barrier: LDS traffic of this wave done (the fence of
-    // __syncthreads would also drain the loads still in flight)
-    __builtin_amdgcn_s_waitcnt(ATT_LGKMCNT0);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    if (i + 2 < nt) issue(i + 2, k_ofs[nxt], v_ofs[nxt]);
+  // S^T = K Q^T of local tile i: sc[qb][kb][e] = raw score of key kb*16 + 4*lg + e, query lc of block qb
+  auto scores = [&](int st) __attribute__((always_inline)) {
+    const u32x4* Kcur = Ks + st * KSL;
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kp = 0; kp < 4; kp += 2) {
+      // the fragments of two key blocks are requested before the first is used
+      bf16x8 kf[2][DS];
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int r = att_key_row(kp + k2, lc);
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds)
+          kf[k2][ds] = __builtin_bit_cast(bf16x8, Kcur[r * KCPR + ((ds * 4 + lg) ^ att_kswz<KCPR>(r))]);
+      }
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            sc[qb][kp + k2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[k2][ds], qf[qb][ds],
+                                                                      ds == 0 ? zero : sc[qb][kp + k2], 0, 0, 0);
+    }
+    att_mfma_pipeline<4 * DS, QB>();
+  };
+  // online softmax of local tile i (running maxima in log2 units); leaves the
+  // bf16 probabilities in pb as the B operand of O^T = V^T P^T
+  auto softmax = [&](int i) __attribute__((always_inline)) {
     const int k0 = (t0 + i) * KT;
     const bool ct = k0 < ppad;
     const int kb0 = ct ? k0 : k0 - ppad;
     const int kvalid = ct ? P : G;
-
-    f32x4 sc[QB][4];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) sc[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const int r = kb * 16 + lc;
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) {
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, Kcur[r * KCPR + ((ds * 4 + lg) ^ att_swz<KCPR>(r))]);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          sc[qb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][ds], sc[qb][kb], 0, 0, 0);
-      }
-    }
-    // sc[qb][kb][i]: raw score of key kb*16 + 4*lg + i and query lc of block qb.
-    // Keys past the segment (partial tiles only) get -inf, hence probability 0.
+    // keys past the segment (partial tiles only) get -inf, hence probability 0
     if (kb0 + KT > kvalid) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
@@ -236,9 +286,8 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (kb0 + kb * 16 + lg * 4 + e >= kvalid) sc[qb][kb][e] = -INFINITY;
+            if (kb0 + att_key_row(kb, 4 * lg + e) >= kvalid) sc[qb][kb][e] = -INFINITY;
     }
-    // running maxima are kept in log2 units (score * scale_log2)
     bool grow = false;
     float mt[QB];
 #pragma unroll
@@ -283,38 +332,102 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
         }
       l_run[qb] += ls;
     }
+    // scores of blocks 2 ks and 2 ks + 1 are the keys 32 ks + 8 lg + (0..7):
+    // the k-slice 8 lg .. 8 lg + 7 of the PV MFMA with k-step ks
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 pb[QB];
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pb[qb][e] = (bf16)sc[qb][2 * ks][e];
-          pb[qb][4 + e] = (bf16)sc[qb][2 * ks + 1][e];
+          pb[ks][qb][e] = (bf16)sc[qb][2 * ks][e];
+          pb[ks][qb][4 + e] = (bf16)sc[qb][2 * ks + 1][e];
         }
-      // keys ks*32 + 4*lg + (0..3) and ks*32 + 16 + 4*lg + (0..3): half lg & 1
-      // of logical chunks 4*ks + lg/2 and 4*ks + 2 + lg/2 of row d
+  };
+  // O^T += V^T P^T for local tile i (probabilities in pb)
+  auto pv_update = [&](int st) __attribute__((always_inline)) {
+    const u32x4* Vcur = Vs + st * VSL;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      // keys 32 ks + 8 lg .. + 7 of row d: logical chunk 4 ks + lg.  The
+      // eight fragments of a k-step are requested before the first is used.
+      bf16x8 vf[DB];
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const int d = db * 16 + lc;
-        const int sw = att_swz<8>(d);
-        const unsigned* rowp = (const unsigned*)&Vcur[d * 8];
-        const int c0 = (4 * ks + (lg >> 1)) ^ sw, c1 = (4 * ks + 2 + (lg >> 1)) ^ sw;
-        const uint2 lo = *(const uint2*)(rowp + c0 * 4 + (lg & 1) * 2);
-        const uint2 hi = *(const uint2*)(rowp + c1 * 4 + (lg & 1) * 2);
-        const u32x4 vv = {lo.x, lo.y, hi.x, hi.y};
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+        vf[db] = __builtin_bit_cast(bf16x8, Vcur[d * 8 + ((4 * ks + lg) ^ att_vswz(d))]);
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
-          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb[qb], o[qb][db], 0, 0, 0);
-      }
+          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db], pb[ks][qb], o[qb][db], 0, 0, 0);
     }
+    att_mfma_pipeline<2 * DB, QB>();
   };
-  for (int i = 0; i < nt; i += NST) {
-    tile(i, Ks0, Vs0, 2);
-    if (i + 1 < nt) tile(i + 1, Ks1, Vs1, 0);
-    if (i + 2 < nt) tile(i + 2, Ks2, Vs2, 1);
+
+  // Ping-pong schedule.  A wave's tile i is an MFMA half M(i) = [PV(i - 1);
+  // S(i)] and a VALU half V(i) = softmax(i).  Iteration i has two half-steps,
+  // each after a barrier: group 0 runs M(i) then V(i), group 1 runs V(i - 1)
+  // then M(i), so on every SIMD one wave multiplies while the other one does
+  // its softmax.  Tile j is loaded into stage j % 4 at the first half-step of
+  // iteration j - 2 and must have landed before iteration j; its stage is last
+  // read in the second half-step of iteration j + 1 (group 1's PV(j)).
+  auto sync = [&]() __attribute__((always_inline)) {
+    // a plain barrier: this wave's LDS traffic done (the fence of
+    // __syncthreads would also drain the loads still in flight)
+    __builtin_amdgcn_s_waitcnt(ATT_LGKMCNT0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
+  };
+  // iteration i uses stage st = i % NST, passed as a constant so that stage
+  // offsets fold into the LDS instructions
+  auto head = [&](int i, int st) __attribute__((always_inline)) {
+    if (i < nt) {
+      if (i + 1 < nt) __builtin_amdgcn_s_waitcnt(ATT_VMCNT(KI + VI));
+      else __builtin_amdgcn_s_waitcnt(ATT_VMCNT(0));
+      asm volatile("" ::: "memory");    // no LDS access moves above the wait
+      fix_tail(i, st);
+    }
+    sync();
+    if (i + 2 < nt) issue(i + 2, (st + 2) % NST);
+  };
+  auto mfma_half = [&](int i, int st) __attribute__((always_inline)) {
+    if (i >= 1) pv_update((st + NST - 1) % NST);
+    if (i < nt) scores(st);
+  };
+  auto iter0 = [&](int i, int st) __attribute__((always_inline)) {
+    head(i, st);
+    mfma_half(i, st);
+    sync();
+    if (i < nt) softmax(i);
+  };
+  auto iter1 = [&](int i, int st) __attribute__((always_inline)) {
+    head(i, st);
+    if (i >= 1) softmax(i - 1);
+    sync();
+    mfma_half(i, st);
+  };
+  // one loop per group (same barrier count), so that each loop carries only
+  // its own registers from one iteration to the next
+  static_assert(NST == 4, "the loops below are unrolled by the stage count");
+  if (grp == 0) {
+    for (int i = 0; i <= nt; i += 4) {
+      iter0(i, 0);
+      if (i + 1 <= nt) iter0(i + 1, 1);
+      if (i + 2 <= nt) iter0(i + 2, 2);
+      if (i + 3 <= nt) iter0(i + 3, 3);
+    }
+  } else {
+    for (int i = 0; i <= nt; i += 4) {
+      iter1(i, 0);
+      if (i + 1 <= nt) iter1(i + 1, 1);
+      if (i + 2 <= nt) iter1(i + 2, 2);
+      if (i + 3 <= nt) iter1(i + 3, 3);
+    }
   }
 
   // o[qb][db][e]: dimension db*16 + 4*lg + e of query lc of block qb
@@ -336,8 +449,8 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
     return;
   }
 
-  // Split-KV: publish this split's (O, m, l); the last split of the
-  // (query tile, head) to arrive merges all of them and resets the counter.
+  // Split-KV: publish this split's unnormalised (O, m, l); attn_merge_kernel
+  // combines the splits.
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int qrow = rbeg + qt * QT + w * 16 * QB + qb * 16 + lc;
@@ -348,40 +461,48 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(SeqPlan pl, AttnArgs 
     for (int db = 0; db < DB; ++db) *(f32x4v*)(op + db * 16 + lg * 4) = o[qb][db];
     if (lg == 0) *(float2*)(a.ML + base * 2) = make_float2(m_run[qb], l_run[qb]);
   }
-  __syncthreads();
-  int* cnt = a.cnt + (size_t)gq * a.hq + h;
-  if (tid == 0) {
-    const int prev = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    last_flag = prev == nsplit - 1;
-    if (last_flag) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!last_flag) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// Merge of the split-KV partial results of the bf16 kernel, spread over the
+// whole GPU: thread t of a workgroup owns 4 consecutive dimensions of one
+// (query row, head); every split's partial is requested before any is used.
+// Splits are combined in split order, so the result is a function of the
+// row's own partials only.  Rows of sequences with one split were stored by
+// the attention kernel itself.
+constexpr int MERGE_ROWS = 8;
+template <int HD>
+__global__ __launch_bounds__(MERGE_ROWS * HD / 4) void attn_merge_kernel(SeqPlan pl, AttnArgs a) {
+  constexpr int TPR = HD / 4;                       // threads per row
+  const int row = blockIdx.x * MERGE_ROWS + threadIdx.x / TPR, h = blockIdx.y, d0 = (threadIdx.x % TPR) * 4;
+  if (row >= pl.rows) return;
+  const int s = plan_find(pl.row_off, pl.n, row);
+  const int nsplit = pl.nsplit[s];
+  if (nsplit == 1) return;
+  float2 ml[ATTN_MAX_SPLIT];
+  f32x4v part[ATTN_MAX_SPLIT];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qrow = rbeg + qt * QT + w * 16 * QB + qb * 16 + lc;
-    if (qrow >= rend) continue;
-    float M = -INFINITY;
-    for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, a.ML[(((size_t)sp * a.hq + h) * pl.rows + qrow) * 2]);
-    float den = 0.f;
-    f32x4 num[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db) num[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const size_t base = ((size_t)sp * a.hq + h) * pl.rows + qrow;
-      const float2 ml = *(const float2*)(a.ML + base * 2);
-      const float wgt = exp2f(ml.x - M);
-      den += wgt * ml.y;
-      const float* op = a.Opart + base * HD;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) num[db] += wgt * *(const f32x4v*)(op + db * 16 + lg * 4);
+  for (int sp = 0; sp < ATTN_MAX_SPLIT; ++sp) {
+    if (sp < nsplit) {
+      const size_t base = ((size_t)sp * a.hq + h) * pl.rows + row;
+      ml[sp] = *(const float2*)(a.ML + base * 2);
+      part[sp] = *(const f32x4v*)(a.Opart + base * HD + d0);
     }
-    const float inv = 1.0f / den;
-    const size_t ob = (size_t)qrow * a.ldo + h * HD;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) att_store4(a, ob + db * 16 + lg * 4, num[db] * inv);
   }
+  float M = -INFINITY;
+#pragma unroll
+  for (int sp = 0; sp < ATTN_MAX_SPLIT; ++sp)
+    if (sp < nsplit) M = fmaxf(M, ml[sp].x);
+  float den = 0.f;
+  f32x4v num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int sp = 0; sp < ATTN_MAX_SPLIT; ++sp) {
+    if (sp < nsplit) {
+      const float wgt = exp2f(ml[sp].x - M);
+      den += wgt * ml[sp].y;
+      num += wgt * part[sp];
+    }
+  }
+  att_store4(a, (size_t)row * a.ldo + h * HD + d0, num * (1.0f / den));
 }
 
 int attn_nsplit_for_keys(int nkeys) {
@@ -389,21 +510,31 @@ int attn_nsplit_for_keys(int nkeys) {
   return std::max(1, std::min(ATTN_MAX_SPLIT, (tiles + ATTN_TILES_PER_SPLIT - 1) / ATTN_TILES_PER_SPLIT));
 }
 
+int attn_qt_bf16(const int* rows, const int* nsplit, int n, int hq) {
+  for (int qt : {256, 128}) {
+    long wgs = 0;
+    for (int s = 0; s < n; ++s) wgs += (long)((rows[s] + qt - 1) / qt) * nsplit[s] * hq;
+    if (wgs >= ATTN_MIN_WGS) return qt;
+  }
+  return 64;
+}
+
+template <int HD>
+void attn_launch_hd(const SeqPlan& pl, const AttnArgs& a, dim3 grid, hipStream_t st) {
+  if (pl.qt == 256) attn_bf16_kernel<HD, 2, 8><<<grid, 512, 0, st>>>(pl, a);
+  else if (pl.qt == 128) attn_bf16_kernel<HD, 1, 8><<<grid, 512, 0, st>>>(pl, a);
+  else attn_bf16_kernel<HD, 1, 4><<<grid, 256, 0, st>>>(pl, a);
+  if (pl.max_split > 1)
+    attn_merge_kernel<HD><<<dim3((pl.rows + MERGE_ROWS - 1) / MERGE_ROWS, a.hq), MERGE_ROWS * HD / 4, 0, st>>>(pl, a);
+}
+
 int launch_attn_bf16(const SeqPlan& pl, const AttnArgs& a, hipStream_t st) {
   dim3 grid(pl.qt_off[pl.n], a.hq, pl.max_split);
   if (grid.x == 0) return 0;
-  if (pl.max_split > 1 && (!a.Opart || !a.ML || !a.cnt)) return 1;
-  if (pl.qt != 64 && pl.qt != 128) return 1;
-  const bool wide = pl.qt == 128;
-  if (a.hd == 128) {
-    if (wide) attn_bf16_kernel<128, 2><<<grid, 256, 0, st>>>(pl, a);
-    else attn_bf16_kernel<128, 1><<<grid, 256, 0, st>>>(pl, a);
-  } else if (a.hd == 64) {
-    if (wide) attn_bf16_kernel<64, 2><<<grid, 256, 0, st>>>(pl, a);
-    else attn_bf16_kernel<64, 1><<<grid, 256, 0, st>>>(pl, a);
-  } else {
-    return 1;
-  }
+  if (pl.max_split > 1 && (!a.Opart || !a.ML)) return 1;
+  if ((pl.qt != 256 && pl.qt != 128 && pl.qt != 64) || (a.hd != 128 && a.hd != 64)) return 1;
+  if (a.hd == 128) attn_launch_hd<128>(pl, a, grid, st);
+  else attn_launch_hd<64>(pl, a, grid, st);
   return 0;
 }
 

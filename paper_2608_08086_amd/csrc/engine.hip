@@ -38,10 +38,9 @@ archer_status fail(archer_status s, const std::string& msg) {
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
-  size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML, cnt;
+  size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML;
   size_t part, row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
   int ldcache, ldfresh, Mmax, Rmax, max_pos, ldq;
-  size_t n_cnt;
   size_t cache_layer_elems;
 };
 
@@ -99,10 +98,6 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
   const size_t part_rows = c->dtype == ARCHER_BF16 ? (size_t)L.Mmax : 1;
   L.Opart = take((size_t)kMaxSplit * hq * part_rows * hd * 4);
   L.ML = take((size_t)kMaxSplit * hq * part_rows * 2 * 4);
-  // split-KV arrival counters, one per (query tile, head); zeroed at init,
-  // and each launch leaves them zero again
-  L.n_cnt = ((size_t)L.Mmax + ATTN_QT_BF16_MIN - 1) / ATTN_QT_BF16_MIN + l->max_batch;
-  L.cnt = take(L.n_cnt * hq * 4);
   // split-K partials of response-row launches: max over the projections of ksplit * N
   size_t sn = 0;
   if (c->dtype == ARCHER_BF16) {
@@ -204,10 +199,14 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
   p.full = full ? 1 : 0;
   p.G = c->lim.resp_len;
   int rows = 0, tiles = 0;
-  for (int s = 0; s < p.n; ++s) rows += full ? c->plen[sel[s]] + p.G : p.G;
-  const int qt = is_bf16(c) ? attn_qt_bf16(rows) : ATTN_QT_F32;
+  int nrows[ARCHER_MAXB];
+  for (int s = 0; s < p.n; ++s) {
+    const int b = sel[s];
+    nrows[s] = full ? c->plen[b] + p.G : p.G;
+    p.nsplit[s] = is_bf16(c) ? attn_nsplit_for_keys(((c->plen[b] + 63) & ~63) + p.G) : 1;
+  }
+  const int qt = is_bf16(c) ? attn_qt_bf16(nrows, p.nsplit, p.n, c->cfg.n_heads) : ATTN_QT_F32;
   p.qt = qt;
-  rows = 0;
   for (int s = 0; s < p.n; ++s) {
     const int b = sel[s];
     p.seq[s] = b;
@@ -219,7 +218,6 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
     const int nr = full ? c->plen[b] + p.G : p.G;
     rows += nr;
     tiles += (nr + qt - 1) / qt;
-    p.nsplit[s] = is_bf16(c) ? attn_nsplit_for_keys(((c->plen[b] + 63) & ~63) + p.G) : 1;
     p.max_split = std::max(p.max_split, p.nsplit[s]);
   }
   p.row_off[p.n] = rows;
@@ -320,7 +318,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.ldcache = L.ldcache;
       a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
       a.O = c->at<char>(L.O); a.O2 = lo_part(c, L.O2); a.ldo = hq * hd;
-      a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML); a.cnt = c->at<int>(L.cnt);
+      a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML);
       a.hq = hq; a.hkv = hkv; a.hd = hd;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       const double bytes = (double)rows * hq * hd * es * 2 + kv_keys * hkv * hd * es * 2;
@@ -477,7 +475,6 @@ archer_status archer_init(const archer_model_cfg* cfg, const archer_weights* w, 
   }
   launch_rope_table(c->at<float2>(L.rope), L.max_pos, cfg->head_dim, (double)cfg->rope_theta, c->stream);
   hipError_t he = hipMemsetAsync(c->at<int>(L.err), 0, 256, c->stream);
-  if (he == hipSuccess) he = hipMemsetAsync(c->at<int>(L.cnt), 0, L.n_cnt * cfg->n_heads * 4, c->stream);
   if (he == hipSuccess) he = hipGetLastError();
   if (he == hipSuccess) he = hipStreamSynchronize(c->stream);
   if (he != hipSuccess) {
@@ -671,9 +668,7 @@ static int op_attn_nsplit(int dtype, int nk) { return dtype == ARCHER_BF16 ? att
 size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32_t hd, int32_t nk) {
   if (Mq < 1 || Hq < 1 || hd < 1 || nk < 1) return 0;
   const int ns = op_attn_nsplit(dtype, nk);
-  const size_t qtiles = (size_t)(Mq + ATTN_QT_BF16_MIN - 1) / ATTN_QT_BF16_MIN;
-  return align_up((size_t)ns * Hq * Mq * hd * 4, 256) + align_up((size_t)ns * Hq * Mq * 2 * 4, 256) +
-         qtiles * Hq * 4 + 256;
+  return align_up((size_t)ns * Hq * Mq * hd * 4, 256) + align_up((size_t)ns * Hq * Mq * 2 * 4, 256);
 }
 
 archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd, const void* Q,
@@ -692,7 +687,7 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
   memset(&p, 0, sizeof(p));
   p.n = 1; p.full = 0; p.G = nk2; p.rows = Mq;
   p.row_off[1] = Mq; p.p_len[0] = nk1;
-  const int qt = dtype == ARCHER_BF16 ? attn_qt_bf16(Mq) : ATTN_QT_F32;
+  const int qt = dtype == ARCHER_BF16 ? attn_qt_bf16(&Mq, &ns, 1, Hq) : ATTN_QT_F32;
   p.qt = qt;
   p.qt_off[1] = (Mq + qt - 1) / qt;
   p.nsplit[0] = ns;
@@ -708,12 +703,8 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
   hipStream_t st = (hipStream_t)hip_stream;
   if (ns > 1) {
     const size_t o1 = align_up((size_t)ns * Hq * Mq * hd * 4, 256);
-    const size_t o2 = o1 + align_up((size_t)ns * Hq * Mq * 2 * 4, 256);
     a.Opart = (float*)workspace;
     a.ML = (float*)((char*)workspace + o1);
-    a.cnt = (int*)((char*)workspace + o2);
-    // the counters are cleared by a kernel (not a memset node) on every call
-    launch_fill_i32(a.cnt, 0, (size_t)p.qt_off[1] * Hq, st);
   }
   int rc;
   if (dtype == ARCHER_BF16) {

@@ -36,21 +36,19 @@ struct AttnArgs {
   const void* Kf; const void* Vtf; int ldfresh;
   void* O; void* O2; int ldo;            // [rows][ldo]: hi part, lo part (or null)
   float* Opart; float* ML;               // split partials [max_split][Hq][rows][hd], [max_split][Hq][rows][2]
-  int* cnt;                              // [query tiles][Hq] arrival counters, zero between launches
   int hq, hkv, hd;
   float scale_log2;                      // log2(e) / sqrt(hd)
 };
 
-// query tile (rows per attention workgroup) of each attention kernel
-// bf16: 64 query rows per workgroup (one 16-row block per wave) for passes of
-// fewer than ATTN_QT_WIDE_ROWS rows, 128 (two blocks per wave) otherwise.  The
-// result of a query row does not depend on the tiling (every softmax decision
-// is per query).
-constexpr int ATTN_QT_BF16_MIN = 64;
-constexpr int ATTN_QT_WIDE_ROWS = 512;
-inline int attn_qt_bf16(int rows) { return rows >= ATTN_QT_WIDE_ROWS ? 128 : 64; }
+// Query tile (rows per attention workgroup) of the bf16 kernel: 256 rows (8
+// waves of 32, two waves per SIMD), 128 rows (8 waves of 16) or 64 rows (4
+// waves of 16).  The largest tile that still gives the pass enough
+// workgroups is used; the result of a query row does not depend on the tiling
+// (every softmax decision is per query).
 constexpr int ATTN_MAX_SPLIT = 8;          // split-KV bound (workspace is sized for it)
-constexpr int ATTN_TILES_PER_SPLIT = 16;   // 64-key tiles per split, at least
+constexpr int ATTN_TILES_PER_SPLIT = 8;    // 64-key tiles per split (target)
+constexpr int ATTN_MIN_WGS = 256;          // workgroups wanted per pass (one per CU)
+int attn_qt_bf16(const int* rows, const int* nsplit, int n, int hq);
 constexpr int ATTN_QT_F32 = 1;
 
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
@@ -74,7 +72,7 @@ void launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
 // GEMM_NCFG .. GEMM_NCFG+GEMM_NCFG_LDS-1: direct-to-LDS multistage kernel
 // (gemm_lds.hip).  All give the same bits for the same (N, K) split.
 constexpr int GEMM_NCFG = 7;
-constexpr int GEMM_NCFG_LDS = 5;
+constexpr int GEMM_NCFG_LDS = 9;
 int gemm_ksplit(int N, int K);
 bool gemm_lds_cfg_ok(int c, const GemmArgs& a);
 int gemm_lds_tiles(int c, const GemmArgs& a);
@@ -90,6 +88,6 @@ int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st);
 // Split-KV count for a sequence with nkeys keys (padded key space); the same
 // function is used by every pass so results do not depend on the batch or pass.
 int attn_nsplit_for_keys(int nkeys);
-// Attention over the plan's sequences; split-KV partials are merged inside the kernel.
+// Attention over the plan's sequences; split-KV partials are merged by a second kernel.
 int launch_attn_bf16(const SeqPlan& pl, const AttnArgs& a, hipStream_t st);
 int launch_attn_f32(const SeqPlan& pl, const AttnArgs& a, int max_keys, hipStream_t st);
