@@ -43,7 +43,8 @@ KERNEL_OF_CLASS = {
     "gemm_gateup": "gemm_lds_kernel<128, 192, 2, 2, 4, 2, true, 0>",
     "gemm_down": "gemm_lds_kernel<128, 128, 2, 2, 4, 1, true, 2> + gemm_reduce_kernel<1, bf16>",
     "gemm_head": "gemm_lds_kernel<128, 128, 2, 2, 4, 0, true, 0>",
-    "attn": "attn_bf16_kernel<128, 1> (cached passes), attn_bf16_kernel<128, 2> (refresh passes)",
+    "attn": "attn_bf16_kernel<128, QB, NW> + attn_merge_kernel<128> (CachedForward passes)",
+    "attn_full": "attn_bf16_kernel<128, QB, NW> + attn_merge_kernel<128> (FullForward passes)",
     "norm": "rmsnorm_kernel<bf16>", "embed": "embed_kernel<bf16>", "decide": "rowstats_kernel + select_kernel",
 }
 # classes whose bf16 launches multiply two-term activations (two MFMAs per fragment)
@@ -131,6 +132,87 @@ def cpu_baseline(w, lens, T, K_refresh, policy, sample_layers=9):
             "measured_s": round(measured, 2)}
 
 
+def sweep(kind, reps=10):
+    """Per-update and radius sweeps on the LLaDA-8B-shaped random-init model
+    (the paper's prompt-length and radius studies, App. F and App. B):
+      update:   FullForward vs CachedForward per-update time at G = 256 for
+                P in {128, 256, 512, 1024, 2048} (mean of `reps` synchronised calls)
+      response: the same at P = 512 for G in {64, 128, 256, 512}
+      radius:   whole decodes (P 512, G 256, T 256) under the age and Hamming
+                rules for K in {1, 2, 4, 8, 16, 32, never}: steps/s, realised refresh fraction
+    Prints one JSON object."""
+    import numpy as np
+    import torch
+
+    from paper_2608_08086_amd import archer
+    from synth.device import model_weights_cuda
+    from synth.gen import prompts
+    from synth.workloads import get_workload
+
+    w = get_workload("llada_p512")
+    m = w.model
+    Wd = model_weights_cuda(m, seed=w.weight_seed)
+    torch.cuda.synchronize()
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / n * 1e3
+
+    def per_update(P, G):
+        ctx = archer.Context(m, Wd, 1, P, P, G)
+        wl = w.with_decode(prompt_len=P, resp_len=G)
+        prompt = torch.from_numpy(prompts(wl, [P])[0].astype(np.int32)).cuda()
+        resp = torch.full((1, G), m.mask_id, dtype=torch.int32, device="cuda")
+        resp[0, : G // 4] = torch.arange(G // 4, dtype=torch.int32, device="cuda")
+        logits = ctx.new_logits(1)
+        full = timed(lambda: ctx.refresh_prompt(prompt, [P], resp, logits=logits), reps)
+        cached = timed(lambda: ctx.step(resp, logits=logits), 2 * reps)
+        ctx.close()
+        return {"P": P, "G": G, "full_ms": round(full, 3), "cached_ms": round(cached, 3),
+                "speedup": round(full / cached, 3), "ideal_speedup": round((P + G) / G, 3),
+                "measured_over_ideal": round(full / cached / ((P + G) / G), 3)}
+
+    out = {"sweep": kind, "model": "LLaDA-8B shape (32 layers, d 4096, 32 heads x 128, F 12288, V 126464), "
+           "bf16, random init", "data": "synthetic"}
+    if kind == "update":
+        out["rows"] = [per_update(P, 256) for P in (128, 256, 512, 1024, 2048)]
+        log(json.dumps(out["rows"]))
+    elif kind == "response":
+        out["rows"] = [per_update(512, G) for G in (64, 128, 256, 512)]
+    elif kind == "radius":
+        P, G, T = 512, 256, 256
+        ctx = archer.Context(m, Wd, 1, P, P, G)
+        prompt = torch.from_numpy(prompts(w, [P])[0].astype(np.int32)).cuda()
+        resp = torch.full((1, G), m.mask_id, dtype=torch.int32, device="cuda")
+        rows = []
+        for pol_name, pol in (("age", archer.AGE), ("hamming", archer.HAMMING)):
+            for K in (1, 2, 4, 8, 16, 32, archer.NEVER):
+                def run():
+                    resp.fill_(m.mask_id)
+                    return ctx.decode(prompt, [P], resp, policy=pol, K=K, steps=T, k=1, tau=0.1, trace=True)
+                run()
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                _, tr = run()
+                torch.cuda.synchronize()
+                wall = time.perf_counter() - t0
+                q = int(tr["refreshed"].sum().item()) / T
+                rows.append({"policy": pol_name, "K": "never" if K == archer.NEVER else K,
+                             "steps_per_s": round(T / wall, 2), "decode_s": round(wall, 4),
+                             "refresh_fraction": round(q, 4)})
+                log(json.dumps(rows[-1]))
+        out["rows"] = rows
+        out["config"] = {"P": P, "G": G, "T": T, "k": 1, "tau": 0.1}
+    else:
+        raise SystemExit(f"unknown sweep {kind}")
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -144,7 +226,12 @@ def main():
                     help="profiling only: override the workload's denoising steps per decode")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="profiling only: end with a 1 GiB device copy (known HBM traffic) for PMC scaling")
+    ap.add_argument("--sweep", choices=["update", "response", "radius"],
+                    help="run a sweep instead of the throughput bench (prints its own JSON object)")
     args = ap.parse_args()
+    if args.sweep:
+        sweep(args.sweep)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}); run it with --gpus 1", file=sys.stderr)
@@ -196,13 +283,14 @@ def main():
     log("bench: warm-up ms per class " + ", ".join(f"{n}={v['ms']:.1f}" for n, v in warm.items() if v["launches"]))
 
     torch.cuda.synchronize()
-    ctx.timing_begin([archer.K_NAMES.index(dom)])
+    ctx.timing_begin(sorted({archer.K_NAMES.index(dom), archer.K_ATTN}))
     t0 = time.perf_counter()
     for _ in range(args.steps):
         _, tr = decode(pol, Kr)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    tim = ctx.timing_end()[dom]
+    tims = ctx.timing_end()
+    tim = tims[dom]
     refreshed = int(tr["refreshed"].sum().item())
     log(f"bench: {args.steps} decodes in {wall:.3f}s -> {args.steps * T / wall:.1f} steps/s; "
         f"refreshes per decode {refreshed}/{T * B}")
@@ -243,6 +331,21 @@ def main():
                  "executed_mfma_frac": round(exec_flops / sec / 1e12 / peak_f, 4),
                  "timing": "HIP events around each launch of the class, on the library's stream"})
 
+    # the cache-reading attention of the cached passes, against the HBM roofline
+    at = tims["attn"]
+    att_roof = None
+    if at["launches"] and m.dtype == "bf16":
+        asec = at["ms"] / 1e3
+        att_roof = {"bound": "hbm", "achieved": round(at["bytes"] / asec / 1e9, 1), "peak": PEAK_HBM_GBS,
+                    "unit": "GB/s", "frac": round(at["bytes"] / asec / 1e9 / PEAK_HBM_GBS, 4),
+                    "kernel": KERNEL_OF_CLASS["attn"], "class": "attn", "launches": at["launches"],
+                    "avg_us": round(at["ms"] * 1e3 / at["launches"], 2),
+                    "algorithmic_bytes_per_launch": round(at["bytes"] / at["launches"]),
+                    "algorithmic_flops_per_launch": round(at["flops"] / at["launches"]),
+                    "algorithmic_tflops": round(at["flops"] / asec / 1e12, 2),
+                    "mfma_frac": round(at["flops"] / asec / 1e12 / PEAK_BF16_TFLOPS, 4),
+                    "timing": "HIP events around each launch (attention + split-KV merge), on the library's stream"}
+
     out = {
         "metric": "denoising steps/s + response tok/s at 1 GPU; speedup vs full refresh; % roofline",
         "value": round(sps, 3), "unit": "steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -258,6 +361,7 @@ def main():
         "full_refresh_steps_per_s": None if full_sps is None else round(full_sps, 3),
         "speedup_vs_full_refresh": None if full_sps is None else round(sps / full_sps, 3),
         "roofline": roof,
+        "attention_roofline": att_roof,
         "warmup_ms_by_class": {n: round(v["ms"], 2) for n, v in warm.items() if v["launches"]},
     }
     if not args.no_cpu_baseline:

@@ -50,8 +50,9 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
 
 /* Kernel classes for timing. */
 enum {
-  ARCHER_K_EMBED = 0, ARCHER_K_NORM = 1, ARCHER_K_GEMM_QKV = 2, ARCHER_K_ATTN = 3,
-  ARCHER_K_ATTN_MERGE = 4 /* no launches: the split-KV merge runs inside the attention kernel */,
+  ARCHER_K_EMBED = 0, ARCHER_K_NORM = 1, ARCHER_K_GEMM_QKV = 2,
+  ARCHER_K_ATTN = 3 /* attention of CachedForward passes (with its split-KV merge) */,
+  ARCHER_K_ATTN_FULL = 4 /* attention of FullForward (refresh) passes */,
   ARCHER_K_GEMM_O = 5, ARCHER_K_GEMM_GATEUP = 6,
   ARCHER_K_GEMM_DOWN = 7, ARCHER_K_GEMM_HEAD = 8, ARCHER_K_DECIDE = 9,
   ARCHER_K_COUNT = 10

@@ -24,9 +24,9 @@ OK, E_ARG, E_SHAPE, E_STATE, E_HIP, E_WORKSPACE, E_UNSUPPORTED = 0, -1, -2, -3, 
 BF16, FP32 = 0, 1
 HAMMING, AGE, ALWAYS = 0, 1, 2
 NEVER = 2**31 - 1
-K_EMBED, K_NORM, K_GEMM_QKV, K_ATTN, K_ATTN_MERGE, K_GEMM_O, K_GEMM_GATEUP, K_GEMM_DOWN, K_GEMM_HEAD, K_DECIDE = range(10)
+K_EMBED, K_NORM, K_GEMM_QKV, K_ATTN, K_ATTN_FULL, K_GEMM_O, K_GEMM_GATEUP, K_GEMM_DOWN, K_GEMM_HEAD, K_DECIDE = range(10)
 K_COUNT = 10
-K_NAMES = ["embed", "norm", "gemm_qkv", "attn", "attn_merge", "gemm_o", "gemm_gateup", "gemm_down",
+K_NAMES = ["embed", "norm", "gemm_qkv", "attn", "attn_full", "gemm_o", "gemm_gateup", "gemm_down",
            "gemm_head", "decide"]
 
 EXPORTED = [

@@ -321,11 +321,13 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML);
       a.hq = hq; a.hkv = hkv; a.hd = hd;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
-      const double bytes = (double)rows * hq * hd * es * 2 + kv_keys * hkv * hd * es * 2;
+      // Q read once, O written once (two terms for bf16), every real key's K
+      // and V read once
+      const double bytes = (double)rows * hq * hd * es * (a.O2 ? 3 : 2) + kv_keys * hkv * hd * es * 2;
       const double flops = 4.0 * attn_q_keys * hq * hd;
       int max_keys = 0;
       for (int s = 0; s < pl.n; ++s) max_keys = std::max(max_keys, ((pl.p_len[s] + 63) & ~63) + pl.G);
-      st = timed(c, ARCHER_K_ATTN, bytes, flops, [&] {
+      st = timed(c, full ? ARCHER_K_ATTN_FULL : ARCHER_K_ATTN, bytes, flops, [&] {
         return is_bf16(c) ? launch_attn_bf16(pl, a, c->stream) : launch_attn_f32(pl, a, max_keys, c->stream);
       });
       if (st) return st;
