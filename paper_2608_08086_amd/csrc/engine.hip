@@ -41,10 +41,12 @@ struct Layout {
   size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML;
   size_t part, row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
   int ldcache, ldfresh, Mmax, Rmax, max_pos, ldq;
+  int part_rows;   // rows the split-K partial buffer holds
   size_t cache_layer_elems;
 };
 
 constexpr int kMaxSplit = ATTN_MAX_SPLIT;
+constexpr int kPartRowsFull = 4608;
 
 std::string check_cfg(const archer_model_cfg* c, const archer_limits* l) {
   if (!c || !l) return "null cfg or limits";
@@ -108,7 +110,10 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
       if (S > 1) sn = std::max(sn, (size_t)S * nk[0]);
     }
   }
-  L.part = take(sn * L.Rmax * 4);
+  // split-K partials: every cached pass, and full passes of up to
+  // kPartRowsFull rows (larger ones run the slices folded in one workgroup)
+  L.part_rows = std::min(L.Mmax, std::max(L.Rmax, kPartRowsFull));
+  L.part = take(sn * L.part_rows * 4);
   L.row_pos = take((size_t)L.Mmax * 4);
   L.row_dst = take((size_t)L.Mmax * 4);
   L.out_row = take((size_t)L.Rmax * 4);
@@ -229,7 +234,7 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
 archer_status gemm(archer_ctx* c, int cls, int epi, GemmArgs a) {
   if (is_bf16(c)) {
     a.ksplit = gemm_ksplit(a.N, a.K);
-    if (a.M <= c->L.Rmax) a.part = c->at<float>(c->L.part);
+    if (a.M <= c->L.part_rows) a.part = c->at<float>(c->L.part);
   }
   const double es = (double)c->esz;
   double bytes = (double)a.M * a.K * es * (a.A2 ? 2 : 1) + (double)a.N * a.K * es;

@@ -18,11 +18,11 @@
 // SwiGLU pair, and each wave's columns are taken from both halves of the tile
 // so that a pair sits in one lane.
 //
-// Tile order.  Workgroups are dispatched round-robin over the 8 XCDs.  The
-// linear workgroup id is laid out so that all M tiles of one (N tile, slice)
-// group run on the same XCD back to back (the weight tile is read from HBM
-// once and then hits that XCD's L2) and, with 8 slices, each XCD owns one K
-// slice (its slice of A stays in its L2).
+// Tile order (tile_of in gemm_common.h).  Workgroups are dispatched
+// round-robin over the 8 XCDs; each XCD owns every eighth (N tile, slice)
+// group and walks blocks of its groups times all M tiles, so that the tiles
+// it runs at once share both operands through its L2 (with 8 slices each XCD
+// owns one K slice, whose part of A stays in its L2).
 #include <algorithm>
 
 #include "launch.h"
@@ -328,9 +328,11 @@ bool gemm_cfg_ok(int cfg, const GemmArgs& a, int epi) {
 }
 
 int gemm_partial_wanted(int cfg, const GemmArgs& a) {
-  const int tiles = cfg >= GEMM_NCFG ? gemm_lds_tiles(cfg - GEMM_NCFG, a)
-                                     : (a.N / kCfgBN[cfg]) * ((a.M + kCfgBM[cfg] - 1) / kCfgBM[cfg]);
-  return a.ksplit > 1 && tiles < 512;
+  // Measured on MI355X (LLaDA-8B projections, M = 256 .. 4352): one workgroup
+  // per slice with a separate reduction is at least as fast as folding the
+  // slices into one workgroup whenever a partial buffer is available.
+  (void)cfg;
+  return a.ksplit > 1;
 }
 
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st) {

@@ -96,16 +96,28 @@ __device__ __forceinline__ int logical_col(const GemmArgs& a, int tile_n, int r)
   return second ? w + a.N / 2 : w;
 }
 
-// XCD-aware decomposition of the linear workgroup id (see the file comment).
+// XCD-aware decomposition of the linear workgroup id.  Workgroups are
+// dispatched round-robin over the 8 XCDs, so XCD x runs ids x, x + 8, ...;
+// it owns the (N tile, slice) groups g with g mod 8 = x.  With few M tiles
+// (M up to 1024 rows) all M tiles of one group run back to back, so a weight
+// tile is read from memory once and then hits the XCD's L2.  With many M
+// tiles, its workgroups walk blocks of 8 of its groups and inside a block all
+// M tiles, the groups varying fastest: the workgroups an XCD runs at once then
+// cover a few M tiles times 8 weight tiles, so that the activation rows are
+// not re-read from memory for every weight tile.
 __device__ __forceinline__ bool tile_of(int id, int n_tiles, int m_tiles, int S, int* tn, int* tm, int* z) {
   const int groups = n_tiles * S;
-  const int g8 = id % 8, rest = id / 8;
-  const int gblk = rest / m_tiles, m = rest % m_tiles;
-  const int group = gblk * 8 + g8;
-  if (group >= groups) return false;
+  const int x = id % 8, rest = id / 8;
+  const int gx = (groups - x + 7) / 8;                 // groups owned by XCD x
+  if (rest >= gx * m_tiles) return false;
+  const int gb = m_tiles > 8 ? 8 : 1;                  // groups per block
+  const int blk = rest / (gb * m_tiles);
+  const int nb = min(gb, gx - blk * gb);               // groups in this block
+  const int within = rest - blk * gb * m_tiles;
+  const int group = (blk * gb + within % nb) * 8 + x;
   *tn = group / S;
   *z = group % S;
-  *tm = m;
+  *tm = within / nb;
   return true;
 }
 
