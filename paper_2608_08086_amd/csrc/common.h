@@ -86,6 +86,30 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
+// RMSNorm of one row of x (d columns) into a two-term activation row, by a
+// block of 256 threads: thread t owns the float4 chunks at t * 4 + k * 1024.
+// Shared by the stand-alone RMSNorm kernel and the split-K reduction that
+// fuses it, so that both give the same bits.
+template <class T>
+__device__ __forceinline__ void rms_normalize_row(const float* xr, const float* gain, T* orow, T* orow2, int d,
+                                                  float eps, float* red) {
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    const float4 v = *(const float4*)(xr + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    const float4 v = *(const float4*)(xr + c);
+    const float4 g = *(const float4*)(gain + c);
+    store_act<T>(orow, orow2, c + 0, v.x * inv * g.x);
+    store_act<T>(orow, orow2, c + 1, v.y * inv * g.y);
+    store_act<T>(orow, orow2, c + 2, v.z * inv * g.z);
+    store_act<T>(orow, orow2, c + 3, v.w * inv * g.w);
+  }
+}
+
 // dst-row encoding of the K/V destination of a pass row: >= 0 is a row of the
 // fresh (response) K/V buffers, < 0 encodes prompt-cache row (-1 - v).
 __device__ __forceinline__ bool dst_is_fresh(int v) { return v >= 0; }

@@ -231,15 +231,19 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
   return p;
 }
 
-archer_status gemm(archer_ctx* c, int cls, int epi, GemmArgs a) {
-  if (is_bf16(c)) {
-    a.ksplit = gemm_ksplit(a.N, a.K);
-    if (a.M <= c->L.part_rows) a.part = c->at<float>(c->L.part);
-  }
+// split-K slice count and partial buffer of a bf16 projection
+void gemm_prepare(archer_ctx* c, GemmArgs& a) {
+  if (!is_bf16(c)) return;
+  a.ksplit = gemm_ksplit(a.N, a.K);
+  if (a.M <= c->L.part_rows) a.part = c->at<float>(c->L.part);
+}
+
+archer_status gemm(archer_ctx* c, int cls, int epi, GemmArgs& a) {
+  gemm_prepare(c, a);
   const double es = (double)c->esz;
   double bytes = (double)a.M * a.K * es * (a.A2 ? 2 : 1) + (double)a.N * a.K * es;
   if (epi == EPI_STORE) bytes += (double)a.M * a.N * 4;
-  else if (epi == EPI_RESID) bytes += 2.0 * a.M * a.N * 4;
+  else if (epi == EPI_RESID) bytes += 2.0 * a.M * a.N * 4 + (gemm_fuses_norm(a) ? (double)a.M * a.N * es * 2 : 0.0);
   else if (epi == EPI_SWIGLU) bytes += (double)a.M * (a.N / 2) * es * (a.H2 ? 2 : 1);
   else bytes += (double)a.M * a.N * es;
   const double flops = 2.0 * a.M * a.N * a.K;
@@ -300,8 +304,16 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   for (int s = 0; s < pl.n; ++s)
     attn_q_keys += (double)(pl.row_off[s + 1] - pl.row_off[s]) * (pl.p_len[s] + pl.G);
 
+  // RMSNorms whose input is the residual just updated by a split-K GEMM run
+  // inside that GEMM's reduction (same arithmetic as the stand-alone kernel)
+  auto fuse_norm = [&](GemmArgs& a, const float* gain) {
+    if (!is_bf16(c)) return;
+    a.ngain = gain; a.nout = act; a.nout2 = act2; a.neps = m.rms_eps;
+  };
+  bool normed = false;   // attn_norm of the current layer already applied
   for (int l = 0; l < m.n_layers; ++l) {
-    if ((st = norm(c->attn_norm[l], 0, rows, act, act2))) return st;
+    if (!normed && (st = norm(c->attn_norm[l], 0, rows, act, act2))) return st;
+    normed = false;
     {
       GemmArgs a = gargs(act, d, c->w_qkv[l], d, rows, qkv_n, d);
       a.A2 = act2;
@@ -341,9 +353,12 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       GemmArgs a = gargs(c->at<char>(L.O), hq * hd, c->w_o[l], hq * hd, rows, d, hq * hd);
       a.A2 = lo_part(c, L.O2);
       a.X = x; a.ldx = d;
+      fuse_norm(a, c->mlp_norm[l]);
       if ((st = gemm(c, ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
+      normed = gemm_fuses_norm(a);
     }
-    if ((st = norm(c->mlp_norm[l], 0, rows, act, act2))) return st;
+    if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2))) return st;
+    normed = false;
     {
       GemmArgs a = gargs(act, d, c->w_gate[l], d, rows, 2 * F, d);
       a.A2 = act2;
@@ -355,7 +370,9 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       GemmArgs a = gargs(c->at<char>(L.H), F, c->w_down[l], F, rows, d, F);
       a.A2 = lo_part(c, L.H2);
       a.X = x; a.ldx = d;
+      if (l + 1 < m.n_layers) fuse_norm(a, c->attn_norm[l + 1]);
       if ((st = gemm(c, ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
+      normed = gemm_fuses_norm(a);
     }
   }
   const int nresp = pl.n * pl.G;

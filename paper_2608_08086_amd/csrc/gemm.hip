@@ -227,8 +227,44 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
   }
 }
 
+// Split-K reduction of an EPI_RESID GEMM fused with the RMSNorm of the
+// updated rows: one block per row; thread t owns the same float4 chunks as in
+// rms_normalize_row, adds the slices in slice order into X (as
+// gemm_reduce_kernel does) and then normalises the row it has just written.
+template <class T>
+__global__ __launch_bounds__(256) void gemm_reduce_resid_norm_kernel(GemmArgs a) {
+  __shared__ float red[16];
+  const int row = blockIdx.x;
+  const size_t plane = (size_t)a.M * a.N;
+  const float* pr = a.part + (size_t)row * a.N;
+  float* xr = a.X + (size_t)row * a.ldx;
+  for (int c = threadIdx.x * 4; c < a.N; c += blockDim.x * 4) {
+    // all slices are requested before they are summed (in slice order)
+    f32x4 sl[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      if (s < a.ksplit) sl[s] = *(const f32x4*)(pr + s * plane + c);
+    f32x4 v = sl[0];
+#pragma unroll
+    for (int s = 1; s < 8; ++s)
+      if (s < a.ksplit) v += sl[s];
+    f32x4 xv = *(const f32x4*)(xr + c);
+    xv += v;
+    *(f32x4*)(xr + c) = xv;
+  }
+  // each thread reads back only the elements it wrote
+  rms_normalize_row<T>(xr, a.ngain, (T*)a.nout + (size_t)row * a.N,
+                       a.nout2 ? (T*)a.nout2 + (size_t)row * a.N : nullptr, a.N, a.neps, red);
+}
+
 template <int EPI>
 static void reduce_epi(const GemmArgs& a, hipStream_t st) {
+  if constexpr (EPI == EPI_RESID) {
+    if (a.ngain) {
+      gemm_reduce_resid_norm_kernel<bf16><<<a.M, 256, 0, st>>>(a);
+      return;
+    }
+  }
   const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
   const long total = (long)a.M * npair;
   gemm_reduce_kernel<EPI, bf16><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(a);
@@ -347,6 +383,12 @@ int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipS
     default: return 1;
   }
   return 0;
+}
+
+bool gemm_fuses_norm(const GemmArgs& a) {
+  if (!a.ngain || !a.part || a.N % 4 || a.ldx % 4 || a.ksplit > 8) return false;
+  const int cfg = gemm_pick_cfg(a, EPI_RESID);
+  return gemm_partial_wanted(cfg, a) != 0;
 }
 
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st) {

@@ -89,24 +89,8 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, co
     ri = pl.row_off[s] + (pl.full ? pl.p_len[s] : 0) + r;
     if (threadIdx.x == 0) out_row[ro] = pl.seq[s] * pl.G + r;
   }
-  const float* xr = x + (size_t)ri * d;
-  float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
-    const float4 v = *(const float4*)(xr + c);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-  }
-  ss = block_sum(ss, red);
-  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  T* orow = out + (size_t)ro * d;
-  T* orow2 = out2 ? out2 + (size_t)ro * d : nullptr;
-  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
-    const float4 v = *(const float4*)(xr + c);
-    const float4 g = *(const float4*)(gain + c);
-    store_act<T>(orow, orow2, c + 0, v.x * inv * g.x);
-    store_act<T>(orow, orow2, c + 1, v.y * inv * g.y);
-    store_act<T>(orow, orow2, c + 2, v.z * inv * g.z);
-    store_act<T>(orow, orow2, c + 3, v.w * inv * g.w);
-  }
+  rms_normalize_row<T>(x + (size_t)ri * d, gain, out + (size_t)ro * d, out2 ? out2 + (size_t)ro * d : nullptr, d,
+                       eps, red);
 }
 
 template <class T>

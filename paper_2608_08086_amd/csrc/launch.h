@@ -21,6 +21,9 @@ struct GemmArgs {
   float* part;                           // fp32 partials [ksplit][M][N] for the per-slice launch, or null
   float* C; int ldc; const int* out_row; // EPI_STORE
   float* X; int ldx;                     // EPI_RESID
+  // EPI_RESID with a split-K reduction: optionally RMSNorm the updated rows of
+  // X (gain ngain, epsilon neps) into the two-term activation (nout, nout2), [M][N]
+  const float* ngain; void* nout; void* nout2; float neps;
   void* H; void* H2; int ldh;            // EPI_SWIGLU: H = hi part, H2 = lo part (or null)
   // EPI_QKV
   void* Qb; int ldq;                     // Q [Hq][ldq][hd]
@@ -83,6 +86,9 @@ int gemm_pick_cfg(const GemmArgs& a, int epi);
 int gemm_partial_wanted(int cfg, const GemmArgs& a);
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st);
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);
+// true if launch_gemm_bf16 runs this EPI_RESID GEMM with a separate split-K
+// reduction, which then also applies the RMSNorm described by a.ngain
+bool gemm_fuses_norm(const GemmArgs& a);
 int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st);
 
 // Split-KV count for a sequence with nkeys keys (padded key space); the same
