@@ -2,18 +2,19 @@
 // row of a sequence attends to that sequence's cached prompt keys followed by
 // its fresh response keys, with no mask other than key validity.
 //
-// bf16 kernel: flash-style online softmax with MFMA.  A workgroup of NW
-// wave64s (two per SIMD, so that one wave's softmax overlaps the other's
-// MFMAs and LDS reads) owns 16 * QB * NW query rows of one (sequence, query
-// head) -- a whole 256-row response block -- and a contiguous range of 64-key
-// tiles (split-KV over blockIdx.z; the last split to finish merges the
-// partial results).  Every K/V tile staged in LDS serves all 256 queries.  Per tile, K [64][hd] and V^T [hd][64] are
-// loaded straight into one of three LDS stages, two tiles ahead of the one
-// being computed.  Scores are formed transposed, S^T = K Q^T, so
-// that a lane holds 4 keys x 1 query per 16x16 block; the probabilities of two
-// key blocks then form exactly the B operand of O^T = V^T P^T with the key
-// order permuted identically on both operands (the contraction is order-free),
-// which removes any register shuffle between the two MFMA stages.  Row
+// bf16 kernel: flash-style online softmax with MFMA.  A workgroup owns
+// 16 * QB * NW query rows (256, 128 or 64) of one (sequence, query head) and
+// a contiguous range of 64-key tiles; with split-KV the splits' unnormalised
+// partial results are combined by attn_merge_kernel.  With 8 waves, two waves
+// share each SIMD and run a ping-pong schedule: while one multiplies (scores
+// of tile i and P V of tile i - 1) the other does its softmax, separated by
+// one barrier per half tile.  K [64][hd] and V^T [hd][64] tiles are loaded
+// straight into one of four LDS stages, two tiles ahead of the one being
+// computed.  Scores are formed transposed, S^T = K Q^T, so that a lane holds
+// 4 keys x 1 query per 16x16 block; the K rows of each MFMA block are
+// permuted (att_key_row) so that the probabilities a lane holds for two key
+// blocks are 8 consecutive keys, which is exactly the B operand of
+// O^T = V^T P^T and whose V^T partner is one 16-byte LDS read.  Row
 // statistics need only two xor-shuffles across the four lane groups.
 #include <algorithm>
 
@@ -529,7 +530,7 @@ void attn_launch_hd(const SeqPlan& pl, const AttnArgs& a, dim3 grid, hipStream_t
 }
 
 int launch_attn_bf16(const SeqPlan& pl, const AttnArgs& a, hipStream_t st) {
-  dim3 grid(pl.qt_off[pl.n], a.hq, pl.max_split);
+  const dim3 grid(pl.qt_off[pl.n], a.hq, pl.max_split);
   if (grid.x == 0) return 0;
   if (pl.max_split > 1 && (!a.Opart || !a.ML)) return 1;
   if ((pl.qt != 256 && pl.qt != 128 && pl.qt != 64) || (a.hd != 128 && a.hd != 64)) return 1;
