@@ -202,7 +202,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 // (row, logical pair) for SWIGLU / QKV, per (row, column) otherwise.
 template <int EPI, class T>
 __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
-  const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
+  // QKV: the q and k heads only (gemm_reduce_qkv_v_kernel writes the v heads)
+  const int npair = EPI == EPI_QKV ? (a.hq + a.hkv) * a.hd / 2 : epi_paired(EPI) ? a.N / 2 : a.N;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long)a.M * npair) return;
   const int row = (int)(idx / npair), p = (int)(idx % npair);
@@ -238,23 +239,84 @@ __global__ __launch_bounds__(256) void gemm_reduce_resid_norm_kernel(GemmArgs a)
   const size_t plane = (size_t)a.M * a.N;
   const float* pr = a.part + (size_t)row * a.N;
   float* xr = a.X + (size_t)row * a.ldx;
-  for (int c = threadIdx.x * 4; c < a.N; c += blockDim.x * 4) {
-    // all slices are requested before they are summed (in slice order)
-    f32x4 sl[8];
+  // four chunks per thread and pass, every slice of them requested before
+  // any is summed (in slice order)
+  constexpr int NCH = 4;
+  const int step = blockDim.x * 4;
+  for (int c0 = threadIdx.x * 4; c0 < a.N; c0 += step * NCH) {
+    f32x4 sl[NCH][8], xv[NCH];
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
-      if (s < a.ksplit) sl[s] = *(const f32x4*)(pr + s * plane + c);
-    f32x4 v = sl[0];
+    for (int u = 0; u < NCH; ++u) {
+      const int c = c0 + u * step;
+      if (c < a.N) {
+        xv[u] = *(const f32x4*)(xr + c);
 #pragma unroll
-    for (int s = 1; s < 8; ++s)
-      if (s < a.ksplit) v += sl[s];
-    f32x4 xv = *(const f32x4*)(xr + c);
-    xv += v;
-    *(f32x4*)(xr + c) = xv;
+        for (int s = 0; s < 8; ++s)
+          if (s < a.ksplit) sl[u][s] = *(const f32x4*)(pr + s * plane + c);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int c = c0 + u * step;
+      if (c < a.N) {
+        f32x4 v = sl[u][0];
+#pragma unroll
+        for (int s = 1; s < 8; ++s)
+          if (s < a.ksplit) v += sl[u][s];
+        xv[u] += v;
+        *(f32x4*)(xr + c) = xv[u];
+      }
+    }
   }
   // each thread reads back only the elements it wrote
   rms_normalize_row<T>(xr, a.ngain, (T*)a.nout + (size_t)row * a.N,
                        a.nout2 ? (T*)a.nout2 + (size_t)row * a.N : nullptr, a.N, a.neps, red);
+}
+
+// Split-K reduction of the value heads of a QKV projection: 64 rows x hd
+// dimensions of one value head per workgroup, summed in slice order (as in
+// gemm_reduce_kernel), staged transposed in LDS and written to V^T with the
+// rows running fastest across the threads, so that the 2-byte stores of
+// consecutive rows (consecutive K/V destinations within a sequence) coalesce.
+template <class T, int HD>
+__global__ __launch_bounds__(256) void gemm_reduce_qkv_v_kernel(GemmArgs a) {
+  constexpr int RT = 64, TPR = HD, RG = 256 / HD, RPT = RT / RG;   // rows per thread
+  __shared__ T tile[HD][RT + 2];
+  const int r0 = blockIdx.x * RT, vh = blockIdx.y;
+  const size_t plane = (size_t)a.M * a.N;
+  const int d = threadIdx.x % TPR, rg = threadIdx.x / TPR;
+  const float* pr = a.part + (size_t)(a.hq + a.hkv + vh) * HD + d;
+  // every slice of this thread's rows is requested before any is summed
+  float v[RPT];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int row = min(r0 + rg + k * RG, a.M - 1);
+    v[k] = pr[(size_t)row * a.N];
+  }
+  for (int s = 1; s < a.ksplit; ++s) {
+    float t[RPT];
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+      const int row = min(r0 + rg + k * RG, a.M - 1);
+      t[k] = pr[s * plane + (size_t)row * a.N];
+    }
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) v[k] += t[k];
+  }
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) tile[d][rg + k * RG] = from_f32<T>(v[k]);
+  __syncthreads();
+  for (int i = threadIdx.x; i < RT * HD; i += blockDim.x) {
+    const int dd = i / RT, rr = i % RT, row = r0 + rr;
+    if (row < a.M) {
+      const int dst = a.row_dst[row];
+      T* vt;
+      int ld, col;
+      if (dst_is_fresh(dst)) { vt = (T*)a.Vtf; ld = a.ldfresh; col = dst; }
+      else { vt = (T*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
+      vt[((size_t)vh * HD + dd) * ld + col] = tile[dd][rr];
+    }
+  }
 }
 
 template <int EPI>
@@ -265,7 +327,12 @@ static void reduce_epi(const GemmArgs& a, hipStream_t st) {
       return;
     }
   }
-  const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
+  if constexpr (EPI == EPI_QKV) {
+    const dim3 g((a.M + 63) / 64, a.hkv);
+    if (a.hd == 128) gemm_reduce_qkv_v_kernel<bf16, 128><<<g, 256, 0, st>>>(a);
+    else gemm_reduce_qkv_v_kernel<bf16, 64><<<g, 256, 0, st>>>(a);
+  }
+  const int npair = EPI == EPI_QKV ? (a.hq + a.hkv) * a.hd / 2 : epi_paired(EPI) ? a.N / 2 : a.N;
   const long total = (long)a.M * npair;
   gemm_reduce_kernel<EPI, bf16><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(a);
 }
