@@ -74,7 +74,8 @@ __device__ __forceinline__ const void* att_uniform(const void* p) {
 
 // Four consecutive outputs of one query row as two-term bf16 (hi = bf16(v),
 // lo = bf16(v - hi)), one 8-byte store per term.
-__device__ __forceinline__ void att_store4(const AttnArgs& a, size_t i, f32x4 v) {
+__device__ __forceinline__ void att_store4(const AttnArgs& a, int row, int col, f32x4 v) {
+  const size_t i = act_at(row, col, a.ldo, a.o_tiled);   // col is a multiple of 4
   bf16x4 hi, lo;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -442,10 +443,9 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
     for (int qb = 0; qb < QB; ++qb) {
       const int qrow = rbeg + qt * QT + w * 16 * QB + qb * 16 + lc;
       if (qrow >= rend) continue;
-      const size_t ob = (size_t)qrow * a.ldo + h * HD;
       const float inv = 1.0f / l_run[qb];
 #pragma unroll
-      for (int db = 0; db < DB; ++db) att_store4(a, ob + db * 16 + lg * 4, o[qb][db] * inv);
+      for (int db = 0; db < DB; ++db) att_store4(a, qrow, h * HD + db * 16 + lg * 4, o[qb][db] * inv);
     }
     return;
   }
@@ -503,7 +503,7 @@ __global__ __launch_bounds__(MERGE_ROWS * HD / 4) void attn_merge_kernel(SeqPlan
       num += wgt * part[sp];
     }
   }
-  att_store4(a, (size_t)row * a.ldo + h * HD + d0, num * (1.0f / den));
+  att_store4(a, row, h * HD + d0, num * (1.0f / den));
 }
 
 int attn_nsplit_for_keys(int nkeys) {

@@ -86,13 +86,22 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
+// Activations feeding the bf16 projection GEMMs are stored k-block-major:
+// 32-column blocks of all rows one after the other, element (row, k) at
+// ((k / 32) * ld + row) * 32 + k % 32 with ld the row capacity, so that the
+// rows a GEMM tile reads for one 32-wide k step are one contiguous block.
+// Row-major (element (row, k) at row * ld + k) otherwise.
+__device__ __forceinline__ size_t act_at(int row, int k, int ld, int tiled) {
+  return tiled ? ((size_t)(k >> 5) * ld + row) * 32 + (k & 31) : (size_t)row * ld + k;
+}
+
 // RMSNorm of one row of x (d columns) into a two-term activation row, by a
 // block of 256 threads: thread t owns the float4 chunks at t * 4 + k * 1024.
 // Shared by the stand-alone RMSNorm kernel and the split-K reduction that
 // fuses it, so that both give the same bits.
 template <class T>
-__device__ __forceinline__ void rms_normalize_row(const float* xr, const float* gain, T* orow, T* orow2, int d,
-                                                  float eps, float* red) {
+__device__ __forceinline__ void rms_normalize_row(const float* xr, const float* gain, T* out, T* out2, int orow,
+                                                  int ld, int tiled, int d, float eps, float* red) {
   float ss = 0.f;
   for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
     const float4 v = *(const float4*)(xr + c);
@@ -103,10 +112,11 @@ __device__ __forceinline__ void rms_normalize_row(const float* xr, const float* 
   for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
     const float4 v = *(const float4*)(xr + c);
     const float4 g = *(const float4*)(gain + c);
-    store_act<T>(orow, orow2, c + 0, v.x * inv * g.x);
-    store_act<T>(orow, orow2, c + 1, v.y * inv * g.y);
-    store_act<T>(orow, orow2, c + 2, v.z * inv * g.z);
-    store_act<T>(orow, orow2, c + 3, v.w * inv * g.w);
+    const size_t i = act_at(orow, c, ld, tiled);   // 4 consecutive elements in either layout
+    store_act<T>(out, out2, i + 0, v.x * inv * g.x);
+    store_act<T>(out, out2, i + 1, v.y * inv * g.y);
+    store_act<T>(out, out2, i + 2, v.z * inv * g.z);
+    store_act<T>(out, out2, i + 3, v.w * inv * g.w);
   }
 }
 

@@ -288,12 +288,17 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   });
   if (st) return st;
 
-  auto norm = [&](const float* gain, int gather, int nrows, void* out, void* out2) {
+  // bf16 activations that feed a projection GEMM are stored k-block-major
+  // with the buffer's row capacity as ld (act, O, H: Mmax rows; Cn: Rmax)
+  const int tiled = is_bf16(c) ? 1 : 0;
+  auto norm = [&](const float* gain, int gather, int nrows, void* out, void* out2, int cap) {
     return timed(c, ARCHER_K_NORM, (double)nrows * d * (4 + es * (out2 ? 2 : 1)), 0.0, [&] {
       if (is_bf16(c))
-        launch_rmsnorm<bf16>(pl, gather, nrows, x, gain, out, out2, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
+        launch_rmsnorm<bf16>(pl, gather, nrows, x, gain, out, out2, cap, 1, d, m.rms_eps, c->at<int>(L.out_row),
+                             c->stream);
       else
-        launch_rmsnorm<float>(pl, gather, nrows, x, gain, out, out2, d, m.rms_eps, c->at<int>(L.out_row), c->stream);
+        launch_rmsnorm<float>(pl, gather, nrows, x, gain, out, out2, d, 0, d, m.rms_eps, c->at<int>(L.out_row),
+                              c->stream);
       return 0;
     });
   };
@@ -308,15 +313,15 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   // inside that GEMM's reduction (same arithmetic as the stand-alone kernel)
   auto fuse_norm = [&](GemmArgs& a, const float* gain) {
     if (!is_bf16(c)) return;
-    a.ngain = gain; a.nout = act; a.nout2 = act2; a.neps = m.rms_eps;
+    a.ngain = gain; a.nout = act; a.nout2 = act2; a.neps = m.rms_eps; a.nld = L.Mmax; a.ntiled = 1;
   };
   bool normed = false;   // attn_norm of the current layer already applied
   for (int l = 0; l < m.n_layers; ++l) {
-    if (!normed && (st = norm(c->attn_norm[l], 0, rows, act, act2))) return st;
+    if (!normed && (st = norm(c->attn_norm[l], 0, rows, act, act2, L.Mmax))) return st;
     normed = false;
     {
-      GemmArgs a = gargs(act, d, c->w_qkv[l], d, rows, qkv_n, d);
-      a.A2 = act2;
+      GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_qkv[l], d, rows, qkv_n, d);
+      a.A2 = act2; a.a_tiled = tiled;
       a.Qb = c->at<char>(L.Q); a.ldq = L.ldq;
       a.Kc = c->at<char>(L.Kc) + (size_t)l * L.cache_layer_elems * es;
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
@@ -334,7 +339,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
       a.ldcache = L.ldcache;
       a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
-      a.O = c->at<char>(L.O); a.O2 = lo_part(c, L.O2); a.ldo = hq * hd;
+      a.O = c->at<char>(L.O); a.O2 = lo_part(c, L.O2); a.ldo = tiled ? L.Mmax : hq * hd; a.o_tiled = tiled;
       a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML);
       a.hq = hq; a.hkv = hkv; a.hd = hd;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
@@ -350,25 +355,25 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       if (st) return st;
     }
     {
-      GemmArgs a = gargs(c->at<char>(L.O), hq * hd, c->w_o[l], hq * hd, rows, d, hq * hd);
-      a.A2 = lo_part(c, L.O2);
+      GemmArgs a = gargs(c->at<char>(L.O), tiled ? L.Mmax : hq * hd, c->w_o[l], hq * hd, rows, d, hq * hd);
+      a.A2 = lo_part(c, L.O2); a.a_tiled = tiled;
       a.X = x; a.ldx = d;
       fuse_norm(a, c->mlp_norm[l]);
       if ((st = gemm(c, ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
       normed = gemm_fuses_norm(a);
     }
-    if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2))) return st;
+    if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2, L.Mmax))) return st;
     normed = false;
     {
-      GemmArgs a = gargs(act, d, c->w_gate[l], d, rows, 2 * F, d);
-      a.A2 = act2;
+      GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_gate[l], d, rows, 2 * F, d);
+      a.A2 = act2; a.a_tiled = tiled;
       a.W2 = c->w_up[l];
-      a.H = c->at<char>(L.H); a.H2 = lo_part(c, L.H2); a.ldh = F;
+      a.H = c->at<char>(L.H); a.H2 = lo_part(c, L.H2); a.ldh = tiled ? L.Mmax : F; a.h_tiled = tiled;
       if ((st = gemm(c, ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
     }
     {
-      GemmArgs a = gargs(c->at<char>(L.H), F, c->w_down[l], F, rows, d, F);
-      a.A2 = lo_part(c, L.H2);
+      GemmArgs a = gargs(c->at<char>(L.H), tiled ? L.Mmax : F, c->w_down[l], F, rows, d, F);
+      a.A2 = lo_part(c, L.H2); a.a_tiled = tiled;
       a.X = x; a.ldx = d;
       if (l + 1 < m.n_layers) fuse_norm(a, c->attn_norm[l + 1]);
       if ((st = gemm(c, ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
@@ -376,10 +381,10 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
     }
   }
   const int nresp = pl.n * pl.G;
-  if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn), lo_part(c, L.Cn2)))) return st;
+  if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn), lo_part(c, L.Cn2), L.Rmax))) return st;
   {
-    GemmArgs a = gargs(c->at<char>(L.Cn), d, c->lm_head, d, nresp, m.vocab, d);
-    a.A2 = lo_part(c, L.Cn2);
+    GemmArgs a = gargs(c->at<char>(L.Cn), tiled ? L.Rmax : d, c->lm_head, d, nresp, m.vocab, d);
+    a.A2 = lo_part(c, L.Cn2); a.a_tiled = tiled;
     a.C = logits; a.ldc = m.vocab; a.out_row = c->at<int>(L.out_row);
     if ((st = gemm(c, ARCHER_K_GEMM_HEAD, EPI_STORE, a))) return st;
   }

@@ -38,7 +38,7 @@ int gemm_grid_size(int n_tiles, int m_tiles, int S) { return ((n_tiles * S + 7) 
   do {                                                                                   \
     _Pragma("unroll") for (int t = 0; t < NA; ++t)                                       \
       _Pragma("unroll") for (int j = 0; j < A_CH; ++j)                                   \
-        RA##slot[t][j] = *(const u32x4*)(Ap[t] + aoffg[j] + (k0));                       \
+        RA##slot[t][j] = *(const u32x4*)(Ap[t] + aoffg[j] + (size_t)(k0) * akmul);      \
     _Pragma("unroll") for (int j = 0; j < B_CH; ++j) RB##slot[j] = *(const u32x4*)(bsrc[j] + (k0)); \
   } while (0)
 #define GEMM_SSTORE(slot, buf)                                                           \
@@ -98,6 +98,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   const int nslices = FOLD ? a.ksplit : 1;
   const int kt_slice = (PARTIAL || FOLD ? kslice : a.K) / BK;   // k tiles per accumulation
   const bf16* Ap[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
+  const int akmul = a.a_tiled ? a.lda : 1;
 
   // rows past M load row M-1 (finite data; those output rows are never stored)
   uint32_t aoffg[A_CH], aoff[A_CH];
@@ -105,7 +106,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   for (int j = 0; j < A_CH; ++j) {
     const int c = tid + 256 * j, r = c / CPR, kc = c % CPR;
     const int row = min(m0 + r, a.M - 1);
-    aoffg[j] = (uint32_t)row * a.lda + kc * 8;
+    // k0 (a multiple of 32) contributes k0 * akmul elements
+    aoffg[j] = a.a_tiled ? (uint32_t)((kc / 4) * a.lda * 32 + row * 32 + (kc % 4) * 8) : (uint32_t)row * a.lda + kc * 8;
     aoff[j] = r * BK + ((kc ^ (r % CPR)) * 8);
   }
   const bf16* bsrc[B_CH];
@@ -269,8 +271,7 @@ __global__ __launch_bounds__(256) void gemm_reduce_resid_norm_kernel(GemmArgs a)
     }
   }
   // each thread reads back only the elements it wrote
-  rms_normalize_row<T>(xr, a.ngain, (T*)a.nout + (size_t)row * a.N,
-                       a.nout2 ? (T*)a.nout2 + (size_t)row * a.N : nullptr, a.N, a.neps, red);
+  rms_normalize_row<T>(xr, a.ngain, (T*)a.nout, (T*)a.nout2, row, a.nld, a.ntiled, a.N, a.neps, red);
 }
 
 // Split-K reduction of the value heads of a QKV projection: 64 rows x hd

@@ -46,7 +46,7 @@ __device__ __forceinline__ void epi_resid(const GemmArgs& a, int row, int col, f
 template <class T>
 __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int f, float g, float u) {
   const float s = g / (1.0f + expf(-g));
-  store_act<T>((T*)a.H, (T*)a.H2, (size_t)row * a.ldh + f, s * u);
+  store_act<T>((T*)a.H, (T*)a.H2, act_at(row, f, a.ldh, a.h_tiled), s * u);
 }
 
 // head in [0, hq + 2 hkv): q heads, k heads, v heads; v1 / v2 = dims j, j + hd/2

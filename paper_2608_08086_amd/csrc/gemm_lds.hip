@@ -105,7 +105,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
     for (int j = 0; j < AI; ++j) {
       const int q = j * 256 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
       const int row = min(m0 + r, a.M - 1);
-      a_go[j] = ((unsigned)row * a.lda + (pc ^ gl_swz(r)) * 8) * 2;
+      a_go[j] = ((unsigned)row * (a.a_tiled ? BK : a.lda) + (pc ^ gl_swz(r)) * 8) * 2;
     }
 #pragma unroll
     for (int j = 0; j < BI; ++j) {
@@ -120,6 +120,8 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
     const bf16* Wlo = (const bf16*)a.W;
     const bf16* Whi = (const bf16*)(a.W2 ? a.W2 : a.W);
     // tiles past the last are clamped: redundant loads into stages no wave reads again
+    // k-block-major A: the block of k step k0 starts k0 * row-capacity elements in
+    const size_t akmul = a.a_tiled ? (size_t)a.lda : 1;
     auto issue = [&](int g) {
       const int k0 = kbeg + min(g, ntot - 1) * BK;
       const unsigned st = lds0 + (unsigned)((g % NST) * STAGE);
@@ -127,7 +129,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
       for (int t = 0; t < NA; ++t)
 #pragma unroll
         for (int j = 0; j < AI; ++j)
-          gl_dma16(Abase[t] + k0, a_go[j], st + (unsigned)((t * A_SL + j * 256 + wp * 64) * 16));
+          gl_dma16(Abase[t] + (size_t)k0 * akmul, a_go[j], st + (unsigned)((t * A_SL + j * 256 + wp * 64) * 16));
 #pragma unroll
       for (int j = 0; j < BI; ++j)
         gl_dma16((b_hi[j] ? Whi : Wlo) + k0, b_go[j], st + (unsigned)((NA * A_SL + j * 256 + wp * 64) * 16));
@@ -316,9 +318,10 @@ __global__ __launch_bounds__(512, 1) void gemm_ws_kernel(GemmArgs a) {
       for (int j = 0; j < AJ; ++j) {
         const int q = j * 128 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
         const int row = min(m0 + r, a.M - 1);
-        a_go[j] = ((unsigned)row * a.lda + (pc ^ gl_swz(r)) * 8) * 2;
+        a_go[j] = ((unsigned)row * (a.a_tiled ? BK : a.lda) + (pc ^ gl_swz(r)) * 8) * 2;
       }
       const bf16* Abase[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
+      const size_t akmul = a.a_tiled ? (size_t)a.lda : 1;
       auto issue = [&](int g) {
         if (g >= ntot) return;
         const int k0 = kbeg + g * BK;
@@ -327,7 +330,7 @@ __global__ __launch_bounds__(512, 1) void gemm_ws_kernel(GemmArgs a) {
         for (int t = 0; t < NA; ++t)
 #pragma unroll
           for (int j = 0; j < AJ; ++j)
-            gl_dma16(Abase[t] + k0, a_go[j], st + (unsigned)((t * A_SL + j * 128 + wp * 64) * 16));
+            gl_dma16(Abase[t] + (size_t)k0 * akmul, a_go[j], st + (unsigned)((t * A_SL + j * 128 + wp * 64) * 16));
       };
 #pragma unroll
       for (int s = 0; s < NSA; ++s) issue(s);
@@ -553,7 +556,8 @@ bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
   const LdsCfg& k = kLds[c];
   if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * BK)) return false;
   // 32-bit lane offsets
-  if ((size_t)a.N * a.ldw * 2 >= (1ull << 32) || (size_t)a.M * a.lda * 2 >= (1ull << 32)) return false;
+  if ((size_t)a.N * a.ldw * 2 >= (1ull << 32) || (size_t)a.M * (a.a_tiled ? BK : a.lda) * 2 >= (1ull << 32))
+    return false;
   return true;
 }
 

@@ -79,7 +79,7 @@ template void launch_embed<bf16>(const SeqPlan&, const void*, int, int, int, con
 template <class T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, const float* __restrict__ x,
                                                       const float* __restrict__ gain, T* __restrict__ out,
-                                                      T* __restrict__ out2, int d, float eps,
+                                                      T* __restrict__ out2, int ld, int tiled, int d, float eps,
                                                       int* __restrict__ out_row) {
   __shared__ float red[16];
   const int ro = blockIdx.x;
@@ -89,19 +89,18 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, co
     ri = pl.row_off[s] + (pl.full ? pl.p_len[s] : 0) + r;
     if (threadIdx.x == 0) out_row[ro] = pl.seq[s] * pl.G + r;
   }
-  rms_normalize_row<T>(x + (size_t)ri * d, gain, out + (size_t)ro * d, out2 ? out2 + (size_t)ro * d : nullptr, d,
-                       eps, red);
+  rms_normalize_row<T>(x + (size_t)ri * d, gain, out, out2, ro, ld, tiled, d, eps, red);
 }
 
 template <class T>
 void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
-                    void* out2, int d, float eps, int* out_row, hipStream_t st) {
-  rmsnorm_kernel<T><<<nrows, 256, 0, st>>>(pl, gather, x, gain, (T*)out, (T*)out2, d, eps, out_row);
+                    void* out2, int ld, int tiled, int d, float eps, int* out_row, hipStream_t st) {
+  rmsnorm_kernel<T><<<nrows, 256, 0, st>>>(pl, gather, x, gain, (T*)out, (T*)out2, ld, tiled, d, eps, out_row);
 }
-template void launch_rmsnorm<float>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int,
-                                    float, int*, hipStream_t);
-template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int,
-                                   float, int*, hipStream_t);
+template void launch_rmsnorm<float>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int, int,
+                                    int, float, int*, hipStream_t);
+template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int, int,
+                                   int, float, int*, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Decision pass 1: per response row, over the non-MASK vocabulary:

@@ -13,7 +13,8 @@ enum GemmEpi {
 };
 
 struct GemmArgs {
-  const void* A; int lda;               // [M][K]
+  const void* A; int lda;               // [M][K] row-major (lda = row stride), or k-block-major (a_tiled,
+  int a_tiled;                          //   lda = row capacity; see act_at in common.h)
   const void* A2;                       // optional low part of a two-term A (same layout), or null
   const void* W; const void* W2; int ldw; // [N][K] (SWIGLU: W = gate [F][K], W2 = up [F][K], N = 2F)
   int M, N, K;
@@ -22,9 +23,10 @@ struct GemmArgs {
   float* C; int ldc; const int* out_row; // EPI_STORE
   float* X; int ldx;                     // EPI_RESID
   // EPI_RESID with a split-K reduction: optionally RMSNorm the updated rows of
-  // X (gain ngain, epsilon neps) into the two-term activation (nout, nout2), [M][N]
-  const float* ngain; void* nout; void* nout2; float neps;
-  void* H; void* H2; int ldh;            // EPI_SWIGLU: H = hi part, H2 = lo part (or null)
+  // X (gain ngain, epsilon neps) into the two-term activation (nout, nout2)
+  // laid out as act_at(row, k, nld, ntiled)
+  const float* ngain; void* nout; void* nout2; float neps; int nld, ntiled;
+  void* H; void* H2; int ldh, h_tiled;   // EPI_SWIGLU: H = hi part, H2 = lo part (or null), act_at layout
   // EPI_QKV
   void* Qb; int ldq;                     // Q [Hq][ldq][hd]
   void* Kc; void* Vtc; int ldcache;      // prompt cache of this layer: K [Hkv][ldcache][hd], Vt [Hkv][hd][ldcache]
@@ -37,7 +39,7 @@ struct AttnArgs {
   const void* Q; int ldq;                // [Hq][ldq][hd]
   const void* Kc; const void* Vtc; int ldcache;
   const void* Kf; const void* Vtf; int ldfresh;
-  void* O; void* O2; int ldo;            // [rows][ldo]: hi part, lo part (or null)
+  void* O; void* O2; int ldo, o_tiled;   // hi part, lo part (or null), layout act_at(row, col, ldo, o_tiled)
   float* Opart; float* ML;               // split partials [max_split][Hq][rows][hd], [max_split][Hq][rows][2]
   int hq, hkv, hd;
   float scale_log2;                      // log2(e) / sqrt(hd)
@@ -61,7 +63,7 @@ void launch_embed(const SeqPlan& pl, const void* emb, int d, int V, int mask_id,
                   hipStream_t st);
 template <class T>
 void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
-                    void* out2, int d, float eps, int* out_row, hipStream_t st);
+                    void* out2, int ld, int tiled, int d, float eps, int* out_row, hipStream_t st);
 void launch_rowstats(int rows, const float* logits, int V, int mask_id, const int* g, int* xhat, float* ell,
                      float* qv, hipStream_t st);
 void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, const int* xhat, const float* ell,
