@@ -67,9 +67,19 @@ typedef struct {
   int32_t dtype;              /* archer_dtype of weights, activations and caches */
 } archer_model_cfg;
 
-/* Weights, row-major [out][in], element type = cfg.dtype; norm gains fp32.
+/* Layouts of the projection matrices (lm_head, w_qkv, w_o, w_gate, w_up,
+ * w_down).  ROWMAJOR: element (r, c) of a [rows][cols] matrix at r * cols + c.
+ * KBLOCK (bf16 only): 32-column blocks of all rows one after another,
+ * element (r, c) at ((c / 32) * rows + r) * 32 + c % 32, which lets every
+ * projection GEMM tile read the weights of one 32-wide k step as one
+ * contiguous block; archer_pack_weight converts a matrix.  tok_emb is always
+ * row-major. */
+typedef enum { ARCHER_LAYOUT_ROWMAJOR = 0, ARCHER_LAYOUT_KBLOCK = 1 } archer_weight_layout;
+
+/* Weights [out][in] in `layout`, element type = cfg.dtype; norm gains fp32.
  * Every pointer is a device pointer; the per-layer fields are HOST arrays of
- * n_layers device pointers.  Weights must outlive the context.            */
+ * n_layers device pointers.  Weights must outlive the context.  A zeroed
+ * `layout` is row-major.                                                   */
 typedef struct {
   const void *tok_emb;                /* [V][d]                              */
   const void *lm_head;                /* [V][d]                              */
@@ -81,6 +91,7 @@ typedef struct {
   const void *const *w_gate;          /* L x [F][d]                          */
   const void *const *w_up;            /* L x [F][d]                          */
   const void *const *w_down;          /* L x [d][F]                          */
+  int32_t layout;                     /* archer_weight_layout                */
 } archer_weights;
 
 /* Context limits: they size the workspace. */
@@ -129,10 +140,20 @@ typedef struct {
  * (0 if the arguments are invalid; see archer_last_error). */
 size_t archer_workspace_bytes(const archer_model_cfg *cfg, const archer_limits *lim);
 
+/* Layout helper (no operation of the method; the model is the same in
+ * either layout and the results are bitwise the same): copy the row-major
+ * bf16 matrix src [rows][cols] into dst in the KBLOCK layout.  Device
+ * pointers, 16-byte aligned, not overlapping; rows >= 1, cols a positive
+ * multiple of 32; dtype must be ARCHER_BF16 (else ARCHER_E_UNSUPPORTED).
+ * Enqueued on hip_stream (NULL = default stream); does not synchronise. */
+archer_status archer_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void *src, void *dst,
+                                 void *hip_stream);
+
 /* Create a context.  workspace: device, >= archer_workspace_bytes bytes,
  * 256-byte aligned, owned by the caller and not touched by anything else
  * while the context lives.  hip_stream: a hipStream_t (NULL = default stream).
- * Synchronises once (device constant tables). */
+ * Synchronises once (device constant tables).  w->layout KBLOCK needs
+ * cfg.dtype ARCHER_BF16 (else ARCHER_E_UNSUPPORTED). */
 archer_status archer_init(const archer_model_cfg *cfg, const archer_weights *w,
                           const archer_limits *lim, void *workspace, size_t ws_bytes,
                           void *hip_stream, archer_ctx **out);

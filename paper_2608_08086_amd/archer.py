@@ -23,6 +23,7 @@ lib = C.CDLL(_LIB_PATH)
 OK, E_ARG, E_SHAPE, E_STATE, E_HIP, E_WORKSPACE, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 BF16, FP32 = 0, 1
 HAMMING, AGE, ALWAYS = 0, 1, 2
+LAYOUT_ROWMAJOR, LAYOUT_KBLOCK = 0, 1
 NEVER = 2**31 - 1
 K_EMBED, K_NORM, K_GEMM_QKV, K_ATTN, K_ATTN_FULL, K_GEMM_O, K_GEMM_GATEUP, K_GEMM_DOWN, K_GEMM_HEAD, K_DECIDE = range(10)
 K_COUNT = 10
@@ -33,6 +34,7 @@ EXPORTED = [
     "archer_workspace_bytes", "archer_init", "archer_refresh_prompt", "archer_step", "archer_decide",
     "archer_decode", "archer_sync", "archer_destroy", "archer_last_error", "archer_op_gemm",
     "archer_op_attention_ws_bytes", "archer_op_attention", "archer_timing_begin", "archer_timing_end",
+    "archer_pack_weight",
 ]
 
 
@@ -48,7 +50,7 @@ class Weights(C.Structure):
                 ("attn_norm", C.POINTER(C.c_void_p)), ("w_qkv", C.POINTER(C.c_void_p)),
                 ("w_o", C.POINTER(C.c_void_p)), ("mlp_norm", C.POINTER(C.c_void_p)),
                 ("w_gate", C.POINTER(C.c_void_p)), ("w_up", C.POINTER(C.c_void_p)),
-                ("w_down", C.POINTER(C.c_void_p))]
+                ("w_down", C.POINTER(C.c_void_p)), ("layout", C.c_int32)]
 
 
 class Limits(C.Structure):
@@ -99,6 +101,8 @@ lib.archer_op_attention_ws_bytes.argtypes = [C.c_int32] * 5
 lib.archer_op_attention.restype = C.c_int
 lib.archer_op_attention.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P, P, P, C.c_int32,
                                     C.c_int32, P, P, C.c_int32, C.c_int32, P, P, C.c_size_t, P]
+lib.archer_pack_weight.restype = C.c_int
+lib.archer_pack_weight.argtypes = [C.c_int32, C.c_int32, C.c_int32, P, P, P]
 lib.archer_timing_begin.restype = C.c_int
 lib.archer_timing_begin.argtypes = [P, C.c_uint32]
 lib.archer_timing_end.restype = C.c_int
@@ -158,7 +162,8 @@ class Context:
             self._keep.append(a)
             fields[key] = p
         self.cw = Weights(weights["tok_emb"].data_ptr(), weights["lm_head"].data_ptr(),
-                          weights["final_norm"].data_ptr(), **fields)
+                          weights["final_norm"].data_ptr(), **fields,
+                          layout=weights.get("layout", LAYOUT_ROWMAJOR))
         nbytes = lib.archer_workspace_bytes(C.byref(self.cfg), C.byref(self.lim))
         if nbytes == 0:
             raise ArcherError(E_ARG, lib.archer_last_error().decode())
@@ -260,6 +265,37 @@ def upload_weights(W: dict, dtype: str) -> dict:
 
     out = {k: dev(W[k]) for k in ("tok_emb", "lm_head", "final_norm")}
     out["layers"] = [{k: dev(v) for k, v in L.items()} for L in W["layers"]]
+    return out
+
+
+PROJECTIONS = ("w_qkv", "w_o", "w_gate", "w_up", "w_down")
+
+
+def pack_weight(w):
+    """Row-major bf16 [rows][cols] CUDA tensor -> a new tensor in the k-block layout (archer_pack_weight)."""
+    assert w.dtype == torch.bfloat16 and w.dim() == 2
+    out = torch.empty_like(w)
+    _check(lib.archer_pack_weight(BF16, w.shape[0], w.shape[1], _ptr(w), _ptr(out), _stream()))
+    return out
+
+
+def pack_weights(weights: dict, drop_source: bool = False) -> dict:
+    """Weights dict (row-major device tensors) -> the same model with every projection matrix
+    (lm_head and the per-layer w_qkv, w_o, w_gate, w_up, w_down) in the k-block layout.
+    drop_source releases each source matrix once it is packed (its dict entry is replaced)."""
+    out = {k: v for k, v in weights.items() if k != "layers"}
+    out["lm_head"] = pack_weight(weights["lm_head"])
+    if drop_source:
+        weights["lm_head"] = None
+    out["layers"] = []
+    for L in weights["layers"]:
+        P = dict(L)
+        for k in PROJECTIONS:
+            P[k] = pack_weight(L[k])
+            if drop_source:
+                L[k] = None
+        out["layers"].append(P)
+    out["layout"] = LAYOUT_KBLOCK
     return out
 
 

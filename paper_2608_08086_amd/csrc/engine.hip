@@ -150,6 +150,7 @@ struct archer_ctx {
   const float* final_norm;
   std::vector<const float*> attn_norm, mlp_norm;
   std::vector<const void*> w_qkv, w_o, w_gate, w_up, w_down;
+  int w_tiled = 0;   // projection matrices in the k-block-major layout
   // session
   int batch = 0;
   int plen[ARCHER_MAXB];
@@ -320,8 +321,8 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
     if (!normed && (st = norm(c->attn_norm[l], 0, rows, act, act2, L.Mmax))) return st;
     normed = false;
     {
-      GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_qkv[l], d, rows, qkv_n, d);
-      a.A2 = act2; a.a_tiled = tiled;
+      GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_qkv[l], c->w_tiled ? qkv_n : d, rows, qkv_n, d);
+      a.A2 = act2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.Qb = c->at<char>(L.Q); a.ldq = L.ldq;
       a.Kc = c->at<char>(L.Kc) + (size_t)l * L.cache_layer_elems * es;
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
@@ -355,8 +356,9 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       if (st) return st;
     }
     {
-      GemmArgs a = gargs(c->at<char>(L.O), tiled ? L.Mmax : hq * hd, c->w_o[l], hq * hd, rows, d, hq * hd);
-      a.A2 = lo_part(c, L.O2); a.a_tiled = tiled;
+      GemmArgs a = gargs(c->at<char>(L.O), tiled ? L.Mmax : hq * hd, c->w_o[l], c->w_tiled ? d : hq * hd, rows,
+                         d, hq * hd);
+      a.A2 = lo_part(c, L.O2); a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.X = x; a.ldx = d;
       fuse_norm(a, c->mlp_norm[l]);
       if ((st = gemm(c, ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
@@ -365,15 +367,15 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
     if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2, L.Mmax))) return st;
     normed = false;
     {
-      GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_gate[l], d, rows, 2 * F, d);
-      a.A2 = act2; a.a_tiled = tiled;
+      GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_gate[l], c->w_tiled ? F : d, rows, 2 * F, d);
+      a.A2 = act2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.W2 = c->w_up[l];
       a.H = c->at<char>(L.H); a.H2 = lo_part(c, L.H2); a.ldh = tiled ? L.Mmax : F; a.h_tiled = tiled;
       if ((st = gemm(c, ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
     }
     {
-      GemmArgs a = gargs(c->at<char>(L.H), tiled ? L.Mmax : F, c->w_down[l], F, rows, d, F);
-      a.A2 = lo_part(c, L.H2); a.a_tiled = tiled;
+      GemmArgs a = gargs(c->at<char>(L.H), tiled ? L.Mmax : F, c->w_down[l], c->w_tiled ? d : F, rows, d, F);
+      a.A2 = lo_part(c, L.H2); a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.X = x; a.ldx = d;
       if (l + 1 < m.n_layers) fuse_norm(a, c->attn_norm[l + 1]);
       if ((st = gemm(c, ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
@@ -383,8 +385,9 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   const int nresp = pl.n * pl.G;
   if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn), lo_part(c, L.Cn2), L.Rmax))) return st;
   {
-    GemmArgs a = gargs(c->at<char>(L.Cn), tiled ? L.Rmax : d, c->lm_head, d, nresp, m.vocab, d);
-    a.A2 = lo_part(c, L.Cn2); a.a_tiled = tiled;
+    GemmArgs a = gargs(c->at<char>(L.Cn), tiled ? L.Rmax : d, c->lm_head, c->w_tiled ? m.vocab : d, nresp,
+                       m.vocab, d);
+    a.A2 = lo_part(c, L.Cn2); a.a_tiled = tiled; a.w_tiled = c->w_tiled;
     a.C = logits; a.ldc = m.vocab; a.out_row = c->at<int>(L.out_row);
     if ((st = gemm(c, ARCHER_K_GEMM_HEAD, EPI_STORE, a))) return st;
   }
@@ -480,6 +483,10 @@ archer_status archer_init(const archer_model_cfg* cfg, const archer_weights* w, 
     if (!w->attn_norm[l] || !w->w_qkv[l] || !w->w_o[l] || !w->mlp_norm[l] || !w->w_gate[l] || !w->w_up[l] ||
         !w->w_down[l])
       return fail(ARCHER_E_ARG, "null per-layer weight pointer");
+  if (w->layout != ARCHER_LAYOUT_ROWMAJOR && w->layout != ARCHER_LAYOUT_KBLOCK)
+    return fail(ARCHER_E_ARG, "unknown weight layout");
+  if (w->layout == ARCHER_LAYOUT_KBLOCK && cfg->dtype != ARCHER_BF16)
+    return fail(ARCHER_E_UNSUPPORTED, "the k-block weight layout is bf16 only");
   if (!workspace || ((uintptr_t)workspace & 255)) return fail(ARCHER_E_ARG, "workspace null or not 256-byte aligned");
   const Layout L = make_layout(cfg, lim);
   if (ws_bytes < L.total) return fail(ARCHER_E_WORKSPACE, "workspace smaller than archer_workspace_bytes()");
@@ -491,6 +498,7 @@ archer_status archer_init(const archer_model_cfg* cfg, const archer_weights* w, 
   c->ws = (char*)workspace;
   c->esz = cfg->dtype == ARCHER_BF16 ? 2 : 4;
   c->tok_emb = w->tok_emb;
+  c->w_tiled = w->layout == ARCHER_LAYOUT_KBLOCK;
   c->lm_head = w->lm_head;
   c->final_norm = w->final_norm;
   for (int l = 0; l < cfg->n_layers; ++l) {
@@ -674,6 +682,20 @@ archer_status archer_timing_end(archer_ctx* c, int64_t* launches, double* total_
 }
 
 // ---------------------------------------------------------------------------
+archer_status archer_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void* src, void* dst,
+                                 void* hip_stream) {
+  if (dtype != ARCHER_BF16) return fail(ARCHER_E_UNSUPPORTED, "the k-block weight layout is bf16 only");
+  if (!src || !dst) return fail(ARCHER_E_ARG, "null src or dst");
+  if (((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return fail(ARCHER_E_ARG, "src and dst must be 16-byte aligned");
+  if (rows < 1 || cols < 32 || cols % 32) return fail(ARCHER_E_SHAPE, "need rows >= 1 and cols a multiple of 32");
+  const size_t bytes = (size_t)rows * cols * 2;
+  const uintptr_t s0 = (uintptr_t)src, d0 = (uintptr_t)dst;
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return fail(ARCHER_E_ARG, "src and dst overlap");
+  launch_pack_kblock(src, dst, rows, cols, (hipStream_t)hip_stream);
+  HIPCHK(hipGetLastError());
+  return ARCHER_OK;
+}
+
 archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, const void* A_lo,
                              const void* W, float* Y, void* hip_stream) {
   if (!A || !W || !Y) return fail(ARCHER_E_ARG, "null operand");

@@ -39,7 +39,7 @@ int gemm_grid_size(int n_tiles, int m_tiles, int S) { return ((n_tiles * S + 7) 
     _Pragma("unroll") for (int t = 0; t < NA; ++t)                                       \
       _Pragma("unroll") for (int j = 0; j < A_CH; ++j)                                   \
         RA##slot[t][j] = *(const u32x4*)(Ap[t] + aoffg[j] + (size_t)(k0) * akmul);      \
-    _Pragma("unroll") for (int j = 0; j < B_CH; ++j) RB##slot[j] = *(const u32x4*)(bsrc[j] + (k0)); \
+    _Pragma("unroll") for (int j = 0; j < B_CH; ++j) RB##slot[j] = *(const u32x4*)(bsrc[j] + (size_t)(k0) * wkmul); \
   } while (0)
 #define GEMM_SSTORE(slot, buf)                                                           \
   do {                                                                                   \
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
   const int nslices = FOLD ? a.ksplit : 1;
   const int kt_slice = (PARTIAL || FOLD ? kslice : a.K) / BK;   // k tiles per accumulation
   const bf16* Ap[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
-  const int akmul = a.a_tiled ? a.lda : 1;
+  const int akmul = a.a_tiled ? a.lda : 1, wkmul = a.w_tiled ? a.ldw : 1;
 
   // rows past M load row M-1 (finite data; those output rows are never stored)
   uint32_t aoffg[A_CH], aoff[A_CH];
@@ -117,7 +117,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
     const int c = tid + 256 * j, r = c / CPR, kc = c % CPR;
     bool second;
     const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
-    bsrc[j] = (const bf16*)(second ? a.W2 : a.W) + (size_t)wr * a.ldw + kc * 8;
+    bsrc[j] = (const bf16*)(second ? a.W2 : a.W) +
+              (a.w_tiled ? (size_t)(kc / 4) * a.ldw * 32 + (size_t)wr * 32 + (kc % 4) * 8 : (size_t)wr * a.ldw + kc * 8);
     boff[j] = r * BK + ((kc ^ (r % CPR)) * 8);
   }
   // tile column of accumulator block cb: blocks 0..CB/2-1 from the first tile

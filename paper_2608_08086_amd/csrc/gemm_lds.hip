@@ -112,7 +112,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
       const int q = j * 256 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
       bool second;
       const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
-      b_go[j] = ((unsigned)wr * a.ldw + (pc ^ gl_swz(r)) * 8) * 2;
+      b_go[j] = ((unsigned)wr * (a.w_tiled ? BK : a.ldw) + (pc ^ gl_swz(r)) * 8) * 2;
       // uniform over the wave's 64 slots (rows j*256/CPR + wp*64/CPR + [0, 64/CPR))
       b_hi[j] = __builtin_amdgcn_readfirstlane(second ? 1 : 0) != 0;
     }
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
     const bf16* Whi = (const bf16*)(a.W2 ? a.W2 : a.W);
     // tiles past the last are clamped: redundant loads into stages no wave reads again
     // k-block-major A: the block of k step k0 starts k0 * row-capacity elements in
-    const size_t akmul = a.a_tiled ? (size_t)a.lda : 1;
+    const size_t akmul = a.a_tiled ? (size_t)a.lda : 1, wkmul = a.w_tiled ? (size_t)a.ldw : 1;
     auto issue = [&](int g) {
       const int k0 = kbeg + min(g, ntot - 1) * BK;
       const unsigned st = lds0 + (unsigned)((g % NST) * STAGE);
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
           gl_dma16(Abase[t] + (size_t)k0 * akmul, a_go[j], st + (unsigned)((t * A_SL + j * 256 + wp * 64) * 16));
 #pragma unroll
       for (int j = 0; j < BI; ++j)
-        gl_dma16((b_hi[j] ? Whi : Wlo) + k0, b_go[j], st + (unsigned)((NA * A_SL + j * 256 + wp * 64) * 16));
+        gl_dma16((b_hi[j] ? Whi : Wlo) + (size_t)k0 * wkmul, b_go[j], st + (unsigned)((NA * A_SL + j * 256 + wp * 64) * 16));
     };
 #pragma unroll
     for (int s = 0; s < NST; ++s) issue(s);
@@ -350,19 +350,20 @@ __global__ __launch_bounds__(512, 1) void gemm_ws_kernel(GemmArgs a) {
         const int q = j * 128 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
         bool second;
         const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
-        b_go[j] = ((unsigned)wr * a.ldw + (pc ^ gl_swz(r)) * 8) * 2;
+        b_go[j] = ((unsigned)wr * (a.w_tiled ? BK : a.ldw) + (pc ^ gl_swz(r)) * 8) * 2;
         // uniform over the instruction's 64 slots (16 consecutive tile rows)
         b_hi[j] = __builtin_amdgcn_readfirstlane(second ? 1 : 0) != 0;
       }
       const bf16* Wlo = (const bf16*)a.W;
       const bf16* Whi = (const bf16*)(a.W2 ? a.W2 : a.W);
+      const size_t wkmul = a.w_tiled ? (size_t)a.ldw : 1;
       auto issue = [&](int g) {
         if (g >= ntot) return;
         const int k0 = kbeg + g * BK;
         const unsigned st = lds0 + (unsigned)((g % NSW) * W_STAGE);
 #pragma unroll
         for (int j = 0; j < BJ; ++j)
-          gl_dma16((b_hi[j] ? Whi : Wlo) + k0, b_go[j], st + (unsigned)((j * 128 + wp * 64) * 16));
+          gl_dma16((b_hi[j] ? Whi : Wlo) + (size_t)k0 * wkmul, b_go[j], st + (unsigned)((j * 128 + wp * 64) * 16));
       };
 #pragma unroll
       for (int s = 0; s < NSW; ++s) issue(s);
@@ -556,7 +557,7 @@ bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
   const LdsCfg& k = kLds[c];
   if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * BK)) return false;
   // 32-bit lane offsets
-  if ((size_t)a.N * a.ldw * 2 >= (1ull << 32) || (size_t)a.M * (a.a_tiled ? BK : a.lda) * 2 >= (1ull << 32))
+  if ((size_t)a.N * (a.w_tiled ? BK : a.ldw) * 2 >= (1ull << 32) || (size_t)a.M * (a.a_tiled ? BK : a.lda) * 2 >= (1ull << 32))
     return false;
   return true;
 }

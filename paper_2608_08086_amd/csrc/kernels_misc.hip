@@ -20,6 +20,25 @@ void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream
 }
 
 // ---------------------------------------------------------------------------
+// Weight packing: row-major [rows][cols] -> k-block-major (32-column blocks of
+// all rows one after another).  One thread per 16-byte chunk, enumerated in
+// destination order so the stores are contiguous; each source row segment of
+// one block is 64 contiguous bytes.
+__global__ void pack_kblock_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, size_t rows,
+                                   size_t cols, size_t nchunk) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < nchunk; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t cb = i / (rows * 4), rem = i - cb * rows * 4, r = rem >> 2, q = rem & 3;
+    dst[i] = src[(r * cols + cb * 32 + q * 8) / 8];
+  }
+}
+
+void launch_pack_kblock(const void* src, void* dst, int rows, int cols, hipStream_t st) {
+  const size_t nchunk = (size_t)rows * cols / 8;
+  const size_t blocks = std::min<size_t>((nchunk + 255) / 256, 65536);
+  pack_kblock_kernel<<<(unsigned)blocks, 256, 0, st>>>((const uint4*)src, (uint4*)dst, rows, cols, nchunk);
+}
+
+// ---------------------------------------------------------------------------
 // Embedding gather.  One block per pass row: resolve (sequence, token,
 // position, K/V destination) from the plan, copy E[token] into the fp32
 // residual stream, and in a full pass record the response token as anchor g_r.

@@ -17,6 +17,7 @@ struct GemmArgs {
   int a_tiled;                          //   lda = row capacity; see act_at in common.h)
   const void* A2;                       // optional low part of a two-term A (same layout), or null
   const void* W; const void* W2; int ldw; // [N][K] (SWIGLU: W = gate [F][K], W2 = up [F][K], N = 2F)
+  int w_tiled;                           //   k-block-major W (ldw = rows of each matrix), see act_at
   int M, N, K;
   int ksplit;                            // K slices (bf16): a function of (N, K) only, see gemm_ksplit
   float* part;                           // fp32 partials [ksplit][M][N] for the per-slice launch, or null
@@ -57,6 +58,8 @@ int attn_qt_bf16(const int* rows, const int* nsplit, int n, int hq);
 constexpr int ATTN_QT_F32 = 1;
 
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
+// bf16 [rows][cols] row-major -> k-block-major (cols % 32 == 0)
+void launch_pack_kblock(const void* src, void* dst, int rows, int cols, hipStream_t st);
 template <class T>
 void launch_embed(const SeqPlan& pl, const void* emb, int d, int V, int mask_id, const int* prompt,
                   const int* resp, float* x, int* row_pos, int* row_dst, int* g_anchor, int* err,

@@ -46,9 +46,15 @@ def rand_f32(shape, seed, stream, scale=1.0):
     return dev_f32(v), v.astype(np.float64)
 
 
-def make_ctx(shape, W, max_batch, max_prompt_len, max_prompt_total, resp_len):
+def make_ctx(shape, W, max_batch, max_prompt_len, max_prompt_total, resp_len, layout=None):
+    """Context over host weights W.  layout None: the k-block weight layout for bf16 models
+    (the one the bench runs), row-major for fp32."""
     a = archer()
     Wd = a.upload_weights(W, shape.dtype)
+    if layout is None:
+        layout = a.LAYOUT_KBLOCK if shape.dtype == "bf16" else a.LAYOUT_ROWMAJOR
+    if layout == a.LAYOUT_KBLOCK:
+        Wd = a.pack_weights(Wd, drop_source=True)
     return a.Context(shape, Wd, max_batch, max_prompt_len, max_prompt_total, resp_len)
 
 

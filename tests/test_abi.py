@@ -74,3 +74,22 @@ def test_workspace_bytes_and_host_side_errors():
     # shape checks happen on the host before any launch (N not a multiple of 64)
     assert archer.lib.archer_op_gemm(archer.BF16, 8, 60, 64, C.c_void_p(16), None, C.c_void_p(16),
                                      C.c_void_p(16), None) == archer.E_SHAPE
+    # weight packing: host-side checks before any launch
+    pk = archer.lib.archer_pack_weight
+    a0, a1 = C.c_void_p(1 << 20), C.c_void_p(1 << 30)
+    assert pk(archer.FP32, 64, 64, a0, a1, None) == archer.E_UNSUPPORTED
+    assert pk(archer.BF16, 64, 64, None, a1, None) == archer.E_ARG
+    assert pk(archer.BF16, 64, 48, a0, a1, None) == archer.E_SHAPE
+    assert pk(archer.BF16, 0, 64, a0, a1, None) == archer.E_SHAPE
+    assert pk(archer.BF16, 64, 64, a0, C.c_void_p((1 << 20) + 4096), None) == archer.E_ARG   # overlap
+    assert pk(archer.BF16, 64, 64, C.c_void_p((1 << 20) + 8), a1, None) == archer.E_ARG      # alignment
+    # the k-block weight layout is refused for fp32 models, unknown layouts for any model
+    cfg32 = _cfg(archer, dtype=archer.FP32)
+    L = cfg32.n_layers
+    per = (C.c_void_p * L)(*([16] * L))
+    pp = C.cast(per, C.POINTER(C.c_void_p))
+    for dt, layout, want in ((archer.FP32, archer.LAYOUT_KBLOCK, archer.E_UNSUPPORTED),
+                             (archer.BF16, 7, archer.E_ARG)):
+        w = archer.Weights(16, 16, 16, pp, pp, pp, pp, pp, pp, pp, layout)
+        assert archer.lib.archer_init(C.byref(_cfg(archer, dtype=dt)), C.byref(w), C.byref(lim), None, 0, None,
+                                      C.byref(h)) == want

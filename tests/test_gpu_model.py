@@ -7,6 +7,9 @@
 * on the GPU, CachedForward on the cache of the same response equals
   FullForward bitwise, and a sequence's logits do not depend on the batch;
 * a ragged batch with per-sequence refresh (seq_sel);
+* the k-block weight layout: the pack kernel is the stated permutation, and a
+  model gives the same bits in either layout (bf16 contexts use the k-block
+  layout unless a test says otherwise, as the bench does);
 * a full-width 2-layer LLaDA-8B-shaped model (d 4096, vocab 126464, P 512,
   G 256) in the bench's launch configuration.
 """
@@ -17,7 +20,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import dev_i32, host, make_ctx, rel_err, say, with_gains
+from gpu_util import archer, dev_i32, host, make_ctx, rand_bf16, rel_err, say, with_gains
 from oracle import model as om
 from synth.gen import model_weights, prompts
 from synth.workloads import ModelShape, get_workload
@@ -85,6 +88,37 @@ def test_small_bf16_full_and_cached(name):
     zc = host(ctx.step(dev_i32(g1[None])))[0]
     zc_ref, _ = om.cached_forward(W, m, g1, cache, P)
     assert np.max(np.abs(zc - zc_ref)) < 2e-2
+
+
+@pytest.mark.parametrize("rows,cols", [(1, 32), (100, 96), (257, 4096)])
+def test_pack_weight_is_the_k_block_permutation(rows, cols):
+    a = archer()
+    say(f"pack weight {rows}x{cols}")
+    w, _ = rand_bf16((rows, cols), 61, rows * 7 + cols)
+    got = a.pack_weight(w)
+    # element (r, c) at ((c / 32) * rows + r) * 32 + c % 32
+    want = w.view(rows, cols // 32, 32).permute(1, 0, 2).contiguous().view(rows, cols)
+    assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+
+
+def test_weight_layouts_give_the_same_bits():
+    """The k-block and row-major weight layouts feed the same tiles in the same order."""
+    a = archer()
+    m = SMALL_BF16["gqa_hd64"]
+    say("bf16 model, row-major vs k-block weights")
+    W = with_gains(model_weights(m, seed=12), 12)
+    P, G = 77, 32
+    p = _prompt(m, P, 13)
+    g0, g1 = _resp(m, G, 14), _resp(m, G, 15, frac=0.5)
+    out = []
+    for layout in (a.LAYOUT_ROWMAJOR, a.LAYOUT_KBLOCK):
+        ctx = make_ctx(m, W, 1, P, P, G, layout=layout)
+        z = host(ctx.refresh_prompt(dev_i32(p), [P], dev_i32(g0[None])))[0]
+        zc = host(ctx.step(dev_i32(g1[None])))[0]
+        out.append((z, zc))
+        ctx.close()
+    np.testing.assert_array_equal(out[0][0], out[1][0])
+    np.testing.assert_array_equal(out[0][1], out[1][1])
 
 
 def test_ragged_batch_per_sequence_refresh_and_batch_invariance():
