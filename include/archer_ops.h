@@ -58,15 +58,19 @@ enum {
   ARCHER_K_COUNT = 10
 };
 
-/* Start recording HIP events around every launch of the classes in
- * class_mask (bit c = class c) made by this context; stops and clears any
- * earlier recording. */
-archer_status archer_timing_begin(archer_ctx *ctx, uint32_t class_mask);
+/* Start recording HIP events around launches of the classes in class_mask
+ * (bit c = class c) made by this context: the 1st, (every+1)-th, (2 every+1)-th
+ * ... launch of each class (every >= 1; 1 = every launch).  Each event pair
+ * idles the GPU for a few microseconds, so a stride keeps the measurement from
+ * slowing what it measures.  Stops and clears any earlier recording;
+ * ARCHER_E_ARG if every < 1. */
+archer_status archer_timing_begin(archer_ctx *ctx, uint32_t class_mask, int32_t every);
 
 /* Synchronise, stop recording and return, per class c < ARCHER_K_COUNT:
- * launches[c], total_ms[c] (sum of event-bracketed launch durations) and the
- * algorithmic bytes[c] and flops[c] of those launches (minimum HBM traffic:
- * operands read once and results written once).  Any output may be NULL. */
+ * launches[c] (recorded launches), total_ms[c] (sum of their event-bracketed
+ * durations) and the algorithmic bytes[c] and flops[c] of those launches
+ * (minimum HBM traffic: operands read once and results written once).  Any
+ * output may be NULL. */
 archer_status archer_timing_end(archer_ctx *ctx, int64_t *launches, double *total_ms,
                                 double *bytes, double *flops);
 

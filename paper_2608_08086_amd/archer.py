@@ -104,7 +104,7 @@ lib.archer_op_attention.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, 
 lib.archer_pack_weight.restype = C.c_int
 lib.archer_pack_weight.argtypes = [C.c_int32, C.c_int32, C.c_int32, P, P, P]
 lib.archer_timing_begin.restype = C.c_int
-lib.archer_timing_begin.argtypes = [P, C.c_uint32]
+lib.archer_timing_begin.argtypes = [P, C.c_uint32, C.c_int32]
 lib.archer_timing_end.restype = C.c_int
 lib.archer_timing_end.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                   C.POINTER(C.c_double)]
@@ -239,11 +239,12 @@ class Context:
         _check(lib.archer_sync(self.h))
 
     # -- timing of archer_ops.h ---------------------------------------------------------------
-    def timing_begin(self, classes):
+    def timing_begin(self, classes, every=1):
+        """Record every `every`-th launch of each class in `classes` (1 = all)."""
         mask = 0
         for c in classes:
             mask |= 1 << c
-        _check(lib.archer_timing_begin(self.h, mask))
+        _check(lib.archer_timing_begin(self.h, mask, every))
 
     def timing_end(self):
         n = (C.c_int64 * K_COUNT)()

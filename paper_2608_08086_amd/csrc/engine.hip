@@ -160,6 +160,8 @@ struct archer_ctx {
   // timing
   bool t_on = false;
   uint32_t t_mask = 0;
+  int t_every = 1;                       // record every t_every-th launch of a class
+  int64_t t_seen[ARCHER_K_COUNT] = {0};  // launches of each class since timing began
   std::vector<TimerRec> t_recs;
   size_t t_used = 0;
 
@@ -175,12 +177,14 @@ void* lo_part(archer_ctx* c, size_t off) { return is_bf16(c) ? (void*)(c->ws + o
 
 template <class F>
 archer_status timed(archer_ctx* c, int cls, double bytes, double flops, F&& launch) {
-  const bool rec = c->t_on && ((c->t_mask >> cls) & 1u);
+  const bool rec = c->t_on && ((c->t_mask >> cls) & 1u) && (c->t_seen[cls]++ % c->t_every) == 0;
   if (rec) {
     if (c->t_used == c->t_recs.size()) {
       TimerRec r{};
-      HIPCHK(hipEventCreate(&r.a));
-      HIPCHK(hipEventCreate(&r.b));
+      // timing-only events: no system-scope fence (an L2 writeback and
+      // invalidate per record, which idles the GPU ~5 us between kernels)
+      HIPCHK(hipEventCreateWithFlags(&r.a, hipEventDisableSystemFence));
+      HIPCHK(hipEventCreateWithFlags(&r.b, hipEventDisableSystemFence));
       c->t_recs.push_back(r);
     }
     HIPCHK(hipEventRecord(c->t_recs[c->t_used].a, c->stream));
@@ -648,10 +652,13 @@ void archer_destroy(archer_ctx* c) {
   delete c;
 }
 
-archer_status archer_timing_begin(archer_ctx* c, uint32_t mask) {
+archer_status archer_timing_begin(archer_ctx* c, uint32_t mask, int32_t every) {
   if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  if (every < 1) return fail(ARCHER_E_ARG, "every must be >= 1");
   c->t_on = mask != 0;
   c->t_mask = mask;
+  c->t_every = every;
+  for (int k = 0; k < ARCHER_K_COUNT; ++k) c->t_seen[k] = 0;
   c->t_used = 0;
   return ARCHER_OK;
 }

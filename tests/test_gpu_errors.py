@@ -68,3 +68,25 @@ def test_bad_token_ids_are_flagged(ctx):
     with pytest.raises(a.ArcherError) as e:
         c.sync()
     assert e.value.status == a.E_ARG
+
+
+def test_timing_stride(ctx):
+    """archer_timing_begin records the 1st, (every+1)-th, ... launch of each class."""
+    m, c = ctx
+    a = archer()
+    with pytest.raises(a.ArcherError) as e:
+        c.timing_begin([a.K_GEMM_QKV], every=0)
+    assert e.value.status == a.E_ARG
+    p = dev_i32(np.arange(10) % (m.vocab - 1))
+    g = dev_i32(np.full((1, 8), m.mask_id))
+    c.refresh_prompt(p, [10], g)
+    for every, want in ((1, 7), (3, 3), (7, 1)):
+        # 7 forwards of a 1-layer model: 7 QKV GEMMs and 7 LM heads
+        c.timing_begin([a.K_GEMM_QKV, a.K_GEMM_HEAD], every=every)
+        for _ in range(7):
+            c.step(g)
+        t = c.timing_end()
+        for k in ("gemm_qkv", "gemm_head"):
+            assert t[k]["launches"] == want, (every, k, t[k])
+            assert t[k]["ms"] > 0 and t[k]["flops"] > 0
+        assert t["attn"]["launches"] == 0
