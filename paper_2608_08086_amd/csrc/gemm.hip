@@ -202,11 +202,11 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmArgs a) {
 }
 
 // Sum of the S partials in slice order, then the epilogue.  One thread per
-// (row, logical pair) for SWIGLU / QKV, per (row, column) otherwise.
+// (row, logical pair) for SWIGLU, per (row, column) otherwise.
 template <int EPI, class T>
 __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
-  // QKV: the q and k heads only (gemm_reduce_qkv_v_kernel writes the v heads)
-  const int npair = EPI == EPI_QKV ? (a.hq + a.hkv) * a.hd / 2 : epi_paired(EPI) ? a.N / 2 : a.N;
+  static_assert(EPI != EPI_QKV, "QKV partials are reduced by gemm_reduce_qkv_kernel");
+  const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long)a.M * npair) return;
   const int row = (int)(idx / npair), p = (int)(idx % npair);
@@ -217,12 +217,6 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
     float g = pr[p], u = pr[F + p];
     for (int s = 1; s < a.ksplit; ++s) { g += pr[s * plane + p]; u += pr[s * plane + F + p]; }
     epi_swiglu<T>(a, row, p, g, u);
-  } else if constexpr (EPI == EPI_QKV) {
-    const int half = a.hd / 2, head = p / half, j = p % half;
-    const int c1 = head * a.hd + j, c2 = c1 + half;
-    float v1 = pr[c1], v2 = pr[c2];
-    for (int s = 1; s < a.ksplit; ++s) { v1 += pr[s * plane + c1]; v2 += pr[s * plane + c2]; }
-    epi_qkv<T>(a, row, head, j, v1, v2);
   } else {
     float v = pr[p];
     for (int s = 1; s < a.ksplit; ++s) v += pr[s * plane + p];
@@ -232,81 +226,124 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
 }
 
 // Split-K reduction of an EPI_RESID GEMM fused with the RMSNorm of the
-// updated rows: one block per row; thread t owns the same float4 chunks as in
-// rms_normalize_row, adds the slices in slice order into X (as
-// gemm_reduce_kernel does) and then normalises the row it has just written.
-template <class T>
+// updated rows: one block per row; thread t owns the float4 chunks t, t + 256,
+// ... (KC of them, N <= KC * 1024) as in rms_normalize_row, adds the slices in
+// slice order into X (as gemm_reduce_kernel does) and normalises the row from
+// the values it keeps in registers, with the same expressions in the same
+// order as rms_normalize_row (same bits).
+template <class T, int KC>
 __global__ __launch_bounds__(256) void gemm_reduce_resid_norm_kernel(GemmArgs a) {
   __shared__ float red[16];
   const int row = blockIdx.x;
   const size_t plane = (size_t)a.M * a.N;
   const float* pr = a.part + (size_t)row * a.N;
   float* xr = a.X + (size_t)row * a.ldx;
-  // four chunks per thread and pass, every slice of them requested before
-  // any is summed (in slice order)
-  constexpr int NCH = 4;
   const int step = blockDim.x * 4;
-  for (int c0 = threadIdx.x * 4; c0 < a.N; c0 += step * NCH) {
-    f32x4 sl[NCH][8], xv[NCH];
+  f32x4 xv[KC];
+  // groups of four chunks, every slice of a group requested before any is summed
 #pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = c0 + u * step;
+  for (int g = 0; g < KC; g += 4) {
+    f32x4 sl[4][8];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = threadIdx.x * 4 + (g + u) * step;
       if (c < a.N) {
-        xv[u] = *(const f32x4*)(xr + c);
+        xv[g + u] = *(const f32x4*)(xr + c);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
           if (s < a.ksplit) sl[u][s] = *(const f32x4*)(pr + s * plane + c);
       }
     }
 #pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = c0 + u * step;
+    for (int u = 0; u < 4; ++u) {
+      const int c = threadIdx.x * 4 + (g + u) * step;
       if (c < a.N) {
         f32x4 v = sl[u][0];
 #pragma unroll
         for (int s = 1; s < 8; ++s)
           if (s < a.ksplit) v += sl[u][s];
-        xv[u] += v;
-        *(f32x4*)(xr + c) = xv[u];
+        xv[g + u] += v;
+        *(f32x4*)(xr + c) = xv[g + u];
       }
     }
   }
-  // each thread reads back only the elements it wrote
-  rms_normalize_row<T>(xr, a.ngain, (T*)a.nout, (T*)a.nout2, row, a.nld, a.ntiled, a.N, a.neps, red);
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < KC; ++k) {
+    const int c = threadIdx.x * 4 + k * step;
+    if (c < a.N) {
+      const f32x4 v = xv[k];
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)a.N + a.neps);
+#pragma unroll
+  for (int k = 0; k < KC; ++k) {
+    const int c = threadIdx.x * 4 + k * step;
+    if (c < a.N) {
+      const f32x4 v = xv[k];
+      const float4 g = *(const float4*)(a.ngain + c);
+      const size_t i = act_at(row, c, a.nld, a.ntiled);
+      store_act<T>((T*)a.nout, (T*)a.nout2, i + 0, v.x * inv * g.x);
+      store_act<T>((T*)a.nout, (T*)a.nout2, i + 1, v.y * inv * g.y);
+      store_act<T>((T*)a.nout, (T*)a.nout2, i + 2, v.z * inv * g.z);
+      store_act<T>((T*)a.nout, (T*)a.nout2, i + 3, v.w * inv * g.w);
+    }
+  }
 }
 
-// Split-K reduction of the value heads of a QKV projection: 64 rows x hd
-// dimensions of one value head per workgroup, summed in slice order (as in
-// gemm_reduce_kernel), staged transposed in LDS and written to V^T with the
-// rows running fastest across the threads, so that the 2-byte stores of
-// consecutive rows (consecutive K/V destinations within a sequence) coalesce.
+// Split-K reduction of a QKV projection in one launch.  Blocks [0, nvb) sum
+// the value heads: 32 rows x hd dimensions of one value head per block
+// (float4 loads, slices summed in slice order as in gemm_reduce_kernel),
+// staged transposed in LDS and written to V^T with the rows running fastest
+// across the threads, so that the 2-byte stores of consecutive rows
+// (consecutive K/V destinations within a sequence) coalesce.  The remaining
+// blocks sum the q/k column pairs (one pair per thread) and apply RoPE.
 template <class T, int HD>
-__global__ __launch_bounds__(256) void gemm_reduce_qkv_v_kernel(GemmArgs a) {
-  constexpr int RT = 64, TPR = HD, RG = 256 / HD, RPT = RT / RG;   // rows per thread
-  __shared__ T tile[HD][RT + 2];
-  const int r0 = blockIdx.x * RT, vh = blockIdx.y;
+__global__ __launch_bounds__(256) void gemm_reduce_qkv_kernel(GemmArgs a, int nvb) {
   const size_t plane = (size_t)a.M * a.N;
-  const int d = threadIdx.x % TPR, rg = threadIdx.x / TPR;
-  const float* pr = a.part + (size_t)(a.hq + a.hkv + vh) * HD + d;
+  if ((int)blockIdx.x >= nvb) {
+    const int npair = (a.hq + a.hkv) * HD / 2;
+    const long idx = (long)(blockIdx.x - nvb) * blockDim.x + threadIdx.x;
+    if (idx >= (long)a.M * npair) return;
+    const int row = (int)(idx / npair), p = (int)(idx % npair);
+    const float* pr = a.part + (size_t)row * a.N;
+    const int half = HD / 2, head = p / half, j = p % half;
+    const int c1 = head * HD + j, c2 = c1 + half;
+    float v1 = pr[c1], v2 = pr[c2];
+    for (int s = 1; s < a.ksplit; ++s) { v1 += pr[s * plane + c1]; v2 += pr[s * plane + c2]; }
+    epi_qkv<T>(a, row, head, j, v1, v2);
+    return;
+  }
+  constexpr int RT = 32, TPR = HD / 4, RG = 256 / TPR, RPT = RT / RG;
+  static_assert(RPT >= 1 && RT % RG == 0, "row tiling");
+  __shared__ T tile[HD][RT + 2];
+  const int mb = (a.M + RT - 1) / RT;
+  const int vh = blockIdx.x / mb, r0 = (blockIdx.x % mb) * RT;
+  const int d4 = (threadIdx.x % TPR) * 4, rg = threadIdx.x / TPR;
+  const float* pr = a.part + (size_t)(a.hq + a.hkv + vh) * HD + d4;
   // every slice of this thread's rows is requested before any is summed
-  float v[RPT];
+  f32x4 v[RPT];
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
     const int row = min(r0 + rg + k * RG, a.M - 1);
-    v[k] = pr[(size_t)row * a.N];
+    v[k] = *(const f32x4*)(pr + (size_t)row * a.N);
   }
   for (int s = 1; s < a.ksplit; ++s) {
-    float t[RPT];
+    f32x4 t[RPT];
 #pragma unroll
     for (int k = 0; k < RPT; ++k) {
       const int row = min(r0 + rg + k * RG, a.M - 1);
-      t[k] = pr[s * plane + (size_t)row * a.N];
+      t[k] = *(const f32x4*)(pr + s * plane + (size_t)row * a.N);
     }
 #pragma unroll
     for (int k = 0; k < RPT; ++k) v[k] += t[k];
   }
 #pragma unroll
-  for (int k = 0; k < RPT; ++k) tile[d][rg + k * RG] = from_f32<T>(v[k]);
+  for (int k = 0; k < RPT; ++k)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tile[d4 + e][rg + k * RG] = from_f32<T>(v[k][e]);
   __syncthreads();
   for (int i = threadIdx.x; i < RT * HD; i += blockDim.x) {
     const int dd = i / RT, rr = i % RT, row = r0 + rr;
@@ -325,18 +362,22 @@ template <int EPI>
 static void reduce_epi(const GemmArgs& a, hipStream_t st) {
   if constexpr (EPI == EPI_RESID) {
     if (a.ngain) {
-      gemm_reduce_resid_norm_kernel<bf16><<<a.M, 256, 0, st>>>(a);
+      if (a.N <= 4096) gemm_reduce_resid_norm_kernel<bf16, 4><<<a.M, 256, 0, st>>>(a);
+      else gemm_reduce_resid_norm_kernel<bf16, 8><<<a.M, 256, 0, st>>>(a);
       return;
     }
   }
   if constexpr (EPI == EPI_QKV) {
-    const dim3 g((a.M + 63) / 64, a.hkv);
-    if (a.hd == 128) gemm_reduce_qkv_v_kernel<bf16, 128><<<g, 256, 0, st>>>(a);
-    else gemm_reduce_qkv_v_kernel<bf16, 64><<<g, 256, 0, st>>>(a);
+    const int nvb = (a.M + 31) / 32 * a.hkv;
+    const long nqk = (long)a.M * (a.hq + a.hkv) * a.hd / 2;
+    const unsigned grid = (unsigned)(nvb + (nqk + 255) / 256);
+    if (a.hd == 128) gemm_reduce_qkv_kernel<bf16, 128><<<grid, 256, 0, st>>>(a, nvb);
+    else gemm_reduce_qkv_kernel<bf16, 64><<<grid, 256, 0, st>>>(a, nvb);
+  } else {
+    const int npair = epi_paired(EPI) ? a.N / 2 : a.N;
+    const long total = (long)a.M * npair;
+    gemm_reduce_kernel<EPI, bf16><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(a);
   }
-  const int npair = EPI == EPI_QKV ? (a.hq + a.hkv) * a.hd / 2 : epi_paired(EPI) ? a.N / 2 : a.N;
-  const long total = (long)a.M * npair;
-  gemm_reduce_kernel<EPI, bf16><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(a);
 }
 
 void launch_gemm_reduce(int epi, const GemmArgs& a, hipStream_t st) {
@@ -455,7 +496,7 @@ int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipS
 }
 
 bool gemm_fuses_norm(const GemmArgs& a) {
-  if (!a.ngain || !a.part || a.N % 4 || a.ldx % 4 || a.ksplit > 8) return false;
+  if (!a.ngain || !a.part || a.N % 4 || a.N > 8192 || a.ldx % 4 || a.ksplit > 8) return false;
   const int cfg = gemm_pick_cfg(a, EPI_RESID);
   return gemm_partial_wanted(cfg, a) != 0;
 }
