@@ -126,8 +126,8 @@ template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const
 //   m = max z, xhat = smallest id attaining m, s = sum exp(z - m),
 //   ell = -log s (= m - lse, log top probability),
 //   q = z[g] - m - log s (log probability of the current token; decided rows).
-// One block per row; each thread scans a strided slice with an online
-// (max, sum) pair, then a fixed-order tree combines the threads.
+// One block of 1024 threads per row; each thread scans a strided slice with an
+// online (max, sum) pair, then a fixed-order tree combines the threads.
 __device__ __forceinline__ void stat_combine(float& m, float& s, int& id, float m2, float s2, int id2) {
   if (s2 == 0.f) return;
   if (s == 0.f) { m = m2; s = s2; id = id2; return; }
@@ -143,29 +143,45 @@ __device__ __forceinline__ void stat_combine(float& m, float& s, int& id, float 
   }
 }
 
-__global__ __launch_bounds__(256) void rowstats_kernel(const float* __restrict__ logits, int V, int mask_id,
-                                                       const int* __restrict__ g, int* __restrict__ xhat,
-                                                       float* __restrict__ ell, float* __restrict__ qv) {
-  __shared__ float sm[256], ss[256];
-  __shared__ int sid[256];
+constexpr int RS_THREADS = 1024;   // threads per row
+constexpr int RS_BATCH = 8;        // float4 loads of a thread in flight before any is consumed
+
+__global__ __launch_bounds__(RS_THREADS) void rowstats_kernel(const float* __restrict__ logits, int V,
+                                                              int mask_id, const int* __restrict__ g,
+                                                              int* __restrict__ xhat, float* __restrict__ ell,
+                                                              float* __restrict__ qv) {
+  __shared__ float sm[RS_THREADS], ss[RS_THREADS];
+  __shared__ int sid[RS_THREADS];
   const int row = blockIdx.x;
   const float* z = logits + (size_t)row * V;
   float m = -INFINITY, s = 0.f;
   int id = 0x7fffffff;
-  for (int v0 = threadIdx.x * 4; v0 < V; v0 += blockDim.x * 4) {
-    const float4 t = *(const float4*)(z + v0);
-    const float e[4] = {t.x, t.y, t.z, t.w};
+  // thread t scans the float4 chunks t, t + RS_THREADS, ... in increasing
+  // order, RS_BATCH chunks requested at a time
+  for (int base = threadIdx.x * 4; base < V; base += RS_THREADS * 4 * RS_BATCH) {
+    float4 t[RS_BATCH];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int v = v0 + k;
-      if (v == mask_id) continue;
-      const float zv = e[k];
-      if (zv > m) {
-        s = s * expf(m - zv) + 1.f;
-        m = zv;
-        id = v;
-      } else {
-        s += expf(zv - m);
+    for (int u = 0; u < RS_BATCH; ++u) {
+      const int v0 = base + u * RS_THREADS * 4;
+      if (v0 < V) t[u] = *(const float4*)(z + v0);
+    }
+#pragma unroll
+    for (int u = 0; u < RS_BATCH; ++u) {
+      const int v0 = base + u * RS_THREADS * 4;
+      if (v0 >= V) break;
+      const float e[4] = {t[u].x, t[u].y, t[u].z, t[u].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int v = v0 + k;
+        if (v == mask_id) continue;
+        const float zv = e[k];
+        if (zv > m) {
+          s = s * expf(m - zv) + 1.f;
+          m = zv;
+          id = v;
+        } else {
+          s += expf(zv - m);
+        }
       }
     }
   }
@@ -196,7 +212,7 @@ __global__ __launch_bounds__(256) void rowstats_kernel(const float* __restrict__
 
 void launch_rowstats(int rows, const float* logits, int V, int mask_id, const int* g, int* xhat, float* ell,
                      float* qv, hipStream_t st) {
-  rowstats_kernel<<<rows, 256, 0, st>>>(logits, V, mask_id, g, xhat, ell, qv);
+  rowstats_kernel<<<rows, RS_THREADS, 0, st>>>(logits, V, mask_id, g, xhat, ell, qv);
 }
 
 // ---------------------------------------------------------------------------
@@ -212,32 +228,37 @@ __global__ __launch_bounds__(512) void select_kernel(const int* __restrict__ g_i
                                                      int* __restrict__ remask_pos, int* __restrict__ tr_dist,
                                                      int* __restrict__ tr_unmask, int* __restrict__ tr_utok,
                                                      int* __restrict__ tr_remask) {
-  extern __shared__ unsigned char smem_raw[];
-  float* sell = (float*)smem_raw;               // [G]
-  int* smask = (int*)(sell + G);                // [G]
-  int* ssel = smask + G;                        // [G]
+  extern __shared__ float4 smem_raw4[];
+  // key[i] = ell[i] for masked rows, -inf for decided rows (which then never
+  // outrank a masked row: ell = -log sum exp(z - max) is finite)
+  float* skey = (float*)smem_raw4;              // [G], G % 4 == 0
+  int* ssel = (int*)(skey + G);                 // [G]
   __shared__ float rq[512];
   __shared__ int ri[512];
   __shared__ int rcnt[512];
+  __shared__ int wcnt[8];
   const int b = blockIdx.x;
   const int* gi = g_in + (size_t)b * G;
-  for (int i = threadIdx.x; i < G; i += blockDim.x) {
-    const int msk = gi[i] == mask_id;
-    smask[i] = msk;
-    sell[i] = ell[(size_t)b * G + i];
-  }
+  for (int i = threadIdx.x; i < G; i += blockDim.x)
+    skey[i] = gi[i] == mask_id ? ell[(size_t)b * G + i] : -INFINITY;
   __syncthreads();
-  // unmask selection by rank
+  // unmask selection by rank among the masked rows (ties: smaller position)
   for (int i = threadIdx.x; i < G; i += blockDim.x) {
     int sel = 0;
-    if (smask[i]) {
+    const float ei = skey[i];
+    if (gi[i] == mask_id) {
       if (final_step) {
         sel = 1;
       } else {
-        const float ei = sell[i];
         int rank = 0;
-        for (int j = 0; j < G; ++j)
-          rank += smask[j] && (sell[j] > ei || (sell[j] == ei && j < i));
+        const float4* k4 = (const float4*)skey;
+#pragma unroll 4
+        for (int j4 = 0; j4 < G / 4; ++j4) {
+          const float4 kk = k4[j4];
+          const int j = 4 * j4;
+          rank += (kk.x > ei || (kk.x == ei && j + 0 < i)) + (kk.y > ei || (kk.y == ei && j + 1 < i)) +
+                  (kk.z > ei || (kk.z == ei && j + 2 < i)) + (kk.w > ei || (kk.w == ei && j + 3 < i));
+        }
         sel = rank < k;
       }
     }
@@ -247,7 +268,7 @@ __global__ __launch_bounds__(512) void select_kernel(const int* __restrict__ g_i
   float bq = INFINITY;
   int bi = 0x7fffffff;
   for (int i = threadIdx.x; i < G; i += blockDim.x) {
-    if (!smask[i]) {
+    if (gi[i] != mask_id) {
       const float q = qv[(size_t)b * G + i];
       if (q < bq || (q == bq && i < bi)) { bq = q; bi = i; }
     }
@@ -267,23 +288,38 @@ __global__ __launch_bounds__(512) void select_kernel(const int* __restrict__ g_i
     __syncthreads();
   }
   const int rm = (!final_step && max_remask > 0 && ri[0] < G && rq[0] < log_tau) ? ri[0] : -1;
-  // write g_out, count distance to the anchor, list unmasked positions
-  int cnt = 0;
-  for (int i = threadIdx.x; i < G; i += blockDim.x) {
-    int v = gi[i];
-    if (ssel[i]) v = xhat[(size_t)b * G + i];
-    if (i == rm) v = mask_id;
-    g_out[(size_t)b * G + i] = v;
-    cnt += v != g_anchor[(size_t)b * G + i];
-    if (ssel[i] && (unmask_pos || tr_unmask || tr_utok)) {
-      int order = 0;
-      for (int j = 0; j < i; ++j) order += ssel[j];
-      if (order < k) {
+  // write g_out, count the distance to the anchor, list the unmasked
+  // positions in ascending order (position among the selected rows by a
+  // ballot scan over blocks of blockDim rows)
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
+  const bool list = unmask_pos || tr_unmask || tr_utok;
+  int cnt = 0, nsel = 0;
+  for (int i0 = 0; i0 < G; i0 += blockDim.x) {
+    const int i = i0 + threadIdx.x;
+    const int f = i < G ? ssel[i] : 0;
+    const unsigned long long bal = __ballot(f);
+    if (lane == 0) wcnt[wv] = __popcll(bal);
+    __syncthreads();
+    int before = nsel, total = nsel;
+    for (int w = 0; w < nw; ++w) {
+      if (w < wv) before += wcnt[w];
+      total += wcnt[w];
+    }
+    if (i < G) {
+      int v = gi[i];
+      if (f) v = xhat[(size_t)b * G + i];
+      if (i == rm) v = mask_id;
+      g_out[(size_t)b * G + i] = v;
+      cnt += v != g_anchor[(size_t)b * G + i];
+      const int order = before + __popcll(bal & ((1ull << lane) - 1));
+      if (f && list && order < k) {
         if (unmask_pos) unmask_pos[(size_t)b * k + order] = i;
         if (tr_unmask) tr_unmask[(size_t)b * k + order] = i;
         if (tr_utok) tr_utok[(size_t)b * k + order] = v;
       }
     }
+    nsel = total;
+    __syncthreads();
   }
   rcnt[threadIdx.x] = cnt;
   __syncthreads();
@@ -292,8 +328,6 @@ __global__ __launch_bounds__(512) void select_kernel(const int* __restrict__ g_i
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    int nsel = 0;
-    for (int j = 0; j < G; ++j) nsel += ssel[j];
     for (int o = nsel; o < k; ++o) {
       if (unmask_pos) unmask_pos[(size_t)b * k + o] = -1;
       if (tr_unmask) tr_unmask[(size_t)b * k + o] = -1;
@@ -310,7 +344,7 @@ void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, cons
                    const float* qv, int G, int mask_id, int k, float log_tau, int max_remask, int final_step,
                    int* dist, int* unmask_pos, int* remask_pos, int* tr_dist, int* tr_unmask, int* tr_utok,
                    int* tr_remask, hipStream_t st) {
-  const size_t shm = (size_t)G * 12;
+  const size_t shm = (size_t)G * 8;
   select_kernel<<<B, 512, shm, st>>>(g_in, g_out, g_anchor, xhat, ell, qv, G, mask_id, k, log_tau, max_remask,
                                      final_step, dist, unmask_pos, remask_pos, tr_dist, tr_unmask, tr_utok,
                                      tr_remask);
