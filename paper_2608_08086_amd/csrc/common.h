@@ -95,8 +95,13 @@ __device__ __forceinline__ size_t act_at(int row, int k, int ld, int tiled) {
   return tiled ? ((size_t)(k >> 5) * ld + row) * 32 + (k & 31) : (size_t)row * ld + k;
 }
 
+// Threads per row of the RMSNorm kernels (stand-alone and fused into the
+// split-K reduction; both must use the same count to give the same bits).
+constexpr int NORM_THREADS = 512;
+
 // RMSNorm of one row of x (d columns) into a two-term activation row, by a
-// block of 256 threads: thread t owns the float4 chunks at t * 4 + k * 1024.
+// block of NORM_THREADS threads: thread t owns the float4 chunks at
+// t * 4 + k * 4 * NORM_THREADS.
 // Shared by the stand-alone RMSNorm kernel and the split-K reduction that
 // fuses it, so that both give the same bits.
 template <class T>

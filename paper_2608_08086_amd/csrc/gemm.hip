@@ -226,26 +226,33 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs a) {
 }
 
 // Split-K reduction of an EPI_RESID GEMM fused with the RMSNorm of the
-// updated rows: one block per row; thread t owns the float4 chunks t, t + 256,
-// ... (KC of them, N <= KC * 1024) as in rms_normalize_row, adds the slices in
-// slice order into X (as gemm_reduce_kernel does) and normalises the row from
-// the values it keeps in registers, with the same expressions in the same
-// order as rms_normalize_row (same bits).
+// updated rows: one block of NORM_THREADS per row; thread t owns the float4
+// chunks t, t + NORM_THREADS, ... (KC of them, N <= 4 * KC * NORM_THREADS) as
+// in rms_normalize_row, adds the slices in slice order into X (as
+// gemm_reduce_kernel does) and normalises the row from the values it keeps in
+// registers, with the same expressions in the same order as
+// rms_normalize_row (same bits as the stand-alone kernel).
 template <class T, int KC>
-__global__ __launch_bounds__(256) void gemm_reduce_resid_norm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(NORM_THREADS) void gemm_reduce_resid_norm_kernel(GemmArgs a) {
+  constexpr int GRP = KC < 4 ? KC : 4;   // chunks whose slices are requested together
   __shared__ float red[16];
   const int row = blockIdx.x;
   const size_t plane = (size_t)a.M * a.N;
   const float* pr = a.part + (size_t)row * a.N;
   float* xr = a.X + (size_t)row * a.ldx;
-  const int step = blockDim.x * 4;
+  const int step = NORM_THREADS * 4;
   f32x4 xv[KC];
-  // groups of four chunks, every slice of a group requested before any is summed
+  float4 gv[KC];
 #pragma unroll
-  for (int g = 0; g < KC; g += 4) {
-    f32x4 sl[4][8];
+  for (int k = 0; k < KC; ++k) {
+    const int c = threadIdx.x * 4 + k * step;
+    if (c < a.N) gv[k] = *(const float4*)(a.ngain + c);
+  }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+  for (int g = 0; g < KC; g += GRP) {
+    f32x4 sl[GRP][8];
+#pragma unroll
+    for (int u = 0; u < GRP; ++u) {
       const int c = threadIdx.x * 4 + (g + u) * step;
       if (c < a.N) {
         xv[g + u] = *(const f32x4*)(xr + c);
@@ -255,7 +262,7 @@ __global__ __launch_bounds__(256) void gemm_reduce_resid_norm_kernel(GemmArgs a)
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < GRP; ++u) {
       const int c = threadIdx.x * 4 + (g + u) * step;
       if (c < a.N) {
         f32x4 v = sl[u][0];
@@ -283,7 +290,7 @@ __global__ __launch_bounds__(256) void gemm_reduce_resid_norm_kernel(GemmArgs a)
     const int c = threadIdx.x * 4 + k * step;
     if (c < a.N) {
       const f32x4 v = xv[k];
-      const float4 g = *(const float4*)(a.ngain + c);
+      const float4 g = gv[k];
       const size_t i = act_at(row, c, a.nld, a.ntiled);
       store_act<T>((T*)a.nout, (T*)a.nout2, i + 0, v.x * inv * g.x);
       store_act<T>((T*)a.nout, (T*)a.nout2, i + 1, v.y * inv * g.y);
@@ -362,8 +369,8 @@ template <int EPI>
 static void reduce_epi(const GemmArgs& a, hipStream_t st) {
   if constexpr (EPI == EPI_RESID) {
     if (a.ngain) {
-      if (a.N <= 4096) gemm_reduce_resid_norm_kernel<bf16, 4><<<a.M, 256, 0, st>>>(a);
-      else gemm_reduce_resid_norm_kernel<bf16, 8><<<a.M, 256, 0, st>>>(a);
+      if (a.N <= 8 * NORM_THREADS) gemm_reduce_resid_norm_kernel<bf16, 2><<<a.M, NORM_THREADS, 0, st>>>(a);
+      else gemm_reduce_resid_norm_kernel<bf16, 4><<<a.M, NORM_THREADS, 0, st>>>(a);
       return;
     }
   }
@@ -496,7 +503,7 @@ int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipS
 }
 
 bool gemm_fuses_norm(const GemmArgs& a) {
-  if (!a.ngain || !a.part || a.N % 4 || a.N > 8192 || a.ldx % 4 || a.ksplit > 8) return false;
+  if (!a.ngain || !a.part || a.N % 4 || a.N > 16 * NORM_THREADS || a.ldx % 4 || a.ksplit > 8) return false;
   const int cfg = gemm_pick_cfg(a, EPI_RESID);
   return gemm_partial_wanted(cfg, a) != 0;
 }

@@ -96,7 +96,7 @@ template void launch_embed<bf16>(const SeqPlan&, const void*, int, int, int, con
 // gather = 1 (final norm): output row ri in [0, n*G) is response row ri % G of
 // pass sequence ri / G; its logits row b*G + (ri % G) is written to out_row.
 template <class T>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, const float* __restrict__ x,
+__global__ __launch_bounds__(NORM_THREADS) void rmsnorm_kernel(SeqPlan pl, int gather, const float* __restrict__ x,
                                                       const float* __restrict__ gain, T* __restrict__ out,
                                                       T* __restrict__ out2, int ld, int tiled, int d, float eps,
                                                       int* __restrict__ out_row) {
@@ -114,7 +114,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(SeqPlan pl, int gather, co
 template <class T>
 void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
                     void* out2, int ld, int tiled, int d, float eps, int* out_row, hipStream_t st) {
-  rmsnorm_kernel<T><<<nrows, 256, 0, st>>>(pl, gather, x, gain, (T*)out, (T*)out2, ld, tiled, d, eps, out_row);
+  rmsnorm_kernel<T><<<nrows, NORM_THREADS, 0, st>>>(pl, gather, x, gain, (T*)out, (T*)out2, ld, tiled, d, eps, out_row);
 }
 template void launch_rmsnorm<float>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int, int,
                                     int, float, int*, hipStream_t);
