@@ -511,6 +511,14 @@ int attn_nsplit_for_keys(int nkeys) {
   return std::max(1, std::min(ATTN_MAX_SPLIT, (tiles + ATTN_TILES_PER_SPLIT - 1) / ATTN_TILES_PER_SPLIT));
 }
 
+bool attn_split_wanted(const int* rows, int n, int hq) {
+  long wgs = 0;
+  for (int s = 0; s < n; ++s) wgs += (long)((rows[s] + 255) / 256) * hq;
+  return wgs < ATTN_MIN_WGS;
+}
+
+int attn_split_rows_max(int hq) { return 256 * ((ATTN_MIN_WGS + hq - 1) / hq); }
+
 int attn_qt_bf16(const int* rows, const int* nsplit, int n, int hq) {
   for (int qt : {256, 128}) {
     long wgs = 0;

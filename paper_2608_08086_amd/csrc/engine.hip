@@ -97,7 +97,9 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
   L.Cn = take((size_t)L.Rmax * d * esz);
   L.Cn2 = take(lo * L.Rmax * d * esz);
   L.logits = take((size_t)L.Rmax * c->vocab * 4);
-  const size_t part_rows = c->dtype == ARCHER_BF16 ? (size_t)L.Mmax : 1;
+  // split-KV partials: only passes with fewer than attn_split_rows_max rows split
+  const size_t part_rows =
+      c->dtype == ARCHER_BF16 ? (size_t)std::min(L.Mmax, attn_split_rows_max(hq)) : 1;
   L.Opart = take((size_t)kMaxSplit * hq * part_rows * hd * 4);
   L.ML = take((size_t)kMaxSplit * hq * part_rows * 2 * 4);
   // split-K partials of response-row launches: max over the projections of ksplit * N
@@ -210,11 +212,10 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
   p.G = c->lim.resp_len;
   int rows = 0, tiles = 0;
   int nrows[ARCHER_MAXB];
-  for (int s = 0; s < p.n; ++s) {
-    const int b = sel[s];
-    nrows[s] = full ? c->plen[b] + p.G : p.G;
-    p.nsplit[s] = is_bf16(c) ? attn_nsplit_for_keys(((c->plen[b] + 63) & ~63) + p.G) : 1;
-  }
+  for (int s = 0; s < p.n; ++s) nrows[s] = full ? c->plen[sel[s]] + p.G : p.G;
+  const bool split = is_bf16(c) && attn_split_wanted(nrows, p.n, c->cfg.n_heads);
+  for (int s = 0; s < p.n; ++s)
+    p.nsplit[s] = split ? attn_nsplit_for_keys(((c->plen[sel[s]] + 63) & ~63) + p.G) : 1;
   const int qt = is_bf16(c) ? attn_qt_bf16(nrows, p.nsplit, p.n, c->cfg.n_heads) : ATTN_QT_F32;
   p.qt = qt;
   for (int s = 0; s < p.n; ++s) {
@@ -721,11 +722,13 @@ archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, con
   return ARCHER_OK;
 }
 
-static int op_attn_nsplit(int dtype, int nk) { return dtype == ARCHER_BF16 ? attn_nsplit_for_keys(nk) : 1; }
+static int op_attn_nsplit(int dtype, int Mq, int Hq, int nk) {
+  return dtype == ARCHER_BF16 && attn_split_wanted(&Mq, 1, Hq) ? attn_nsplit_for_keys(nk) : 1;
+}
 
 size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32_t hd, int32_t nk) {
   if (Mq < 1 || Hq < 1 || hd < 1 || nk < 1) return 0;
-  const int ns = op_attn_nsplit(dtype, nk);
+  const int ns = op_attn_nsplit(dtype, Mq, Hq, nk);
   return align_up((size_t)ns * Hq * Mq * hd * 4, 256) + align_up((size_t)ns * Hq * Mq * 2 * 4, 256);
 }
 
@@ -737,7 +740,7 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
   if (Mq < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (hd != 64 && hd != 128)) return fail(ARCHER_E_SHAPE, "bad head shape");
   if (nk1 < 1 || nk2 < 1 || ld1 % 64 || ld2 % 64 || nk1 > ld1 || nk2 > ld2) return fail(ARCHER_E_SHAPE, "bad key segments");
   if (dtype != ARCHER_BF16 && dtype != ARCHER_FP32) return fail(ARCHER_E_ARG, "bad dtype");
-  const int ns = op_attn_nsplit(dtype, ((nk1 + 63) & ~63) + nk2);
+  const int ns = op_attn_nsplit(dtype, Mq, Hq, ((nk1 + 63) & ~63) + nk2);
   const size_t need = archer_op_attention_ws_bytes(dtype, Mq, Hq, hd, ((nk1 + 63) & ~63) + nk2);
   if (ns > 1 && (!workspace || ws_bytes < need || ((uintptr_t)workspace & 255)))
     return fail(ARCHER_E_WORKSPACE, "attention workspace too small or misaligned");

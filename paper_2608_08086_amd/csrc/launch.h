@@ -55,6 +55,12 @@ constexpr int ATTN_MAX_SPLIT = 8;          // split-KV bound (workspace is sized
 constexpr int ATTN_TILES_PER_SPLIT = 8;    // 64-key tiles per split (target)
 constexpr int ATTN_MIN_WGS = 256;          // workgroups wanted per pass (one per CU)
 int attn_qt_bf16(const int* rows, const int* nsplit, int n, int hq);
+// Split-KV only for passes short of workgroups: false when the pass's 256-row
+// query tiles alone give ATTN_MIN_WGS workgroups (a split would only add
+// partial-result traffic).  A split pass therefore has fewer than
+// attn_split_rows_max(hq) rows (sizes the partial buffers).
+bool attn_split_wanted(const int* rows, int n, int hq);
+int attn_split_rows_max(int hq);
 constexpr int ATTN_QT_F32 = 1;
 
 void launch_rope_table(float2* tab, int max_pos, int hd, double theta, hipStream_t st);
