@@ -45,7 +45,11 @@ __device__ __forceinline__ void epi_resid(const GemmArgs& a, int row, int col, f
 
 template <class T>
 __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int f, float g, float u) {
-  const float s = g / (1.0f + expf(-g));
+  // SiLU with the hardware exponential and reciprocal (v_exp_f32, v_rcp_f32):
+  // a few ulp in fp32, far below the two-term bf16 rounding of the stored
+  // product, for a fraction of the instructions of the IEEE-exact forms; the
+  // denominator is >= 1 (and rcp(inf) = 0 gives the limit for large -g)
+  const float s = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
   store_act<T>((T*)a.H, (T*)a.H2, act_at(row, f, a.ldh, a.h_tiled), s * u);
 }
 

@@ -194,14 +194,40 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
       for (int cb = 0; cb < CB; ++cb)
         acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][t][rb], fb[buf][cb], acc[rb][cb], 0, 0, 0);
   };
+  // Two-term tiles of at most 64 columns per wave: the fragment reads of tile
+  // g + 1 are spread one per lo-term MFMA of tile g, so that a burst of reads
+  // never holds up the MFMA issue (wider wave tiles, and the folded mode with
+  // its second set of accumulators, run out of registers with the reads in
+  // flight between the MFMAs, and keep the burst).
+  constexpr bool PIPE = NA == 2 && CB <= 4 && !FOLD;
   auto tile_body = [&](int g, int cur) {
     mfma_term(cur, 0);
-    if (g + 1 < ntot) {
-      __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
-      gl_barrier();                               // X_g
-      read_frags(g + 1, cur ^ 1);
+    if constexpr (PIPE) {
+      if (g + 1 < ntot) {
+        __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
+        gl_barrier();                               // X_g
+        read_frags(g + 1, cur ^ 1);
+        mfma_term(cur, 1);
+        constexpr int NRD = CB + NA * RB, NM = RB * CB;
+#pragma unroll
+        for (int i = 0; i < (NRD < NM ? NRD : NM); ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+        }
+        if constexpr (NM > NRD) __builtin_amdgcn_sched_group_barrier(0x008, NM - NRD, 0);
+        if constexpr (NRD > NM) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NM, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+        mfma_term(cur, 1);
+      }
+    } else {
+      if (g + 1 < ntot) {
+        __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
+        gl_barrier();                               // X_g
+        read_frags(g + 1, cur ^ 1);
+      }
+      if constexpr (NA == 2) mfma_term(cur, 1);
     }
-    if constexpr (NA == 2) mfma_term(cur, 1);
     if constexpr (FOLD) {
       if ((g + 1) % kt_slice == 0) {
 #pragma unroll
