@@ -488,7 +488,22 @@ int gemm_partial_wanted(int cfg, const GemmArgs& a) {
   return a.ksplit > 1;
 }
 
+bool gemm_args_ok(int epi, const GemmArgs& a) {
+  if (!a.A || !a.W || a.M <= 0 || a.N <= 0 || a.K <= 0 || a.ksplit < 1) return false;
+  switch (epi) {
+    case EPI_STORE: return a.C && a.ldc >= a.N;
+    case EPI_RESID: return a.X && a.ldx >= a.N;
+    case EPI_SWIGLU: return a.H && a.W2 && a.N % 2 == 0;
+    case EPI_QKV:
+      // the column mapping divides by hd / 2 and the epilogue indexes every table
+      return a.hd > 0 && a.hd % 2 == 0 && a.hq > 0 && a.hkv > 0 && a.N == (a.hq + 2 * a.hkv) * a.hd && a.Qb &&
+             a.Kf && a.Vtf && a.Kc && a.Vtc && a.row_dst && a.row_pos && a.rope;
+    default: return false;
+  }
+}
+
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st) {
+  if (!gemm_args_ok(epi, a)) return 1;
   if (cfg >= GEMM_NCFG) return launch_gemm_lds_cfg(epi, cfg - GEMM_NCFG, partial, a, st);
   if (!gemm_cfg_ok(cfg, a, epi)) return 1;
   if (partial && (!a.part || a.ksplit < 2)) return 1;
@@ -571,6 +586,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 
 int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st) {
   constexpr int BM = 64, BN = 64;
+  if (!gemm_args_ok(epi, a)) return 1;
   if (a.M <= 0 || a.N % BN || a.K % 16) return 1;
   if (epi == EPI_QKV && (a.hd % BN)) return 1;
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM);

@@ -594,7 +594,7 @@ int gemm_lds_tiles(int c, const GemmArgs& a) {
 }
 
 int launch_gemm_lds_cfg(int epi, int c, bool partial, const GemmArgs& a, hipStream_t st) {
-  if (!gemm_lds_cfg_ok(c, a)) return 1;
+  if (!gemm_args_ok(epi, a) || !gemm_lds_cfg_ok(c, a)) return 1;
   if (partial && (!a.part || a.ksplit < 2)) return 1;
   switch (epi) {
     case EPI_STORE: lds_epi<EPI_STORE>(c, a, partial, st); break;

@@ -100,6 +100,9 @@ int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);
 // true if launch_gemm_bf16 runs this EPI_RESID GEMM with a separate split-K
 // reduction, which then also applies the RMSNorm described by a.ngain
 bool gemm_fuses_norm(const GemmArgs& a);
+// Host-side check of the operands an epilogue uses (pointers, the QKV head
+// shape); every launcher rejects arguments that fail it before any launch.
+bool gemm_args_ok(int epi, const GemmArgs& a);
 int launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t st);
 
 // Split-KV count for a sequence with nkeys keys (padded key space); the same
