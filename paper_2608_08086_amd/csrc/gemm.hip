@@ -306,21 +306,28 @@ __global__ __launch_bounds__(NORM_THREADS) void gemm_reduce_resid_norm_kernel(Ge
 // staged transposed in LDS and written to V^T with the rows running fastest
 // across the threads, so that the 2-byte stores of consecutive rows
 // (consecutive K/V destinations within a sequence) coalesce.  The remaining
-// blocks sum the q/k column pairs (one pair per thread) and apply RoPE.
+// blocks sum the q/k column pairs (four consecutive pairs of a head per
+// thread, float4 loads) and apply RoPE.
 template <class T, int HD>
 __global__ __launch_bounds__(256) void gemm_reduce_qkv_kernel(GemmArgs a, int nvb) {
   const size_t plane = (size_t)a.M * a.N;
   if ((int)blockIdx.x >= nvb) {
-    const int npair = (a.hq + a.hkv) * HD / 2;
+    // four consecutive pairs (j .. j + 3) of one head per thread
+    constexpr int Q4 = HD / 8;                    // quads of pairs per head
+    const int nquad = (a.hq + a.hkv) * Q4;
     const long idx = (long)(blockIdx.x - nvb) * blockDim.x + threadIdx.x;
-    if (idx >= (long)a.M * npair) return;
-    const int row = (int)(idx / npair), p = (int)(idx % npair);
+    if (idx >= (long)a.M * nquad) return;
+    const int row = (int)(idx / nquad), q = (int)(idx % nquad);
     const float* pr = a.part + (size_t)row * a.N;
-    const int half = HD / 2, head = p / half, j = p % half;
-    const int c1 = head * HD + j, c2 = c1 + half;
-    float v1 = pr[c1], v2 = pr[c2];
-    for (int s = 1; s < a.ksplit; ++s) { v1 += pr[s * plane + c1]; v2 += pr[s * plane + c2]; }
-    epi_qkv<T>(a, row, head, j, v1, v2);
+    const int head = q / Q4, j = (q % Q4) * 4;
+    const int c1 = head * HD + j, c2 = c1 + HD / 2;
+    f32x4 v1 = *(const f32x4*)(pr + c1), v2 = *(const f32x4*)(pr + c2);
+    for (int s = 1; s < a.ksplit; ++s) {
+      v1 += *(const f32x4*)(pr + s * plane + c1);
+      v2 += *(const f32x4*)(pr + s * plane + c2);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) epi_qkv<T>(a, row, head, j + e, v1[e], v2[e]);
     return;
   }
   constexpr int RT = 32, TPR = HD / 4, RG = 256 / TPR, RPT = RT / RG;
@@ -376,7 +383,7 @@ static void reduce_epi(const GemmArgs& a, hipStream_t st) {
   }
   if constexpr (EPI == EPI_QKV) {
     const int nvb = (a.M + 31) / 32 * a.hkv;
-    const long nqk = (long)a.M * (a.hq + a.hkv) * a.hd / 2;
+    const long nqk = (long)a.M * (a.hq + a.hkv) * a.hd / 8;
     const unsigned grid = (unsigned)(nvb + (nqk + 255) / 256);
     if (a.hd == 128) gemm_reduce_qkv_kernel<bf16, 128><<<grid, 256, 0, st>>>(a, nvb);
     else gemm_reduce_qkv_kernel<bf16, 64><<<grid, 256, 0, st>>>(a, nvb);
