@@ -129,6 +129,7 @@ def test_attention_f32_matches_oracle(Mq, Hq, Hkv, hd, nk1, nk2):
     (256, 32, 32, 4096, 256),   # LLaDA-8B-shaped long-prompt cached step
     (256, 32, 32, 512, 256),    # LLaDA-8B-shaped cached step
     (512, 28, 4, 1024, 512),    # Dream-7B-shaped GQA cached step
+    (4352, 32, 32, 4096, 256),  # LLaDA-8B-shaped refresh pass at P 4096: enough query tiles, one split
 ])
 def test_attention_full_size_sampled(Mq, Hq, Hkv, nk1, nk2):
     say(f"attention full size Mq={Mq} Hq={Hq} Hkv={Hkv} nk1={nk1} nk2={nk2}")
