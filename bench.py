@@ -230,6 +230,10 @@ def main():
                     help="profiling only: end with a 1 GiB device copy (known HBM traffic) for PMC scaling")
     ap.add_argument("--sweep", choices=["update", "response", "radius"],
                     help="run a sweep instead of the throughput bench (prints its own JSON object)")
+    ap.add_argument("--probe", action="store_true",
+                    help="run the cache-validity probe (shadow full forwards at cached steps) on the "
+                         "workload instead of the throughput bench (prints its own JSON object)")
+    ap.add_argument("--probe-every", type=int, default=4, help="probe every n-th cached forward")
     args = ap.parse_args()
     if args.sweep:
         sweep(args.sweep)
@@ -267,6 +271,23 @@ def main():
     ctx = archer.Context(m, Wd, B, max(lens), sum(lens), G)
     prompt = torch.from_numpy(np.concatenate(prompts(w, lens)).astype(np.int32)).cuda()
     resp = torch.full((B, G), m.mask_id, dtype=torch.int32, device="cuda")
+    if args.probe:
+        from paper_2608_08086_amd import probe
+
+        # the shadow context's prompt cache is the scratch cache of the fresh forwards
+        shadow = archer.Context(m, Wd, B, max(lens), sum(lens), G)
+        t0 = time.perf_counter()
+        _, tr, recs = probe.shadow_probe(ctx, shadow, prompt, lens, resp, policy=pol, K=Kr, steps=T, k=k,
+                                         tau=dec.remask_threshold, every=args.probe_every)
+        torch.cuda.synchronize()
+        out = {"probe": "decision-level cache validity (non-intervening shadow full forwards)",
+               "workload": f"{w.name}: {w.note}", "policy": args.policy, "K": Kr, "steps": T,
+               "probe_every_cached_forward": args.probe_every, "wall_s": round(time.perf_counter() - t0, 3),
+               "refresh_fraction": round(float(tr["refreshed"].mean()), 4),
+               "data": "synthetic: random-init weights and prompts; values are not comparable to the paper's",
+               **probe.summarize(recs)}
+        print(json.dumps(out))
+        return
 
     def decode(policy, K):
         resp.fill_(m.mask_id)
