@@ -141,6 +141,7 @@ def summarize(probes):
         bins.append(dict(D=f"{lo}-{hi}" if hi is not None else f">={lo}", probes=n,
                          action_disagreement_pct=round(100.0 * dis[sel].mean(), 2) if n else None,
                          next_state_dH=round(float(dH[sel].mean()), 3) if n else None))
+
     def rho(x, y, z):   # None where a signal is constant over the probes (undefined)
         v = partial_spearman(x, y, z) if len(probes) > 2 else float("nan")
         return None if np.isnan(v) else round(v, 4)
