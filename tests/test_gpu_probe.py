@@ -6,7 +6,9 @@
 * on the tiny fp32 workload every probe record (forward index, D_t, A_t,
   action disagreement, next-state Hamming distance) equals the one of the
   same probe run by the oracle (cached and fresh forwards in float64), up to
-  decisions whose oracle margin is below the fp32 error of the kernels.
+  decisions whose oracle margin is below the fp32 error of the kernels;
+* archer_decode on a ragged bf16 batch (per-sequence refreshes mixed with
+  cached forwards) equals the same algorithm driven call by call, bitwise.
 """
 
 import numpy as np
@@ -94,3 +96,37 @@ def test_probe_is_non_intervening_and_matches_oracle(policy, K):
             say(f"  margin-exempt record at forward {o['t']} (margins {mc:.2e}, {mf:.2e})")
             return
     say(f"  {len(recs)} probes, disagreement {np.mean([r['disagree'] for r in recs]):.3f}")
+
+
+@pytest.mark.parametrize("policy,K", [("age", 3), ("hamming", 4)])
+def test_batched_bf16_decode_equals_call_driven_trajectory(policy, K):
+    """archer_decode on a ragged bf16 batch (k-block weights, per-sequence refreshes mixed with
+    cached steps in one forward) against the same Algorithm 1 driven through archer_refresh_prompt /
+    archer_step / archer_decide: bitwise the same trajectories and responses."""
+    from paper_2608_08086_amd import probe
+    from synth.workloads import ModelShape
+
+    a = archer()
+    m = ModelShape(n_layers=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=1024,
+                   dtype="bf16", init_std=0.05)
+    say(f"batched bf16 decode vs call-driven trajectory, policy={policy} K={K}")
+    W = model_weights(m, seed=21)
+    lens, G, T, k = [37, 90], 32, 24, 2
+    rng = np.random.default_rng(22)
+    ps = [rng.integers(0, m.vocab - 1, n).astype(np.int32) for n in lens]
+    prompt = dev_i32(np.concatenate(ps))
+    pol = {"age": a.AGE, "hamming": a.HAMMING}[policy]
+    ctx = make_ctx(m, W, 2, max(lens), sum(lens), G)
+    shadow = make_ctx(m, W, 2, max(lens), sum(lens), G)
+    g0 = dev_i32(np.full((2, G), m.mask_id))
+    g_fin, tr, _ = probe.shadow_probe(ctx, shadow, prompt, lens, g0, policy=pol, K=K, steps=T, k=k, tau=0.1,
+                                      every=5)
+    ref_ctx = make_ctx(m, W, 2, max(lens), sum(lens), G)
+    out, tr_d = ref_ctx.decode(prompt, lens, dev_i32(np.full((2, G), m.mask_id)), policy=pol, K=K, steps=T, k=k,
+                               tau=0.1)
+    np.testing.assert_array_equal(g_fin.cpu().numpy(), out.cpu().numpy())
+    for key in ("refreshed", "dist", "age"):
+        np.testing.assert_array_equal(tr[key], tr_d[key].cpu().numpy(), err_msg=key)
+    # after the initial forward both refreshes and cached forwards happened
+    assert 0 < tr["refreshed"][1:].sum() < (T - 1) * 2, tr["refreshed"].T
+    assert (out.cpu().numpy() != m.mask_id).all()
