@@ -62,6 +62,29 @@ __device__ __forceinline__ void store_act(T* hi, T* lo, size_t i, float v) {
   if (lo) lo[i] = from_f32<T>(v - to_f32(h));
 }
 
+// Four consecutive activations (i a multiple of 4, so the 4 elements are
+// contiguous and 8-byte aligned in either activation layout): the same values
+// as four store_act calls, written with one vector store per term.
+template <class T>
+__device__ __forceinline__ void store_act4(T* hi, T* lo, size_t i, float v0, float v1, float v2, float v3) {
+  if constexpr (sizeof(T) == 2) {
+    const float v[4] = {v0, v1, v2, v3};
+    bf16x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[e] = from_f32<T>(v[e]);
+      l[e] = from_f32<T>(v[e] - to_f32((T)h[e]));
+    }
+    *(bf16x4*)(hi + i) = h;
+    if (lo) *(bf16x4*)(lo + i) = l;
+  } else {
+    store_act<T>(hi, lo, i + 0, v0);
+    store_act<T>(hi, lo, i + 1, v1);
+    store_act<T>(hi, lo, i + 2, v2);
+    store_act<T>(hi, lo, i + 3, v3);
+  }
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -118,10 +141,7 @@ __device__ __forceinline__ void rms_normalize_row(const float* xr, const float* 
     const float4 v = *(const float4*)(xr + c);
     const float4 g = *(const float4*)(gain + c);
     const size_t i = act_at(orow, c, ld, tiled);   // 4 consecutive elements in either layout
-    store_act<T>(out, out2, i + 0, v.x * inv * g.x);
-    store_act<T>(out, out2, i + 1, v.y * inv * g.y);
-    store_act<T>(out, out2, i + 2, v.z * inv * g.z);
-    store_act<T>(out, out2, i + 3, v.w * inv * g.w);
+    store_act4<T>(out, out2, i, v.x * inv * g.x, v.y * inv * g.y, v.z * inv * g.z, v.w * inv * g.w);
   }
 }
 

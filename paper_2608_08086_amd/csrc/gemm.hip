@@ -292,10 +292,7 @@ __global__ __launch_bounds__(NORM_THREADS) void gemm_reduce_resid_norm_kernel(Ge
       const f32x4 v = xv[k];
       const float4 g = gv[k];
       const size_t i = act_at(row, c, a.nld, a.ntiled);
-      store_act<T>((T*)a.nout, (T*)a.nout2, i + 0, v.x * inv * g.x);
-      store_act<T>((T*)a.nout, (T*)a.nout2, i + 1, v.y * inv * g.y);
-      store_act<T>((T*)a.nout, (T*)a.nout2, i + 2, v.z * inv * g.z);
-      store_act<T>((T*)a.nout, (T*)a.nout2, i + 3, v.w * inv * g.w);
+      store_act4<T>((T*)a.nout, (T*)a.nout2, i, v.x * inv * g.x, v.y * inv * g.y, v.z * inv * g.z, v.w * inv * g.w);
     }
   }
 }
@@ -310,6 +307,7 @@ __global__ __launch_bounds__(NORM_THREADS) void gemm_reduce_resid_norm_kernel(Ge
 // thread, float4 loads) and apply RoPE.
 template <class T, int HD>
 __global__ __launch_bounds__(256) void gemm_reduce_qkv_kernel(GemmArgs a, int nvb) {
+  static_assert(sizeof(T) == 2, "bf16 activations");
   const size_t plane = (size_t)a.M * a.N;
   if ((int)blockIdx.x >= nvb) {
     // four consecutive pairs (j .. j + 3) of one head per thread
@@ -326,8 +324,22 @@ __global__ __launch_bounds__(256) void gemm_reduce_qkv_kernel(GemmArgs a, int nv
       v1 += *(const f32x4*)(pr + s * plane + c1);
       v2 += *(const f32x4*)(pr + s * plane + c2);
     }
+    // RoPE of the four pairs with epi_qkv's expressions, one 8-byte store per half
+    const int dst = a.row_dst[row];
+    const float2* cs = a.rope + (size_t)a.row_pos[row] * (HD / 2) + j;
+    T* p;
+    if (head < a.hq) p = (T*)a.Qb + ((size_t)head * a.ldq + row) * HD;
+    else if (dst_is_fresh(dst)) p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * HD;
+    else p = (T*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * HD;
+    bf16x4 o1, o2;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) epi_qkv<T>(a, row, head, j + e, v1[e], v2[e]);
+    for (int e = 0; e < 4; ++e) {
+      const float2 o = rope_rotate(v1[e], v2[e], cs[e]);
+      o1[e] = from_f32<T>(o.x);
+      o2[e] = from_f32<T>(o.y);
+    }
+    *(bf16x4*)(p + j) = o1;
+    *(bf16x4*)(p + j + HD / 2) = o2;
     return;
   }
   constexpr int RT = 32, TPR = HD / 4, RG = 256 / TPR, RPT = RT / RG;

@@ -53,15 +53,20 @@ __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int f, fl
   store_act<T>((T*)a.H, (T*)a.H2, act_at(row, f, a.ldh, a.h_tiled), s * u);
 }
 
+// RoPE of one (first-half, second-half) dimension pair by (cos, sin); the
+// single definition used by every epilogue that rotates q/k.
+__device__ __forceinline__ float2 rope_rotate(float v1, float v2, float2 cs) {
+  return make_float2(v1 * cs.x - v2 * cs.y, v2 * cs.x + v1 * cs.y);
+}
+
 // head in [0, hq + 2 hkv): q heads, k heads, v heads; v1 / v2 = dims j, j + hd/2
 template <class T>
 __device__ __forceinline__ void epi_qkv(const GemmArgs& a, int row, int head, int j, float v1, float v2) {
   const int hd = a.hd;
   const int dst = a.row_dst[row];
   if (head < a.hq + a.hkv) {
-    const float2 cs = a.rope[(size_t)a.row_pos[row] * (hd / 2) + j];
-    const float o1 = v1 * cs.x - v2 * cs.y;
-    const float o2 = v2 * cs.x + v1 * cs.y;
+    const float2 o = rope_rotate(v1, v2, a.rope[(size_t)a.row_pos[row] * (hd / 2) + j]);
+    const float o1 = o.x, o2 = o.y;
     T* p;
     if (head < a.hq) p = (T*)a.Qb + ((size_t)head * a.ldq + row) * hd;
     else if (dst_is_fresh(dst)) p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * hd;
