@@ -43,14 +43,18 @@ __device__ __forceinline__ void epi_resid(const GemmArgs& a, int row, int col, f
   a.X[(size_t)row * a.ldx + col] += v;
 }
 
+// SiLU(g) * u with the hardware exponential and reciprocal (v_exp_f32,
+// v_rcp_f32): a few ulp in fp32, far below the two-term bf16 rounding of the
+// stored product, for a fraction of the instructions of the IEEE-exact forms;
+// the denominator is >= 1 (and rcp(inf) = 0 gives the limit for large -g)
+__device__ __forceinline__ float silu_times(float g, float u) {
+  const float s = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+  return s * u;
+}
+
 template <class T>
 __device__ __forceinline__ void epi_swiglu(const GemmArgs& a, int row, int f, float g, float u) {
-  // SiLU with the hardware exponential and reciprocal (v_exp_f32, v_rcp_f32):
-  // a few ulp in fp32, far below the two-term bf16 rounding of the stored
-  // product, for a fraction of the instructions of the IEEE-exact forms; the
-  // denominator is >= 1 (and rcp(inf) = 0 gives the limit for large -g)
-  const float s = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
-  store_act<T>((T*)a.H, (T*)a.H2, act_at(row, f, a.ldh, a.h_tiled), s * u);
+  store_act<T>((T*)a.H, (T*)a.H2, act_at(row, f, a.ldh, a.h_tiled), silu_times(g, u));
 }
 
 // RoPE of one (first-half, second-half) dimension pair by (cos, sin); the
@@ -94,6 +98,52 @@ __device__ __forceinline__ void epi_tile_pair(const GemmArgs& a, int tile_n, int
   } else if constexpr (EPI == EPI_QKV) {
     const int half = a.hd / 2, p = tile_n * (BN / 2) + r;
     epi_qkv<T>(a, row, p / half, p % half, v1, v2);
+  }
+}
+
+// Epilogues of four consecutive tile columns r .. r + 3 of one row (r a
+// multiple of 4, so the four outputs are consecutive columns in every map
+// below): the same values as four single-column calls, written with vector
+// stores where the destination is aligned for them.
+__device__ __forceinline__ void epi_store4(const GemmArgs& a, int row, int col, f32x4 v) {
+  const int orow = a.out_row ? a.out_row[row] : row;
+  float* p = a.C + (size_t)orow * a.ldc + col;
+  if (((a.ldc & 3) | ((uintptr_t)a.C & 15)) == 0) {
+    *(f32x4*)p = v;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) p[e] = v[e];
+  }
+}
+
+__device__ __forceinline__ void epi_resid4(const GemmArgs& a, int row, int col, f32x4 v) {
+  float* p = a.X + (size_t)row * a.ldx + col;
+  if (((a.ldx & 3) | ((uintptr_t)a.X & 15)) == 0) {
+    *(f32x4*)p += v;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) p[e] += v[e];
+  }
+}
+
+template <int EPI, class T, int BN>
+__device__ __forceinline__ void epi_tile_pair4(const GemmArgs& a, int tile_n, int r, int row, f32x4 v1, f32x4 v2) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    const int f = tile_n * (BN / 2) + r;
+    const bool vec = sizeof(T) == 2 && ((a.h_tiled ? 0 : (a.ldh & 3)) | ((uintptr_t)a.H & 7) |
+                                        ((uintptr_t)a.H2 & 7)) == 0;
+    if (vec) {
+      float s[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s[e] = silu_times(v1[e], v2[e]);
+      store_act4<T>((T*)a.H, (T*)a.H2, act_at(row, f, a.ldh, a.h_tiled), s[0], s[1], s[2], s[3]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) epi_swiglu<T>(a, row, f + e, v1[e], v2[e]);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) epi_tile_pair<EPI, T, BN>(a, tile_n, r + e, row, v1[e], v2[e]);
   }
 }
 
