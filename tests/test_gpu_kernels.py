@@ -56,6 +56,28 @@ def test_gemm_two_term_activation_matches_oracle(M, N, K):
     np.testing.assert_allclose(Y, ref, rtol=0, atol=4e-5 * np.sqrt(K) * 4)
 
 
+@pytest.mark.parametrize("M,N,K", [(100, 256, 512), (37, 192, 4096)])
+def test_gemm_misaligned_output_equals_aligned(M, N, K):
+    """Y only 4-byte aligned (a view one float into a buffer): the epilogue's
+    element-store fallback gives the same bits as the vector stores, and
+    nothing outside Y is written."""
+    import ctypes as C
+
+    import torch
+    say(f"gemm bf16 misaligned Y M={M} N={N} K={K}")
+    a = archer()
+    A, _ = rand_bf16((M, K), 11, 1)
+    W, _ = rand_bf16((N, K), 11, 2)
+    Y = host(a.op_gemm(A, W, a.BF16))
+    buf = torch.full((M * N + 2,), 7.0, dtype=torch.float32, device="cuda")
+    rc = a.lib.archer_op_gemm(a.BF16, M, N, K, C.c_void_p(A.data_ptr()), None, C.c_void_p(W.data_ptr()),
+                              C.c_void_p(buf.data_ptr() + 4), C.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert rc == a.OK
+    got = host(buf)
+    np.testing.assert_array_equal(got[1:-1].reshape(M, N), Y)
+    assert got[0] == 7.0 and got[-1] == 7.0
+
+
 def test_gemm_deterministic():
     a = archer()
     A, _ = rand_bf16((256, 4096), 7, 1)
