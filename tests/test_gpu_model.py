@@ -10,8 +10,10 @@
 * the k-block weight layout: the pack kernel is the stated permutation, and a
   model gives the same bits in either layout (bf16 contexts use the k-block
   layout unless a test says otherwise, as the bench does);
-* a full-width 2-layer LLaDA-8B-shaped model (d 4096, vocab 126464, P 512,
-  G 256) in the bench's launch configuration.
+* full-width 2-layer LLaDA-8B-shaped models (d 4096, vocab 126464, G 256)
+  at P 512 and P 4096 in the bench's launch configurations (at P 4096: the
+  cached pass with 8-way split-KV, the 4352-row refresh with one split and
+  split-K projections).
 """
 
 import dataclasses
@@ -185,6 +187,34 @@ def test_full_width_two_layer_llada_shape():
     g1[100:140] = np.arange(40) * 11
     zc = host(ctx.step(dev_i32(g1[None])))[0]
     say("  oracle cached forward")
+    zc_ref, _ = om.cached_forward(W, m, g1, cache, P)
+    err = float(np.max(np.abs(zc - zc_ref)))
+    say(f"  cached forward max abs err {err:.3e}")
+    assert err < 2e-2
+
+
+def test_full_width_two_layer_llada_long_prompt():
+    """d 4096, 32 heads x 128, F 12288, vocab 126464, P 4096, G 256 (two layers)."""
+    import time
+    w = get_workload("llada_p4096")
+    m = dataclasses.replace(w.model, n_layers=2)
+    P, G = w.decode.prompt_len, w.decode.resp_len
+    say("full-width 2-layer LLaDA shape, P 4096: generating weights")
+    W = model_weights(m, seed=w.weight_seed)
+    p = prompts(w)[0]
+    ctx = make_ctx(m, W, 1, P, P, G)
+    g0 = np.full(G, m.mask_id)
+    g0[:64] = np.arange(64) * 5
+    z = host(ctx.refresh_prompt(dev_i32(p), [P], dev_i32(g0[None])))[0]
+    g1 = g0.copy()
+    g1[128:192] = np.arange(64) * 13
+    zc = host(ctx.step(dev_i32(g1[None])))[0]
+    t0 = time.time()
+    say("  oracle full forward (4352 rows)")
+    z_ref, cache, _ = om.full_forward(W, m, p, g0)
+    err = float(np.max(np.abs(z - z_ref)))
+    say(f"  full forward max abs err {err:.3e} (max |z| {np.max(np.abs(z_ref)):.2f}, oracle {time.time() - t0:.1f} s)")
+    assert err < 2e-2
     zc_ref, _ = om.cached_forward(W, m, g1, cache, P)
     err = float(np.max(np.abs(zc - zc_ref)))
     say(f"  cached forward max abs err {err:.3e}")
