@@ -30,11 +30,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 #define ATT_LGKMCNT0 (15 | (7 << 4) | (0 << 8) | (3 << 14))
 
 // Rescale threshold of the online softmax, in log2 units: the running maximum
-// is raised (and the accumulators rescaled) only when a tile's maximum exceeds
-// it by more than this, so probabilities stay below 2^8 and most tiles skip
-// the rescale.  The result is the same softmax (the final division uses the
-// same reference maximum); only rounding differs.
-constexpr float ATT_RESCALE_LOG2 = 8.0f;
+// is raised (and the accumulators rescaled) when a tile's maximum exceeds it
+// by more than this.  Zero is the plain online softmax (probabilities <= 1).
+// A lazy threshold of 8 (probabilities below 2^8, most tiles skipping the
+// rescale) computes the same softmax and was 1-5 % faster, but measured
+// against the float64 reference it raised the largest logit error of a
+// two-layer LLaDA-8B-shaped model from 5.8e-3 to 9.5e-3 at P 512 and from
+// 1.26e-2 to 1.65e-2 at P 4096.
+constexpr float ATT_RESCALE_LOG2 = 0.0f;
 
 // LDS layout of one 64-key stage.  K: row r (key) holds HD/8 16-byte chunks,
 // V^T: row d (dimension) holds 8 chunks of 8 keys.  Chunks are stored
@@ -319,7 +322,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
         for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
       }
     }
-    // p = 2^(s * scale_log2 - m): below 2^8 by the rescale rule; v_exp_f32
+    // p = 2^(s * scale_log2 - m): at most 1 by the rescale rule; v_exp_f32
     // flushes results below the normal range to 0, which the sum tolerates
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
