@@ -36,7 +36,11 @@ typedef __attribute__((address_space(3))) void lds_void;
 // rescale) computes the same softmax and was 1-5 % faster, but measured
 // against the float64 reference it raised the largest logit error of a
 // two-layer LLaDA-8B-shaped model from 5.8e-3 to 9.5e-3 at P 512 and from
-// 1.26e-2 to 1.65e-2 at P 4096.
+// 1.26e-2 to 1.65e-2 at P 4096.  The reason: with threshold 0 the key that
+// sets the maximum gets probability 2^0 = 1, exact in bf16, so the dominant
+// term of a peaked softmax enters P V without rounding; with a lazy threshold
+// the dominant probabilities are arbitrary values in (1, 2^8) and carry the
+// full bf16 rounding.
 constexpr float ATT_RESCALE_LOG2 = 0.0f;
 
 // LDS layout of one 64-key stage.  K: row r (key) holds HD/8 16-byte chunks,
