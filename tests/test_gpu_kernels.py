@@ -104,12 +104,12 @@ def test_gemm_full_size_sampled(N, K):
     np.testing.assert_allclose(got, ref, rtol=0, atol=2e-5 * np.sqrt(K) * 4 * 0.02)
 
 
-def _attn_case(dtype, Mq, Hq, Hkv, hd, nk1, nk2, seed, rows=None, heads=None):
+def _attn_case(dtype, Mq, Hq, Hkv, hd, nk1, nk2, seed, rows=None, heads=None, q_scale=1.0):
     a = archer()
     rand = rand_bf16 if dtype == a.BF16 else rand_f32
     ld1 = (nk1 + 63) // 64 * 64
     ld2 = (nk2 + 63) // 64 * 64
-    Q, Q64 = rand((Hq, Mq, hd), seed, 1)
+    Q, Q64 = rand((Hq, Mq, hd), seed, 1, q_scale)
     K1, K164 = rand((Hkv, ld1, hd), seed, 2)
     V1, V164 = rand((Hkv, hd, ld1), seed, 3)
     K2, K264 = rand((Hkv, ld2, hd), seed, 4)
@@ -138,6 +138,16 @@ def test_attention_bf16_matches_oracle(Mq, Hq, Hkv, hd, nk1, nk2):
     a = archer()
     # bf16 probabilities in the P.V product and a bf16 output: |err| <~ 2^-8 max|v|
     assert _attn_case(a.BF16, Mq, Hq, Hkv, hd, nk1, nk2, 11) < 2e-2
+
+
+@pytest.mark.parametrize("Mq,Hq,Hkv,nk1,nk2", [(256, 4, 4, 512, 256), (256, 4, 4, 4096, 256)])
+def test_attention_bf16_peaked_softmax_accuracy(Mq, Hq, Hkv, nk1, nk2):
+    """Scores with standard deviation 4 (a few keys dominate each query)."""
+    say(f"attention bf16 peaked softmax Mq={Mq} Hq={Hq} nk1={nk1} nk2={nk2}")
+    a = archer()
+    err = _attn_case(a.BF16, Mq, Hq, Hkv, 128, nk1, nk2, 14, q_scale=4.0)
+    say(f"  max abs err {err:.3e}")
+    assert err < 2e-2
 
 
 @pytest.mark.parametrize("Mq,Hq,Hkv,hd,nk1,nk2", [(33, 4, 2, 64, 100, 40), (8, 2, 1, 128, 300, 64)])
