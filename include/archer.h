@@ -186,6 +186,9 @@ archer_status archer_step(archer_ctx *ctx, const int32_t *response, const uint8_
 
 /* One decision g_out = D(g_in, logits) for all B sequences of the current
  * batch (device arrays, [B][G] and [B][G][V]; g_out must not alias g_in).
+ * D is the rollback decoder of Sec. 4.2 ("State-Anchored Refresh") and
+ * Algorithm 1, which owns token acceptance, replacement and re-masking; its
+ * rule here is the one described at archer_decide_cfg.
  * dist_out   device int32 [B]: d_H(g_out_b, g_r_b) against the current anchor, or NULL.
  * unmask_pos device int32 [B][k]: unmasked positions ascending, -1 padded, or NULL.
  *            (With final_step the list holds at most k entries; g_out is complete.)
@@ -204,6 +207,64 @@ archer_status archer_decide(archer_ctx *ctx, const float *logits, const int32_t 
 archer_status archer_decode(archer_ctx *ctx, int32_t batch, const int32_t *prompt,
                             const int32_t *prompt_len, int32_t *response_inout,
                             const archer_decode_cfg *cfg, archer_trace *trace);
+
+/* Algorithm 1 as a resumable session.  archer_decode is exactly
+ * archer_session_begin + archer_session_advance(T) + archer_session_response,
+ * then a synchronisation; the split lets a caller advance the schedule a few
+ * decisions at a time, read the state between decisions (archer_read_state),
+ * and save / restore the decoder state, e.g. to branch two continuations from
+ * one matched state as the matched-state feedback intervention of the
+ * paper's mechanism appendix does ("Fresh" rebuilds the prompt cache at once,
+ * "Cached" keeps the snapshot's cache).
+ *
+ * archer_session_begin: validate cfg as archer_decode does, start a new batch
+ * (as archer_refresh_prompt with seq_sel NULL), copy response_init (device
+ * int32 [B][G]) and run forward 0, a FullForward of every sequence.  Decision
+ * count t = 0.  prompt (device) and the trace arrays (device, optional; same
+ * meaning as for archer_decode) must stay valid while the session is used;
+ * row 0 of the trace is written here.  Does not synchronise.  The session
+ * ends when the context starts another batch (archer_refresh_prompt,
+ * archer_decode or another archer_session_begin); archer_step and
+ * archer_decide leave it intact. */
+archer_status archer_session_begin(archer_ctx *ctx, int32_t batch, const int32_t *prompt,
+                                   const int32_t *prompt_len, const int32_t *response_init,
+                                   const archer_decode_cfg *cfg, const archer_trace *trace);
+
+/* Which kind of pass the first forward of an archer_session_advance call is. */
+typedef enum {
+  ARCHER_FORWARD_CONTROLLER = 0,   /* the controller's rule, per sequence (normal decoding)  */
+  ARCHER_FORWARD_REFRESH = 1,      /* every sequence refreshes (FullForward, new anchor)     */
+  ARCHER_FORWARD_CACHED = 2        /* every sequence reuses its anchored cache (CachedForward) */
+} archer_forward_mode;
+
+/* Make up to n more decisions (stopping at the schedule's T), each followed,
+ * unless it is the last of the schedule, by the next forward: per sequence a
+ * refresh or a cached pass as the controller decides -- except the first
+ * forward of this call, whose kind first_forward (archer_forward_mode) may
+ * force.  *t_out (host, may be NULL) receives the number of decisions made so
+ * far.  ARCHER_E_STATE without an active session.  Synchronises once per
+ * decision under ARCHER_REFRESH_HAMMING (the controller reads D_t), never
+ * otherwise. */
+archer_status archer_session_advance(archer_ctx *ctx, int32_t n, int32_t first_forward, int32_t *t_out);
+
+/* Copy the session's current response g_t (device int32 [B][G]) to dst
+ * (device).  Asynchronous. */
+archer_status archer_session_response(archer_ctx *ctx, int32_t *dst);
+
+/* Bytes of a session snapshot of this context (0 and last_error if ctx is NULL). */
+size_t archer_session_state_bytes(const archer_ctx *ctx);
+
+/* Save the decoder state of the active session -- g_t, the anchor g_r, the
+ * logits z_t of the last forward, the prompt cache of every layer, the anchor
+ * steps r_b, t, the batch and the session's configuration -- into dst (device,
+ * 256-byte aligned, >= archer_session_state_bytes bytes, caller-owned).
+ * Synchronises.  archer_session_restore makes that state the context's active
+ * session again (same model and limits; the snapshot's prompt and trace
+ * pointers are used again), after which archer_session_advance continues
+ * exactly as it would have from the saved point.  Restore is asynchronous
+ * after it has read the snapshot's header (one synchronisation). */
+archer_status archer_session_save(archer_ctx *ctx, void *dst, size_t bytes);
+archer_status archer_session_restore(archer_ctx *ctx, const void *src, size_t bytes);
 
 /* Wait for all work of the context and report device-side argument errors. */
 archer_status archer_sync(archer_ctx *ctx);

@@ -74,6 +74,42 @@ archer_status archer_timing_begin(archer_ctx *ctx, uint32_t class_mask, int32_t 
 archer_status archer_timing_end(archer_ctx *ctx, int64_t *launches, double *total_ms,
                                 double *bytes, double *flops);
 
+/* Read-only copies of context state, for checking it against a reference
+ * (none of these changes the state).  dst: device, caller-owned, >= the
+ * stated size in bytes; copies are enqueued on the context's stream.
+ *   ARCHER_READ_LOGITS    fp32 [B][G][V]: the logits the session's decoder reads
+ *                         (those of the last forward of archer_decode or a session).
+ *   ARCHER_READ_HIDDEN    fp32 [n][d]: the final normalised hidden state (the LM
+ *                         head's input) of the response rows of the most recent
+ *                         forward pass, n = G x (sequences in that pass), in
+ *                         ascending sequence order.  bf16 models hold it as a
+ *                         two-term pair; the copy is hi + lo (exact in fp32).
+ *   ARCHER_READ_RESIDUAL  fp32 [n][d]: the residual stream after the last layer
+ *                         for the same rows.
+ *   ARCHER_READ_PROMPT_K  [Hkv][P_b][hd] of the model's element type: the cached
+ *   ARCHER_READ_PROMPT_V  post-RoPE prompt K / prompt V of layer `layer`,
+ *                         sequence `seq` -- C_p of Eq. app-cached (App. "Formal
+ *                         Analysis"), one layer of it.
+ * layer and seq are ignored where they do not apply.  ARCHER_E_STATE before
+ * the first forward (or for a sequence without a cache), ARCHER_E_ARG for a
+ * short dst or an unknown `what`. */
+enum {
+  ARCHER_READ_LOGITS = 0, ARCHER_READ_HIDDEN = 1, ARCHER_READ_RESIDUAL = 2,
+  ARCHER_READ_PROMPT_K = 3, ARCHER_READ_PROMPT_V = 4
+};
+archer_status archer_read_state(archer_ctx *ctx, int32_t what, int32_t layer, int32_t seq, void *dst,
+                                size_t bytes);
+
+/* Precision of the activation operand of each projection class (bf16 models).
+ * By default every projection multiplies a two-term bf16 activation
+ * (hi + lo, about 16 significant bits; two MFMAs per fragment).  A set bit
+ * ARCHER_K_GEMM_QKV, _O, _GATEUP, _DOWN or _HEAD in class_mask makes that
+ * class's producer store and its GEMM read the single bf16 rounding hi = bf16(v)
+ * instead (half the MFMA work of that projection).  Applies to forwards
+ * enqueued after the call.  ARCHER_E_ARG for other bits, ARCHER_E_UNSUPPORTED
+ * for a nonzero mask on an fp32 model. */
+archer_status archer_set_single_term(archer_ctx *ctx, uint32_t class_mask);
+
 #ifdef __cplusplus
 }
 #endif

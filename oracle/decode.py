@@ -1,16 +1,21 @@
-"""Algorithm 1: state-anchored rollback decoding (oracle; test infrastructure only).
+"""Archer decoding of one sequence (oracle; test infrastructure only).
 
-Algorithm 1 of the paper: start from g <- g_0 and g_r <- g_0, run a full
-forward; then repeatedly apply the decoder D and, unless decoding has
-terminated, either refresh (full forward, replace the cache, g_r <- g) when
-d_H(g, g_r) >= K or run the cached forward on the anchored cache.
+What feeds the decoder at step t is the controller's choice of logits,
+Eq. archer-controller (Sec. 4.2; Algorithm 1 states the same procedure):
 
-Termination is not defined in the paper (it belongs to D).  Reading: a fixed
-budget of T decisions -- decisions are numbered t = 0..T-1, the forward that
-precedes decision t is forward t (forward 0 is the initial full forward) and
-decoding ends after decision T-1, which unmasks every remaining masked row.
-So every run has exactly T forwards; the number R of them that are full
-refreshes gives the refresh fraction q_K = R / T of Eq. theory-speedup.
+    z~_t = Phi(g_t; C_p(g_t))   if the refresh predicate holds at t  (and then g_r := g_t, r := t)
+    z~_t = Phi(g_t; C_p(g_r))   otherwise
+    g_{t+1} = D(g_t, z~_t)
+
+with D_t = d_H(g_t, g_r) and A_t = t - r the signals of the predicate
+(:mod:`oracle.controller`).  Step 0 always takes the full forward: it
+creates the first anchor, g_r = g_0.
+
+Termination belongs to the decoder and the paper does not define it.
+Reading: a fixed budget of T decisions t = 0..T-1, each preceded by its
+forward (so exactly T forwards), the last decision unmasking every remaining
+masked row.  The number R of full forwards among the T gives the refresh
+fraction q_K = R / T of Eq. theory-speedup.
 
 Batches are decoded sequence by sequence: each sequence has its own anchor
 g_r, anchor step r and distance D_t.
@@ -31,51 +36,44 @@ from .model import cached_forward, full_forward
 class Trace:
     refreshed: list = field(default_factory=list)   # forward t was a full refresh
     dist: list = field(default_factory=list)        # D_t before forward t (0 at t = 0)
-    age: list = field(default_factory=list)         # A_t = t - r before forward t
+    age: list = field(default_factory=list)         # A_t = t - r before forward t (0 at t = 0)
     unmask: list = field(default_factory=list)      # U of decision t
     remask: list = field(default_factory=list)      # Rm of decision t
     states: list = field(default_factory=list)      # g_t entering forward t
-    logits: list = field(default_factory=list)      # z_t (kept only on request)
+    logits: list = field(default_factory=list)      # z~_t (kept only on request)
 
 
 def decode(W: dict, m, prompt: np.ndarray, g0: np.ndarray, *, steps: int, k: int,
            tau: float, policy: str, K: float, remask: bool = True,
            keep_logits: bool = False):
-    """Decode one sequence.  Returns ``(g_final, Trace)``."""
+    """Decode one sequence for ``steps`` decisions.  Returns ``(g_final, Trace)``."""
     prompt = np.asarray(prompt).copy()
     P = len(prompt)
     g = np.asarray(g0).copy()
     tr = Trace()
-    z, cache, _ = full_forward(W, m, prompt, g)
-    g_r, r = g.copy(), 0
-    tr.refreshed.append(True)
-    tr.dist.append(0)
-    tr.age.append(0)
-    tr.states.append(g.copy())
-    if keep_logits:
-        tr.logits.append(z)
+    g_r, r, cache = None, 0, None
     for t in range(steps):
-        final = t == steps - 1
-        g, U, Rm, _ = decide(z, g, m.mask_id, k, tau, final=final, remask=remask)
-        tr.unmask.append(U)
-        tr.remask.append(Rm)
-        if final:
-            break
-        s = t + 1
-        D = controller.hamming(g, g_r)
-        A = s - r
+        # the controller's signals before forward t, and its choice of logits
+        if t == 0:
+            D, A, refresh = 0, 0, True
+        else:
+            D, A = controller.hamming(g, g_r), t - r
+            refresh = controller.should_refresh(policy, K, D, A)
+        if refresh:
+            z, cache, _ = full_forward(W, m, prompt, g)
+            g_r, r = g.copy(), t
+        else:
+            z, _ = cached_forward(W, m, g, cache, P)
+        tr.refreshed.append(refresh)
         tr.dist.append(D)
         tr.age.append(A)
         tr.states.append(g.copy())
-        if controller.should_refresh(policy, K, D, A):
-            z, cache, _ = full_forward(W, m, prompt, g)
-            g_r, r = g.copy(), s
-            tr.refreshed.append(True)
-        else:
-            z, _ = cached_forward(W, m, g, cache, P)
-            tr.refreshed.append(False)
         if keep_logits:
             tr.logits.append(z)
+        # the decoder's step on those logits
+        g, U, Rm, _ = decide(z, g, m.mask_id, k, tau, final=t == steps - 1, remask=remask)
+        tr.unmask.append(U)
+        tr.remask.append(Rm)
     return g, tr
 
 

@@ -2,8 +2,7 @@
 
 Sec. 4.1 of the paper writes Phi_theta(g; C) for the generation forward that
 uses prompt cache C, and C_p(g) for the prompt K/V of every layer obtained
-when the response is g (App. A.1: C_p(g) stacks the prompt K/V states from
-every transformer layer).
+when the response is g (App. A.1, Eq. app-cached).
 
 * Eager / full forward (Eq. archer-fresh, Eq. app-eager):
   z*_t = Phi_theta(g_t; C_p(g_t)) -- all P+G positions are recomputed and the

@@ -34,8 +34,15 @@ EXPORTED = [
     "archer_workspace_bytes", "archer_init", "archer_refresh_prompt", "archer_step", "archer_decide",
     "archer_decode", "archer_sync", "archer_destroy", "archer_last_error", "archer_op_gemm",
     "archer_op_attention_ws_bytes", "archer_op_attention", "archer_timing_begin", "archer_timing_end",
-    "archer_pack_weight",
+    "archer_pack_weight", "archer_session_begin", "archer_session_advance", "archer_session_response",
+    "archer_session_state_bytes", "archer_session_save", "archer_session_restore", "archer_read_state",
+    "archer_set_single_term",
 ]
+FORWARD_CONTROLLER, FORWARD_REFRESH, FORWARD_CACHED = 0, 1, 2
+READ_LOGITS, READ_HIDDEN, READ_RESIDUAL, READ_PROMPT_K, READ_PROMPT_V = range(5)
+# projection classes that can take a single-term activation (archer_set_single_term)
+SINGLE_TERM_CLASSES = {"qkv": K_GEMM_QKV, "o": K_GEMM_O, "gateup": K_GEMM_GATEUP, "down": K_GEMM_DOWN,
+                       "head": K_GEMM_HEAD}
 
 
 class ModelCfg(C.Structure):
@@ -103,6 +110,23 @@ lib.archer_op_attention.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, 
                                     C.c_int32, P, P, C.c_int32, C.c_int32, P, P, C.c_size_t, P]
 lib.archer_pack_weight.restype = C.c_int
 lib.archer_pack_weight.argtypes = [C.c_int32, C.c_int32, C.c_int32, P, P, P]
+lib.archer_session_begin.restype = C.c_int
+lib.archer_session_begin.argtypes = [P, C.c_int32, P, C.POINTER(C.c_int32), P, C.POINTER(DecodeCfg),
+                                     C.POINTER(Trace)]
+lib.archer_session_advance.restype = C.c_int
+lib.archer_session_advance.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(C.c_int32)]
+lib.archer_session_response.restype = C.c_int
+lib.archer_session_response.argtypes = [P, P]
+lib.archer_session_state_bytes.restype = C.c_size_t
+lib.archer_session_state_bytes.argtypes = [P]
+lib.archer_session_save.restype = C.c_int
+lib.archer_session_save.argtypes = [P, P, C.c_size_t]
+lib.archer_session_restore.restype = C.c_int
+lib.archer_session_restore.argtypes = [P, P, C.c_size_t]
+lib.archer_read_state.restype = C.c_int
+lib.archer_read_state.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, P, C.c_size_t]
+lib.archer_set_single_term.restype = C.c_int
+lib.archer_set_single_term.argtypes = [P, C.c_uint32]
 lib.archer_timing_begin.restype = C.c_int
 lib.archer_timing_begin.argtypes = [P, C.c_uint32, C.c_int32]
 lib.archer_timing_end.restype = C.c_int
@@ -217,23 +241,98 @@ class Context:
                                  _ptr(um), _ptr(rm)))
         return g_out, dist, um, rm
 
+    @staticmethod
+    def _trace(steps, B, k):
+        dev = dict(device="cuda", dtype=torch.int32)
+        tens = dict(refreshed=torch.zeros(steps, B, **dev), dist=torch.zeros(steps, B, **dev),
+                    age=torch.zeros(steps, B, **dev), unmask_pos=torch.full((steps, B, k), -1, **dev),
+                    unmask_tok=torch.full((steps, B, k), -1, **dev),
+                    remask_pos=torch.full((steps, B), -1, **dev))
+        return tens, Trace(*[t.data_ptr() for t in tens.values()])
+
     def decode(self, prompt, prompt_len, response, *, policy, K, steps, k=1, tau=0.1, max_remask=1,
                trace=True):
         B = len(prompt_len)
         pl = (C.c_int32 * B)(*prompt_len)
         dc = DecodeCfg(policy, int(min(K, NEVER)), steps, k, tau, max_remask)
-        tr = None
-        tens = None
-        if trace:
-            dev = dict(device="cuda", dtype=torch.int32)
-            tens = dict(refreshed=torch.zeros(steps, B, **dev), dist=torch.zeros(steps, B, **dev),
-                        age=torch.zeros(steps, B, **dev), unmask_pos=torch.full((steps, B, k), -1, **dev),
-                        unmask_tok=torch.full((steps, B, k), -1, **dev),
-                        remask_pos=torch.full((steps, B), -1, **dev))
-            tr = Trace(*[t.data_ptr() for t in tens.values()])
+        tens, tr = self._trace(steps, B, k) if trace else (None, None)
         _check(lib.archer_decode(self.h, B, _ptr(prompt), pl, _ptr(response), C.byref(dc),
                                  C.byref(tr) if tr is not None else None))
         return response, tens
+
+    # -- the resumable session (Algorithm 1 a few decisions at a time) --------------------------
+    def session_begin(self, prompt, prompt_len, response_init, *, policy, K, steps, k=1, tau=0.1,
+                      max_remask=1, trace=True):
+        """Start a session; returns the trace tensors (or None).  prompt and the trace tensors are
+        kept alive by the context while the session may use them."""
+        B = len(prompt_len)
+        pl = (C.c_int32 * B)(*prompt_len)
+        dc = DecodeCfg(policy, int(min(K, NEVER)), steps, k, tau, max_remask)
+        tens, tr = self._trace(steps, B, k) if trace else (None, None)
+        self._session = (prompt, tens, tr)
+        self.B = B
+        _check(lib.archer_session_begin(self.h, B, _ptr(prompt), pl, _ptr(response_init), C.byref(dc),
+                                        C.byref(tr) if tr is not None else None))
+        return tens
+
+    def session_advance(self, n, first_forward=FORWARD_CONTROLLER):
+        t = C.c_int32(0)
+        _check(lib.archer_session_advance(self.h, n, first_forward, C.byref(t)))
+        return t.value
+
+    def session_response(self):
+        out = torch.empty(self.B, self.G, dtype=torch.int32, device="cuda")
+        _check(lib.archer_session_response(self.h, _ptr(out)))
+        return out
+
+    def session_state_bytes(self):
+        n = lib.archer_session_state_bytes(self.h)
+        if n == 0:
+            raise ArcherError(E_ARG, lib.archer_last_error().decode())
+        return n
+
+    def session_save(self):
+        """Snapshot of the session's decoder state (a device tensor; 256-byte aligned view)."""
+        n = self.session_state_bytes()
+        buf = torch.empty(n + 256, dtype=torch.uint8, device="cuda")
+        off = (-buf.data_ptr()) % 256
+        snap = buf[off: off + n]
+        _check(lib.archer_session_save(self.h, _ptr(snap), n))
+        return snap
+
+    def session_restore(self, snap):
+        _check(lib.archer_session_restore(self.h, _ptr(snap), snap.numel()))
+
+    # -- read-only state copies and the precision switch of archer_ops.h ------------------------
+    def read_logits(self, batch):
+        out = torch.empty(batch, self.G, self.V, dtype=torch.float32, device="cuda")
+        _check(lib.archer_read_state(self.h, READ_LOGITS, 0, 0, _ptr(out), out.numel() * 4))
+        return out
+
+    def read_rows(self, what, n_seq):
+        """Final normalised hidden (READ_HIDDEN) or final residual (READ_RESIDUAL) of the response
+        rows of the last forward: fp32 [n_seq * G][d]."""
+        out = torch.empty(n_seq * self.G, self.shape.d_model, dtype=torch.float32, device="cuda")
+        _check(lib.archer_read_state(self.h, what, 0, 0, _ptr(out), out.numel() * 4))
+        return out
+
+    def read_prompt_kv(self, layer, seq, prompt_len):
+        """Cached post-RoPE prompt K and prompt V of one layer and sequence: two [Hkv][P][hd] tensors."""
+        m = self.shape
+        shape = (m.n_kv_heads, prompt_len, m.head_dim)
+        out = []
+        for what in (READ_PROMPT_K, READ_PROMPT_V):
+            t = torch.empty(shape, dtype=torch_dtype(self.dtype), device="cuda")
+            _check(lib.archer_read_state(self.h, what, layer, seq, _ptr(t), t.numel() * t.element_size()))
+            out.append(t)
+        return out[0], out[1]
+
+    def set_single_term(self, classes):
+        """classes: names from SINGLE_TERM_CLASSES whose activation operand is a single bf16 value."""
+        mask = 0
+        for c in classes:
+            mask |= 1 << SINGLE_TERM_CLASSES[c]
+        _check(lib.archer_set_single_term(self.h, mask))
 
     def sync(self):
         _check(lib.archer_sync(self.h))

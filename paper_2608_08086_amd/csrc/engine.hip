@@ -155,10 +155,27 @@ struct archer_ctx {
   int w_tiled = 0;   // projection matrices in the k-block-major layout
   // session
   int batch = 0;
-  int plen[ARCHER_MAXB];
-  int cache_off[ARCHER_MAXB];
-  int tok_off[ARCHER_MAXB];
-  bool has_cache[ARCHER_MAXB];
+  int plen[ARCHER_MAXB] = {0};
+  int cache_off[ARCHER_MAXB] = {0};
+  int tok_off[ARCHER_MAXB] = {0};
+  bool has_cache[ARCHER_MAXB] = {false};
+  // projection classes (bits ARCHER_K_GEMM_*) whose activation operand is a
+  // single bf16 value instead of the two-term pair
+  uint32_t single_mask = 0;
+  // the most recent forward pass (for archer_read_state)
+  SeqPlan last{};
+  bool have_last = false;
+  uint32_t last_single = 0;
+  // decode session: Algorithm 1 advanced a number of decisions at a time
+  struct {
+    bool active = false;
+    archer_decode_cfg cfg{};
+    archer_trace tr{};
+    const int32_t* prompt = nullptr;
+    int T = 0, t = 0;          // decisions in the schedule / made so far
+    int cur = 0;               // g buffer (gbuf0 / gbuf1) holding the current response
+    int r[ARCHER_MAXB] = {0};  // step of each sequence's anchor
+  } ses;
   // timing
   bool t_on = false;
   uint32_t t_mask = 0;
@@ -278,7 +295,15 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   const size_t es = c->esz;
   float* x = c->at<float>(L.x);
   void* act = c->at<char>(L.act);
-  void* act2 = lo_part(c, L.act2);
+  // low terms of the activations feeding each projection class (null where the
+  // class takes a single bf16 operand)
+  const uint32_t sm = c->single_mask;
+  auto lo_for = [&](int cls, size_t off) -> void* { return ((sm >> cls) & 1u) ? nullptr : lo_part(c, off); };
+  void* act2_qkv = lo_for(ARCHER_K_GEMM_QKV, L.act2);
+  void* act2_mlp = lo_for(ARCHER_K_GEMM_GATEUP, L.act2);
+  void* o2 = lo_for(ARCHER_K_GEMM_O, L.O2);
+  void* h2 = lo_for(ARCHER_K_GEMM_DOWN, L.H2);
+  void* cn2 = lo_for(ARCHER_K_GEMM_HEAD, L.Cn2);
   int* row_pos = c->at<int>(L.row_pos);
   int* row_dst = c->at<int>(L.row_dst);
   archer_status st;
@@ -317,17 +342,17 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
 
   // RMSNorms whose input is the residual just updated by a split-K GEMM run
   // inside that GEMM's reduction (same arithmetic as the stand-alone kernel)
-  auto fuse_norm = [&](GemmArgs& a, const float* gain) {
+  auto fuse_norm = [&](GemmArgs& a, const float* gain, void* out2) {
     if (!is_bf16(c)) return;
-    a.ngain = gain; a.nout = act; a.nout2 = act2; a.neps = m.rms_eps; a.nld = L.Mmax; a.ntiled = 1;
+    a.ngain = gain; a.nout = act; a.nout2 = out2; a.neps = m.rms_eps; a.nld = L.Mmax; a.ntiled = 1;
   };
   bool normed = false;   // attn_norm of the current layer already applied
   for (int l = 0; l < m.n_layers; ++l) {
-    if (!normed && (st = norm(c->attn_norm[l], 0, rows, act, act2, L.Mmax))) return st;
+    if (!normed && (st = norm(c->attn_norm[l], 0, rows, act, act2_qkv, L.Mmax))) return st;
     normed = false;
     {
       GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_qkv[l], c->w_tiled ? qkv_n : d, rows, qkv_n, d);
-      a.A2 = act2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
+      a.A2 = act2_qkv; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.Qb = c->at<char>(L.Q); a.ldq = L.ldq;
       a.Kc = c->at<char>(L.Kc) + (size_t)l * L.cache_layer_elems * es;
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
@@ -345,7 +370,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
       a.ldcache = L.ldcache;
       a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
-      a.O = c->at<char>(L.O); a.O2 = lo_part(c, L.O2); a.ldo = tiled ? L.Mmax : hq * hd; a.o_tiled = tiled;
+      a.O = c->at<char>(L.O); a.O2 = o2; a.ldo = tiled ? L.Mmax : hq * hd; a.o_tiled = tiled;
       a.Opart = c->at<float>(L.Opart); a.ML = c->at<float>(L.ML);
       a.hq = hq; a.hkv = hkv; a.hd = hd;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
@@ -363,40 +388,43 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
     {
       GemmArgs a = gargs(c->at<char>(L.O), tiled ? L.Mmax : hq * hd, c->w_o[l], c->w_tiled ? d : hq * hd, rows,
                          d, hq * hd);
-      a.A2 = lo_part(c, L.O2); a.a_tiled = tiled; a.w_tiled = c->w_tiled;
+      a.A2 = o2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.X = x; a.ldx = d;
-      fuse_norm(a, c->mlp_norm[l]);
+      fuse_norm(a, c->mlp_norm[l], act2_mlp);
       if ((st = gemm(c, ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
       normed = gemm_fuses_norm(a);
     }
-    if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2, L.Mmax))) return st;
+    if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2_mlp, L.Mmax))) return st;
     normed = false;
     {
       GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_gate[l], c->w_tiled ? F : d, rows, 2 * F, d);
-      a.A2 = act2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
+      a.A2 = act2_mlp; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.W2 = c->w_up[l];
-      a.H = c->at<char>(L.H); a.H2 = lo_part(c, L.H2); a.ldh = tiled ? L.Mmax : F; a.h_tiled = tiled;
+      a.H = c->at<char>(L.H); a.H2 = h2; a.ldh = tiled ? L.Mmax : F; a.h_tiled = tiled;
       if ((st = gemm(c, ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
     }
     {
       GemmArgs a = gargs(c->at<char>(L.H), tiled ? L.Mmax : F, c->w_down[l], c->w_tiled ? d : F, rows, d, F);
-      a.A2 = lo_part(c, L.H2); a.a_tiled = tiled; a.w_tiled = c->w_tiled;
+      a.A2 = h2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.X = x; a.ldx = d;
-      if (l + 1 < m.n_layers) fuse_norm(a, c->attn_norm[l + 1]);
+      if (l + 1 < m.n_layers) fuse_norm(a, c->attn_norm[l + 1], act2_qkv);
       if ((st = gemm(c, ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
       normed = gemm_fuses_norm(a);
     }
   }
   const int nresp = pl.n * pl.G;
-  if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn), lo_part(c, L.Cn2), L.Rmax))) return st;
+  if ((st = norm(c->final_norm, 1, nresp, c->at<char>(L.Cn), cn2, L.Rmax))) return st;
   {
     GemmArgs a = gargs(c->at<char>(L.Cn), tiled ? L.Rmax : d, c->lm_head, c->w_tiled ? m.vocab : d, nresp,
                        m.vocab, d);
-    a.A2 = lo_part(c, L.Cn2); a.a_tiled = tiled; a.w_tiled = c->w_tiled;
+    a.A2 = cn2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
     a.C = logits; a.ldc = m.vocab; a.out_row = c->at<int>(L.out_row);
     if ((st = gemm(c, ARCHER_K_GEMM_HEAD, EPI_STORE, a))) return st;
   }
   HIPCHK(hipGetLastError());
+  c->last = pl;
+  c->have_last = true;
+  c->last_single = sm;
   return ARCHER_OK;
 }
 
@@ -460,6 +488,93 @@ archer_status read_err_flag(archer_ctx* c) {
     return fail(ARCHER_E_ARG, "a token id was outside [0, vocab) or a prompt token was MASK");
   }
   return ARCHER_OK;
+}
+
+archer_status check_decode_cfg(const archer_ctx* c, const archer_decode_cfg* dc) {
+  if (dc->policy < ARCHER_REFRESH_HAMMING || dc->policy > ARCHER_REFRESH_ALWAYS) return fail(ARCHER_E_ARG, "bad policy");
+  if (dc->K < 0) return fail(ARCHER_E_ARG, "K must be >= 0");
+  if (dc->steps < 1) return fail(ARCHER_E_ARG, "steps must be >= 1");
+  if (dc->unmask_per_step < 1 || dc->unmask_per_step > c->lim.resp_len) return fail(ARCHER_E_ARG, "unmask_per_step outside [1, G]");
+  if (!(dc->remask_threshold > 0.f && dc->remask_threshold < 1.f)) return fail(ARCHER_E_ARG, "remask_threshold outside (0, 1)");
+  if (dc->max_remask != 0 && dc->max_remask != 1) return fail(ARCHER_E_ARG, "max_remask must be 0 or 1");
+  return ARCHER_OK;
+}
+
+// The refresh rule of the controller (the one place it is decided):
+// Eq. archer-controller refreshes when the anchor distance D_t >= K; the age
+// rule refreshes when A_t = t - r >= K (the cache-age signal of Sec. 6.4);
+// ALWAYS refreshes at every forward (eager decoding).
+bool controller_refresh(int policy, int K, int D, int A) {
+  if (policy == ARCHER_REFRESH_ALWAYS) return true;
+  if (policy == ARCHER_REFRESH_AGE) return A >= K;
+  return D >= K;
+}
+
+// Session snapshot: a header (host state) followed by the device state of the
+// session -- the current response g_t, the anchor g_r, the logits z_t of the
+// last forward and the prompt cache of every layer.
+constexpr uint64_t kSnapMagic = 0x3170616e73726861ull;
+constexpr size_t kSnapHdr = 4096;
+
+struct SnapHeader {
+  uint64_t magic, total, cache_bytes;
+  int32_t n_layers, vocab, rmax, ldcache;
+  int32_t batch, plen[ARCHER_MAXB], cache_off[ARCHER_MAXB], tok_off[ARCHER_MAXB];
+  uint8_t has_cache[ARCHER_MAXB];
+  archer_decode_cfg cfg;
+  archer_trace tr;
+  const int32_t* prompt;
+  int32_t T, t, cur, r[ARCHER_MAXB];
+};
+static_assert(sizeof(SnapHeader) <= kSnapHdr, "snapshot header");
+
+struct SnapRegion {
+  size_t ws_off, snap_off, bytes;
+};
+
+size_t cache_bytes(const archer_ctx* c) { return (size_t)c->cfg.n_layers * c->L.cache_layer_elems * c->esz; }
+
+std::vector<SnapRegion> snapshot_regions(const archer_ctx* c) {
+  const Layout& L = c->L;
+  const size_t g = (size_t)L.Rmax * 4, z = (size_t)L.Rmax * c->cfg.vocab * 4, kv = cache_bytes(c);
+  std::vector<SnapRegion> r;
+  size_t off = kSnapHdr;
+  auto add = [&](size_t ws_off, size_t n) { r.push_back({ws_off, off, n}); off = align_up(off + n, 256); };
+  add(c->ses.cur ? L.gbuf1 : L.gbuf0, g);
+  add(L.g_anchor, g);
+  add(L.logits, z);
+  add(L.Kc, kv);
+  add(L.Vtc, kv);
+  return r;
+}
+
+size_t snapshot_bytes(const archer_ctx* c) {
+  const SnapRegion last = snapshot_regions(c).back();
+  return align_up(last.snap_off + last.bytes, 256);
+}
+
+void fill_header(const archer_ctx* c, SnapHeader& h) {
+  h.magic = kSnapMagic;
+  h.total = snapshot_bytes(c);
+  h.cache_bytes = cache_bytes(c);
+  h.n_layers = c->cfg.n_layers;
+  h.vocab = c->cfg.vocab;
+  h.rmax = c->L.Rmax;
+  h.ldcache = c->L.ldcache;
+  h.batch = c->batch;
+  for (int b = 0; b < ARCHER_MAXB; ++b) {
+    h.plen[b] = c->plen[b];
+    h.cache_off[b] = c->cache_off[b];
+    h.tok_off[b] = c->tok_off[b];
+    h.has_cache[b] = c->has_cache[b] ? 1 : 0;
+    h.r[b] = c->ses.r[b];
+  }
+  h.cfg = c->ses.cfg;
+  h.tr = c->ses.tr;
+  h.prompt = c->ses.prompt;
+  h.T = c->ses.T;
+  h.t = c->ses.t;
+  h.cur = c->ses.cur;
 }
 
 }  // namespace
@@ -533,6 +648,7 @@ archer_status archer_refresh_prompt(archer_ctx* c, int32_t batch, const int32_t*
   if (!prompt || !response || !logits) return fail(ARCHER_E_ARG, "null prompt, response or logits");
   archer_status st = seq_sel ? check_same_batch(c, batch, prompt_len) : set_batch(c, batch, prompt_len);
   if (st) return st;
+  c->ses.active = false;   // the anchors change outside the session's controller
   std::vector<int> sel;
   for (int b = 0; b < batch; ++b)
     if (!seq_sel || seq_sel[b]) sel.push_back(b);
@@ -573,69 +689,234 @@ archer_status archer_decide(archer_ctx* c, const float* logits, const int32_t* g
   return ARCHER_OK;
 }
 
-archer_status archer_decode(archer_ctx* c, int32_t batch, const int32_t* prompt, const int32_t* prompt_len,
-                            int32_t* response_inout, const archer_decode_cfg* dc, archer_trace* tr) {
+archer_status archer_session_begin(archer_ctx* c, int32_t batch, const int32_t* prompt,
+                                   const int32_t* prompt_len, const int32_t* response_init,
+                                   const archer_decode_cfg* dc, const archer_trace* tr) {
   if (!c || !dc) return fail(ARCHER_E_ARG, "null ctx or cfg");
-  if (!prompt || !response_inout) return fail(ARCHER_E_ARG, "null prompt or response");
-  if (dc->policy < ARCHER_REFRESH_HAMMING || dc->policy > ARCHER_REFRESH_ALWAYS) return fail(ARCHER_E_ARG, "bad policy");
-  if (dc->K < 0) return fail(ARCHER_E_ARG, "K must be >= 0");
-  if (dc->steps < 1) return fail(ARCHER_E_ARG, "steps must be >= 1");
-  if (dc->unmask_per_step < 1 || dc->unmask_per_step > c->lim.resp_len) return fail(ARCHER_E_ARG, "unmask_per_step outside [1, G]");
-  if (!(dc->remask_threshold > 0.f && dc->remask_threshold < 1.f)) return fail(ARCHER_E_ARG, "remask_threshold outside (0, 1)");
-  if (dc->max_remask != 0 && dc->max_remask != 1) return fail(ARCHER_E_ARG, "max_remask must be 0 or 1");
-  archer_status st = set_batch(c, batch, prompt_len);
+  if (!prompt || !response_init) return fail(ARCHER_E_ARG, "null prompt or response");
+  archer_status st = check_decode_cfg(c, dc);
   if (st) return st;
-  const int B = batch, G = c->lim.resp_len, T = dc->steps, k = dc->unmask_per_step;
-  int* g[2] = {c->at<int>(c->L.gbuf0), c->at<int>(c->L.gbuf1)};
-  float* logits = c->at<float>(c->L.logits);
-  HIPCHK(hipMemcpyAsync(g[0], response_inout, (size_t)B * G * 4, hipMemcpyDeviceToDevice, c->stream));
+  c->ses.active = false;
+  if ((st = set_batch(c, batch, prompt_len))) return st;
+  const int B = batch, G = c->lim.resp_len;
+  auto& S = c->ses;
+  S.cfg = *dc;
+  S.tr = tr ? *tr : archer_trace{};
+  S.prompt = prompt;
+  S.T = dc->steps;
+  S.t = 0;
+  S.cur = 0;
+  for (int b = 0; b < ARCHER_MAXB; ++b) S.r[b] = 0;
+  int* g0 = c->at<int>(c->L.gbuf0);
+  HIPCHK(hipMemcpyAsync(g0, response_init, (size_t)B * G * 4, hipMemcpyDeviceToDevice, c->stream));
+  // trace row 0: forward 0 is a full refresh, D_0 = A_0 = 0
+  I32Row ones{}, zeros{};
+  for (int b = 0; b < B; ++b) ones.v[b] = 1;
+  launch_store_rows(S.tr.refreshed, S.tr.age, ones, zeros, B, c->stream);
+  launch_store_rows(S.tr.dist, nullptr, zeros, zeros, B, c->stream);
   std::vector<int> all(B);
   for (int b = 0; b < B; ++b) all[b] = b;
-  std::vector<int> h_ref((size_t)T * B, 0), h_age((size_t)T * B, 0), r(B, 0);
-  std::vector<int> D(B, 0);
+  if ((st = run_forward(c, true, all, prompt, g0, c->at<float>(c->L.logits)))) return st;
+  for (int b = 0; b < B; ++b) c->has_cache[b] = true;
+  S.active = true;
+  return ARCHER_OK;
+}
 
-  if ((st = run_forward(c, true, all, prompt, g[0], logits))) return st;
-  for (int b = 0; b < B; ++b) { c->has_cache[b] = true; h_ref[b] = 1; }
-  int cur = 0;
-  for (int t = 0; t < T; ++t) {
+archer_status archer_session_advance(archer_ctx* c, int32_t n, int32_t first_forward, int32_t* t_out) {
+  if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  auto& S = c->ses;
+  if (!S.active) return fail(ARCHER_E_STATE, "no active decode session");
+  if (n < 0) return fail(ARCHER_E_ARG, "n must be >= 0");
+  if (first_forward < ARCHER_FORWARD_CONTROLLER || first_forward > ARCHER_FORWARD_CACHED)
+    return fail(ARCHER_E_ARG, "bad first_forward");
+  const int B = c->batch, T = S.T, k = S.cfg.unmask_per_step;
+  const archer_trace& tr = S.tr;
+  int* g[2] = {c->at<int>(c->L.gbuf0), c->at<int>(c->L.gbuf1)};
+  float* logits = c->at<float>(c->L.logits);
+  archer_status st;
+  for (int i = 0; i < n && S.t < T; ++i) {
+    const int t = S.t;
     const bool final = t == T - 1;
-    int32_t* trd = (tr && tr->dist && !final) ? tr->dist + (size_t)(t + 1) * B : nullptr;
-    int32_t* tru = (tr && tr->unmask_pos) ? tr->unmask_pos + (size_t)t * B * k : nullptr;
-    int32_t* trt = (tr && tr->unmask_tok) ? tr->unmask_tok + (size_t)t * B * k : nullptr;
-    int32_t* trr = (tr && tr->remask_pos) ? tr->remask_pos + (size_t)t * B : nullptr;
-    st = decide_impl(c, logits, g[cur], g[cur ^ 1], k, dc->remask_threshold, dc->max_remask, final ? 1 : 0,
-                     nullptr, nullptr, nullptr, trd, tru, trt, trr);
+    // decision t: g_{t+1} = D(g_t, z_t); its distance to the anchor is D_{t+1}
+    int32_t* trd = (tr.dist && !final) ? tr.dist + (size_t)(t + 1) * B : nullptr;
+    int32_t* tru = tr.unmask_pos ? tr.unmask_pos + (size_t)t * B * k : nullptr;
+    int32_t* trt = tr.unmask_tok ? tr.unmask_tok + (size_t)t * B * k : nullptr;
+    int32_t* trr = tr.remask_pos ? tr.remask_pos + (size_t)t * B : nullptr;
+    st = decide_impl(c, logits, g[S.cur], g[S.cur ^ 1], k, S.cfg.remask_threshold, S.cfg.max_remask,
+                     final ? 1 : 0, nullptr, nullptr, nullptr, trd, tru, trt, trr);
     if (st) return st;
-    cur ^= 1;
+    S.cur ^= 1;
+    S.t = t + 1;
     if (final) break;
+    // forward s = t + 1: the controller picks, per sequence, a refresh or a cached pass
     const int s = t + 1;
-    if (dc->policy == ARCHER_REFRESH_HAMMING) {
-      HIPCHK(hipMemcpyAsync(D.data(), c->at<int>(c->L.dist), (size_t)B * 4, hipMemcpyDeviceToHost, c->stream));
+    const int mode = i == 0 ? first_forward : ARCHER_FORWARD_CONTROLLER;
+    int D[ARCHER_MAXB] = {0};
+    if (mode == ARCHER_FORWARD_CONTROLLER && S.cfg.policy == ARCHER_REFRESH_HAMMING) {
+      HIPCHK(hipMemcpyAsync(D, c->at<int>(c->L.dist), (size_t)B * 4, hipMemcpyDeviceToHost, c->stream));
       HIPCHK(hipStreamSynchronize(c->stream));
     }
     std::vector<int> full, cached;
+    I32Row ref_row{}, age_row{};
     for (int b = 0; b < B; ++b) {
-      const int A = s - r[b];
-      h_age[(size_t)s * B + b] = A;
+      const int A = s - S.r[b];
       bool refresh;
-      if (dc->policy == ARCHER_REFRESH_ALWAYS) refresh = true;
-      else if (dc->policy == ARCHER_REFRESH_AGE) refresh = A >= dc->K;
-      else refresh = D[b] >= dc->K;
+      if (mode == ARCHER_FORWARD_REFRESH) refresh = true;
+      else if (mode == ARCHER_FORWARD_CACHED) refresh = false;
+      else refresh = controller_refresh(S.cfg.policy, S.cfg.K, D[b], A);
       (refresh ? full : cached).push_back(b);
-      if (refresh) { r[b] = s; h_ref[(size_t)s * B + b] = 1; }
+      ref_row.v[b] = refresh ? 1 : 0;
+      age_row.v[b] = A;
+      if (refresh) S.r[b] = s;
     }
-    if ((st = run_forward(c, true, full, prompt, g[cur], logits))) return st;
-    if ((st = run_forward(c, false, cached, nullptr, g[cur], logits))) return st;
+    launch_store_rows(tr.refreshed ? tr.refreshed + (size_t)s * B : nullptr,
+                      tr.age ? tr.age + (size_t)s * B : nullptr, ref_row, age_row, B, c->stream);
+    if ((st = run_forward(c, true, full, S.prompt, g[S.cur], logits))) return st;
+    if ((st = run_forward(c, false, cached, nullptr, g[S.cur], logits))) return st;
   }
-  HIPCHK(hipMemcpyAsync(response_inout, g[cur], (size_t)B * G * 4, hipMemcpyDeviceToDevice, c->stream));
-  if (tr && tr->dist) HIPCHK(hipMemsetAsync(tr->dist, 0, (size_t)B * 4, c->stream));
-  if (tr && tr->refreshed)
-    HIPCHK(hipMemcpyAsync(tr->refreshed, h_ref.data(), h_ref.size() * 4, hipMemcpyHostToDevice, c->stream));
-  if (tr && tr->age)
-    HIPCHK(hipMemcpyAsync(tr->age, h_age.data(), h_age.size() * 4, hipMemcpyHostToDevice, c->stream));
   HIPCHK(hipGetLastError());
+  if (t_out) *t_out = S.t;
+  return ARCHER_OK;
+}
+
+archer_status archer_session_response(archer_ctx* c, int32_t* dst) {
+  if (!c || !dst) return fail(ARCHER_E_ARG, "null ctx or dst");
+  if (!c->ses.active) return fail(ARCHER_E_STATE, "no active decode session");
+  const int* g = c->at<int>(c->ses.cur ? c->L.gbuf1 : c->L.gbuf0);
+  HIPCHK(hipMemcpyAsync(dst, g, (size_t)c->batch * c->lim.resp_len * 4, hipMemcpyDeviceToDevice, c->stream));
+  return ARCHER_OK;
+}
+
+size_t archer_session_state_bytes(const archer_ctx* c) {
+  if (!c) { g_err = "null ctx"; return 0; }
+  return snapshot_bytes(c);
+}
+
+archer_status archer_session_save(archer_ctx* c, void* dst, size_t bytes) {
+  if (!c || !dst) return fail(ARCHER_E_ARG, "null ctx or dst");
+  if (!c->ses.active) return fail(ARCHER_E_STATE, "no active decode session");
+  if (bytes < snapshot_bytes(c)) return fail(ARCHER_E_WORKSPACE, "snapshot buffer smaller than archer_session_state_bytes()");
+  if ((uintptr_t)dst & 255) return fail(ARCHER_E_ARG, "snapshot buffer must be 256-byte aligned");
+  SnapHeader h{};
+  fill_header(c, h);
+  char* d = (char*)dst;
+  for (const SnapRegion& r : snapshot_regions(c))
+    HIPCHK(hipMemcpyAsync(d + r.snap_off, c->ws + r.ws_off, r.bytes, hipMemcpyDeviceToDevice, c->stream));
+  HIPCHK(hipMemcpyAsync(d, &h, sizeof(h), hipMemcpyHostToDevice, c->stream));
+  HIPCHK(hipStreamSynchronize(c->stream));
+  return ARCHER_OK;
+}
+
+archer_status archer_session_restore(archer_ctx* c, const void* src, size_t bytes) {
+  if (!c || !src) return fail(ARCHER_E_ARG, "null ctx or src");
+  if (bytes < snapshot_bytes(c)) return fail(ARCHER_E_WORKSPACE, "snapshot smaller than archer_session_state_bytes()");
+  if ((uintptr_t)src & 255) return fail(ARCHER_E_ARG, "snapshot buffer must be 256-byte aligned");
+  SnapHeader h{};
+  HIPCHK(hipMemcpyAsync(&h, src, sizeof(h), hipMemcpyDeviceToHost, c->stream));
+  HIPCHK(hipStreamSynchronize(c->stream));
+  SnapHeader want{};
+  fill_header(c, want);
+  if (h.magic != kSnapMagic || h.total != want.total || h.n_layers != want.n_layers || h.vocab != want.vocab ||
+      h.rmax != want.rmax || h.ldcache != want.ldcache || h.cache_bytes != want.cache_bytes)
+    return fail(ARCHER_E_ARG, "not a snapshot of a context of this model and these limits");
+  if (h.batch < 1 || h.batch > c->lim.max_batch || h.cur < 0 || h.cur > 1 || h.t < 0 || h.t > h.T)
+    return fail(ARCHER_E_ARG, "corrupt snapshot header");
+  c->batch = h.batch;
+  for (int b = 0; b < ARCHER_MAXB; ++b) {
+    c->plen[b] = h.plen[b];
+    c->cache_off[b] = h.cache_off[b];
+    c->tok_off[b] = h.tok_off[b];
+    c->has_cache[b] = h.has_cache[b] != 0;
+    c->ses.r[b] = h.r[b];
+  }
+  c->ses.cfg = h.cfg;
+  c->ses.tr = h.tr;
+  c->ses.prompt = h.prompt;
+  c->ses.T = h.T;
+  c->ses.t = h.t;
+  c->ses.cur = h.cur;
+  const char* s = (const char*)src;
+  for (const SnapRegion& r : snapshot_regions(c))
+    HIPCHK(hipMemcpyAsync(c->ws + r.ws_off, s + r.snap_off, r.bytes, hipMemcpyDeviceToDevice, c->stream));
+  HIPCHK(hipGetLastError());
+  c->ses.active = true;
+  c->have_last = false;
+  return ARCHER_OK;
+}
+
+archer_status archer_decode(archer_ctx* c, int32_t batch, const int32_t* prompt, const int32_t* prompt_len,
+                            int32_t* response_inout, const archer_decode_cfg* dc, archer_trace* tr) {
+  archer_status st = archer_session_begin(c, batch, prompt, prompt_len, response_inout, dc, tr);
+  if (st) return st;
+  if ((st = archer_session_advance(c, dc->steps, ARCHER_FORWARD_CONTROLLER, nullptr))) return st;
+  if ((st = archer_session_response(c, response_inout))) return st;
   HIPCHK(hipStreamSynchronize(c->stream));
   return read_err_flag(c);
+}
+
+archer_status archer_read_state(archer_ctx* c, int32_t what, int32_t layer, int32_t seq, void* dst, size_t bytes) {
+  if (!c || !dst) return fail(ARCHER_E_ARG, "null ctx or dst");
+  const archer_model_cfg& m = c->cfg;
+  const Layout& L = c->L;
+  const int G = c->lim.resp_len, d = m.d_model;
+  const size_t es = c->esz;
+  if (what == ARCHER_READ_LOGITS) {
+    if (c->batch == 0) return fail(ARCHER_E_STATE, "no batch yet");
+    const size_t need = (size_t)c->batch * G * m.vocab * 4;
+    if (bytes < need) return fail(ARCHER_E_ARG, "dst too small");
+    HIPCHK(hipMemcpyAsync(dst, c->at<float>(L.logits), need, hipMemcpyDeviceToDevice, c->stream));
+    return ARCHER_OK;
+  }
+  if (what == ARCHER_READ_HIDDEN || what == ARCHER_READ_RESIDUAL) {
+    if (!c->have_last) return fail(ARCHER_E_STATE, "no forward pass since the context was created or restored");
+    const SeqPlan& pl = c->last;
+    const int n = pl.n * G;
+    if (bytes < (size_t)n * d * 4) return fail(ARCHER_E_ARG, "dst too small");
+    if (what == ARCHER_READ_HIDDEN) {
+      const bool two = is_bf16(c) && !((c->last_single >> ARCHER_K_GEMM_HEAD) & 1u);
+      if (is_bf16(c))
+        launch_read_act<bf16>(c->at<char>(L.Cn), two ? c->at<char>(L.Cn2) : nullptr, n, d, L.Rmax, 1, (float*)dst,
+                              c->stream);
+      else
+        launch_read_act<float>(c->at<char>(L.Cn), nullptr, n, d, d, 0, (float*)dst, c->stream);
+    } else {
+      const float* x = c->at<float>(L.x);
+      for (int s = 0; s < pl.n; ++s) {
+        const size_t r0 = (size_t)pl.row_off[s] + (pl.full ? pl.p_len[s] : 0);
+        HIPCHK(hipMemcpyAsync((float*)dst + (size_t)s * G * d, x + r0 * d, (size_t)G * d * 4,
+                              hipMemcpyDeviceToDevice, c->stream));
+      }
+    }
+    HIPCHK(hipGetLastError());
+    return ARCHER_OK;
+  }
+  if (what == ARCHER_READ_PROMPT_K || what == ARCHER_READ_PROMPT_V) {
+    if (layer < 0 || layer >= m.n_layers) return fail(ARCHER_E_ARG, "layer outside [0, n_layers)");
+    if (seq < 0 || seq >= c->batch || !c->has_cache[seq]) return fail(ARCHER_E_STATE, "sequence has no prompt cache");
+    const int P = c->plen[seq];
+    if (bytes < (size_t)m.n_kv_heads * P * m.head_dim * es) return fail(ARCHER_E_ARG, "dst too small");
+    const char* K = c->at<char>(L.Kc) + (size_t)layer * L.cache_layer_elems * es;
+    const char* Vt = c->at<char>(L.Vtc) + (size_t)layer * L.cache_layer_elems * es;
+    void* kd = what == ARCHER_READ_PROMPT_K ? dst : nullptr;
+    void* vd = what == ARCHER_READ_PROMPT_V ? dst : nullptr;
+    if (is_bf16(c))
+      launch_read_cache<bf16>(K, Vt, L.ldcache, c->cache_off[seq], P, m.n_kv_heads, m.head_dim, kd, vd, c->stream);
+    else
+      launch_read_cache<float>(K, Vt, L.ldcache, c->cache_off[seq], P, m.n_kv_heads, m.head_dim, kd, vd, c->stream);
+    HIPCHK(hipGetLastError());
+    return ARCHER_OK;
+  }
+  return fail(ARCHER_E_ARG, "unknown state");
+}
+
+archer_status archer_set_single_term(archer_ctx* c, uint32_t class_mask) {
+  if (!c) return fail(ARCHER_E_ARG, "null ctx");
+  const uint32_t allowed = (1u << ARCHER_K_GEMM_QKV) | (1u << ARCHER_K_GEMM_O) | (1u << ARCHER_K_GEMM_GATEUP) |
+                           (1u << ARCHER_K_GEMM_DOWN) | (1u << ARCHER_K_GEMM_HEAD);
+  if (class_mask & ~allowed) return fail(ARCHER_E_ARG, "class_mask names a class that is not a projection");
+  if (class_mask && !is_bf16(c)) return fail(ARCHER_E_UNSUPPORTED, "single-term activations are a bf16 option");
+  c->single_mask = class_mask;
+  return ARCHER_OK;
 }
 
 archer_status archer_sync(archer_ctx* c) {

@@ -363,3 +363,71 @@ void launch_fill_i32(int* p, int v, size_t n, hipStream_t st) {
   const int blocks = (int)std::min<size_t>((n + 255) / 256, 1024);
   fill_i32_kernel<<<blocks, 256, 0, st>>>(p, v, n);
 }
+
+// ---------------------------------------------------------------------------
+// Small copies of the session and state-read calls.
+//
+// Two rows of n <= ARCHER_MAXB ints passed by value (per-sequence trace rows of
+// a session step); a null destination is skipped.
+__global__ void store_rows_kernel(int* a, int* b, I32Row va, I32Row vb, int n) {
+  const int i = threadIdx.x;
+  if (i < n) {
+    if (a) a[i] = va.v[i];
+    if (b) b[i] = vb.v[i];
+  }
+}
+
+void launch_store_rows(int* a, int* b, const I32Row& va, const I32Row& vb, int n, hipStream_t st) {
+  if (n < 1 || (!a && !b)) return;
+  store_rows_kernel<<<1, ARCHER_MAXB, 0, st>>>(a, b, va, vb, n);
+}
+
+// Prompt K / V of one sequence out of one layer of the cache: K rows
+// [off, off + P) of every head plane [Hkv][ld][hd] and the same key columns of
+// V^T [Hkv][hd][ld], both written as [Hkv][P][hd].
+template <class T>
+__global__ void read_cache_kernel(const T* __restrict__ K, const T* __restrict__ Vt, int ld, int off, int P,
+                                  int hkv, int hd, T* __restrict__ Kd, T* __restrict__ Vd) {
+  const size_t n = (size_t)hkv * P * hd;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const int e = (int)(i % hd);
+    const size_t r = i / hd;
+    const int p = (int)(r % P), h = (int)(r / P);
+    if (Kd) Kd[i] = K[((size_t)h * ld + off + p) * hd + e];
+    if (Vd) Vd[i] = Vt[((size_t)h * hd + e) * ld + off + p];
+  }
+}
+
+template <class T>
+void launch_read_cache(const void* K, const void* Vt, int ld, int off, int P, int hkv, int hd, void* Kd, void* Vd,
+                       hipStream_t st) {
+  const size_t n = (size_t)hkv * P * hd;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+  read_cache_kernel<T><<<blocks, 256, 0, st>>>((const T*)K, (const T*)Vt, ld, off, P, hkv, hd, (T*)Kd, (T*)Vd);
+}
+template void launch_read_cache<float>(const void*, const void*, int, int, int, int, int, void*, void*, hipStream_t);
+template void launch_read_cache<bf16>(const void*, const void*, int, int, int, int, int, void*, void*, hipStream_t);
+
+// Activation rows (hi and optional lo term, layout act_at(row, k, ld, tiled))
+// -> fp32 row-major [n][d] holding hi + lo.  The sum is exact in fp32: lo is
+// the bf16 rounding of v - hi, at most 16 significant bits below hi's leading one.
+template <class T>
+__global__ void read_act_kernel(const T* __restrict__ hi, const T* __restrict__ lo, int n, int d, int ld, int tiled,
+                                float* __restrict__ out) {
+  const size_t tot = (size_t)n * d;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < tot; i += (size_t)gridDim.x * blockDim.x) {
+    const int r = (int)(i / d), k = (int)(i % d);
+    const size_t j = act_at(r, k, ld, tiled);
+    out[i] = to_f32(hi[j]) + (lo ? to_f32(lo[j]) : 0.f);
+  }
+}
+
+template <class T>
+void launch_read_act(const void* hi, const void* lo, int n, int d, int ld, int tiled, float* out, hipStream_t st) {
+  const size_t tot = (size_t)n * d;
+  if (tot == 0) return;
+  const int blocks = (int)std::min<size_t>((tot + 255) / 256, 4096);
+  read_act_kernel<T><<<blocks, 256, 0, st>>>((const T*)hi, (const T*)lo, n, d, ld, tiled, out);
+}
+template void launch_read_act<float>(const void*, const void*, int, int, int, int, float*, hipStream_t);
+template void launch_read_act<bf16>(const void*, const void*, int, int, int, int, float*, hipStream_t);

@@ -80,6 +80,14 @@ void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, cons
                    int* dist, int* unmask_pos, int* remask_pos, int* tr_dist, int* tr_unmask, int* tr_utok,
                    int* tr_remask, hipStream_t st);
 void launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
+// Session and state-read copies (kernels_misc.hip).
+struct I32Row { int v[ARCHER_MAXB]; };
+void launch_store_rows(int* a, int* b, const I32Row& va, const I32Row& vb, int n, hipStream_t st);
+template <class T>
+void launch_read_cache(const void* K, const void* Vt, int ld, int off, int P, int hkv, int hd, void* Kd, void* Vd,
+                       hipStream_t st);
+template <class T>
+void launch_read_act(const void* hi, const void* lo, int n, int d, int ld, int tiled, float* out, hipStream_t st);
 
 // GEMM: returns 0 on success, nonzero if the shape is unsupported.
 // Configurations 0 .. GEMM_NCFG-1: register-staged kernel (gemm.hip);

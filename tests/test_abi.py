@@ -71,6 +71,15 @@ def test_workspace_bytes_and_host_side_errors():
     assert archer.lib.archer_step(None, None, None, None) == archer.E_ARG
     assert archer.lib.archer_decode(None, 1, None, None, None, None, None) == archer.E_ARG
     assert archer.lib.archer_op_gemm(archer.BF16, 0, 64, 64, None, None, None, None, None) == archer.E_ARG
+    # session, state-read and precision calls refuse a null context before any HIP call
+    assert archer.lib.archer_session_begin(None, 1, None, None, None, None, None) == archer.E_ARG
+    assert archer.lib.archer_session_advance(None, 1, 0, None) == archer.E_ARG
+    assert archer.lib.archer_session_response(None, None) == archer.E_ARG
+    assert archer.lib.archer_session_state_bytes(None) == 0
+    assert archer.lib.archer_session_save(None, None, 0) == archer.E_ARG
+    assert archer.lib.archer_session_restore(None, None, 0) == archer.E_ARG
+    assert archer.lib.archer_read_state(None, 0, 0, 0, None, 0) == archer.E_ARG
+    assert archer.lib.archer_set_single_term(None, 0) == archer.E_ARG
     # shape checks happen on the host before any launch (N not a multiple of 64)
     assert archer.lib.archer_op_gemm(archer.BF16, 8, 60, 64, C.c_void_p(16), None, C.c_void_p(16),
                                      C.c_void_p(16), None) == archer.E_SHAPE

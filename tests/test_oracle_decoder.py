@@ -127,3 +127,102 @@ def test_margin_is_tight_for_a_planted_argmax_gap():
 def test_margin_zero_on_exact_tie():
     z = np.array([[1.0, 1.0, 0.0]])
     assert od.decision_margin(z, np.array([2]), 2, 1, 0.1) == 0.0
+
+
+# --- tightness of the top-k and remask terms of the margin ---------------------
+# Each case makes one term of the bound the binding one and applies the
+# perturbation that moves the two compared log-confidences towards each other
+# as fast as a sup-norm budget allows: on a flat row of V logits, lowering one
+# logit by eps and raising the others by eps moves its log-probability by
+# 2 eps (1 - p), p its probability.  The decision must hold just inside the
+# bound and flip just beyond it, so the term's constant is pinned from both
+# sides (a constant half as large would leave the flip unreached).
+
+V_FLAT = 1000
+
+
+def _peak_for_logprob(logp, V=V_FLAT):
+    """Peak height c over V - 2 zero logits (MASK excluded) giving log-probability logp."""
+    p = math.exp(logp)
+    return math.log(p * (V - 2) / (1.0 - p))
+
+
+def _flat_row(peak_id, c, V=V_FLAT):
+    z = np.zeros(V)
+    z[peak_id] = c
+    return z
+
+
+def _push(z, row, tok, eps, mask_id, down):
+    """Move row's log-probability of tok by about -2 eps (down) or +2 eps (up)."""
+    d = np.full(z.shape[1], eps if down else -eps)
+    d[tok] = -eps if down else eps
+    d[mask_id] = 0.0
+    z[row] += d
+
+
+def _check_tight(z, g, mask_id, k, tau, want_term, push, slack):
+    mD = od.decision_margin(z, g, mask_id, k, tau)
+    assert abs(mD - want_term) < 1e-12, (mD, want_term)
+    base = od.decide(z, g, mask_id, k, tau)[0].tolist()
+    inside, beyond = z.copy(), z.copy()
+    push(inside, 0.99 * mD)
+    push(beyond, slack * mD)
+    assert od.decide(inside, g, mask_id, k, tau)[0].tolist() == base
+    assert od.decide(beyond, g, mask_id, k, tau)[0].tolist() != base
+
+
+def test_margin_is_tight_for_the_unmask_set():
+    """k = 1, two masked rows whose log-confidences differ by 0.02: the bound is 0.005."""
+    mask_id, k, tau = V_FLAT - 1, 1, 0.1
+    l0 = -6.0
+    gap = 0.02
+    z = np.stack([_flat_row(3, _peak_for_logprob(l0)), _flat_row(5, _peak_for_logprob(l0 - gap))])
+    g = np.array([mask_id, mask_id])
+
+    def push(zz, eps):
+        _push(zz, 0, 3, eps, mask_id, down=True)
+        _push(zz, 1, 5, eps, mask_id, down=False)
+
+    _check_tight(z, g, mask_id, k, tau, gap / 4, push, 1.01)
+
+
+def test_margin_is_tight_for_the_remask_threshold():
+    """A decided row whose log-probability sits 0.02 above log(tau): the bound is 0.01
+    (tau small, so the row's probability is small and the push moves it by ~2 eps)."""
+    mask_id, k, tau = V_FLAT - 1, 1, 1e-3
+    q = math.log(tau) + 0.02
+    z = np.stack([_flat_row(3, 8.0), _flat_row(5, _peak_for_logprob(q)), _flat_row(6, 9.0)])
+    g = np.array([mask_id, 5, 6])
+
+    def push(zz, eps):
+        _push(zz, 1, 5, eps, mask_id, down=True)
+
+    _check_tight(z, g, mask_id, k, tau, 0.01, push, 1.01)
+    # and from below: the remask fires and a push up by just over the bound stops it
+    q2 = math.log(tau) - 0.02
+    z2 = z.copy()
+    z2[1] = _flat_row(5, _peak_for_logprob(q2))
+    assert od.decide(z2, g, mask_id, k, tau)[2] == [1]
+
+    def push_up(zz, eps):
+        _push(zz, 1, 5, eps, mask_id, down=False)
+
+    _check_tight(z2, g, mask_id, k, tau, 0.01, push_up, 1.01)
+
+
+def test_margin_is_tight_for_the_remasked_row():
+    """Two decided rows below log(tau) whose log-probabilities differ by 0.02: which one is
+    remasked has the bound 0.005."""
+    mask_id, k, tau = V_FLAT - 1, 1, 0.1
+    q1 = -7.0
+    gap = 0.02
+    z = np.stack([_flat_row(3, 8.0), _flat_row(5, _peak_for_logprob(q1)), _flat_row(6, _peak_for_logprob(q1 + gap))])
+    g = np.array([mask_id, 5, 6])
+    assert od.decide(z, g, mask_id, k, tau)[2] == [1]
+
+    def push(zz, eps):
+        _push(zz, 1, 5, eps, mask_id, down=False)
+        _push(zz, 2, 6, eps, mask_id, down=True)
+
+    _check_tight(z, g, mask_id, k, tau, gap / 4, push, 1.01)

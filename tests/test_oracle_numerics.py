@@ -33,6 +33,31 @@ def test_round_bf16_ties_and_direct_rounding():
         assert on.round_bf16(np.array([x]))[0] == want, x
 
 
+# --- bf16 bit patterns -> float64 (every bf16 weight the oracle reads) -------
+
+def test_weights_f64_matches_torch_bf16_view_on_every_bit_pattern():
+    """All 65536 bf16 bit patterns: the oracle's decoding equals torch's bf16 -> float64 cast
+    (a library routine that shares no code with it), NaNs in the same places."""
+    u = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = on.weights_f64(u)
+    ref = torch.from_numpy(u.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    np.testing.assert_array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def test_weights_f64_closed_forms():
+    pats = np.array([0x3F80, 0xC000, 0x3F81, 0x4049, 0x8000, 0x0001, 0x7F7F, 0x7F80], dtype=np.uint16)
+    want = [1.0, -2.0, 1.0 + 2.0 ** -7, 3.140625, -0.0, 2.0 ** -133, (2 - 2.0 ** -7) * 2.0 ** 127, math.inf]
+    got = on.weights_f64(pats)
+    assert got.tolist() == want
+    assert math.copysign(1.0, got[4]) == -1.0
+    # float32 weights pass through unchanged
+    x = np.array([0.1, -3.5e-7, 1e30], dtype=np.float32)
+    np.testing.assert_array_equal(on.weights_f64(x), x.astype(np.float64))
+
+
 # --- RMSNorm / SiLU against torch --------------------------------------------
 
 def test_rms_norm_matches_torch(rng):
