@@ -1,18 +1,26 @@
 #!/usr/bin/env python3
 """Throughput of Archer cached-prompt diffusion-LM decoding on one MI355X.
 
-One bench step = one archer_decode call: Algorithm 1 end to end over one
-batch of synthetic input -- the initial full forward, T denoising decisions,
-and before each later forward a refresh (FullForward, new prompt K/V cache)
-or a cached forward (CachedForward over the response rows only), chosen by
-the refresh rule.  Inputs are resident in HBM before the timed region.
+The workload (default: the batched ragged one -- LLaDA-8B shape, 16
+sequences with seeded prompt lengths in [256, 2048], G 256, T 256, refresh
+every 8 decisions) is decoded by Algorithm 1 as one decode session of the
+library (archer_session_begin / archer_session_advance).  One bench step is
+one refresh period of that decode: K decisions, each followed by its forward
+-- K - 1 cached forwards (CachedForward over the response rows only) and one
+refresh (FullForward, new prompt K/V cache) under the age rule.  Every step
+does the same work, and 32 steps are one whole 256-decision decode; when the
+schedule ends, the next decode's first forward (a refresh of every sequence)
+closes the step.  Inputs are resident in HBM before the timed region.
 
 Reported (one JSON line on stdout):
-  value                  denoising steps/s = steps * T / wall
-  response_tok_per_s     completed response tokens/s = steps * B * G / wall
-  speedup_vs_full_refresh  wall(refresh every step) / wall(Archer), same inputs and T
-  roofline               the kernel class with the most time in the timed region,
-                         algorithmic bytes (or flops) / its HIP-event time
+  value                  denoising steps/s = steps * K / wall
+  response_tok_per_s     completed response tokens/s = value * B * G / T
+  speedup_vs_full_refresh  wall(refresh at every forward) / wall(Archer), same work per step
+  roofline               the kernel class with the most time in the timed region:
+                         algorithmic flops (or bytes) / its HIP-event time, the
+                         attainable min(peak, AI * HBM) and the calibrated HBM traffic
+  gemm_rooflines         every projection class, cached and refresh passes apart
+  attention_roofline     the cache-reading attention of the cached passes against HBM
   cpu_baseline           the oracle on this host's cores on a bounded sample
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--policy age|hamming|always]
@@ -34,22 +42,11 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_TFLOPS = 157.3
 
-# kernel symbol of each timed class for the LLaDA-8B shape as rocprofv3 names it
-# (gemm_lds_kernel template arguments: BM, BN, wave grid, stages, epilogue,
-# two-term A, split mode; see csrc/gemm_lds.hip)
-KERNEL_OF_CLASS = {
-    "gemm_qkv": "gemm_lds_kernel<128, 192, 2, 2, 4, 3, true, 2> + gemm_reduce_kernel<3, bf16>",
-    "gemm_o": "gemm_lds_kernel<128, 128, 2, 2, 4, 1, true, 2> + gemm_reduce_kernel<1, bf16>",
-    "gemm_gateup": "gemm_lds_kernel<128, 192, 2, 2, 4, 2, true, 0>",
-    "gemm_down": "gemm_lds_kernel<128, 128, 2, 2, 4, 1, true, 2> + gemm_reduce_kernel<1, bf16>",
-    "gemm_head": "gemm_lds_kernel<128, 128, 2, 2, 4, 0, true, 0>",
-    "attn": "attn_bf16_kernel<128, QB, NW> + attn_merge_kernel<128> (CachedForward passes)",
-    "attn_full": "attn_bf16_kernel<128, QB, NW> + attn_merge_kernel<128> (FullForward passes)",
-    "norm": "rmsnorm_kernel<bf16>", "embed": "embed_kernel<bf16>", "decide": "rowstats_kernel + select_kernel",
-}
 # classes whose bf16 launches multiply two-term activations (two MFMAs per fragment)
-TWO_TERM = {"gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "gemm_head"}
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_gateup_llada_p512.json")
+GEMM_CLASSES = ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "gemm_head",
+                "gemm_qkv_full", "gemm_o_full", "gemm_gateup_full", "gemm_down_full")
+SINGLE_TERM_OF = {c: c.replace("gemm_", "").replace("_full", "") for c in GEMM_CLASSES}
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 
 
 def log(*a):
@@ -66,11 +63,13 @@ def src_hash(paths):
     return h.hexdigest()[:16]
 
 
-def committed_traffic(cls):
-    """HBM bytes per launch from the committed rocprofv3 PMC record, if it
-    was taken on the current kernel sources; else None."""
+def committed_traffic(workload, cls):
+    """HBM bytes per launch from the committed rocprofv3 PMC record of this
+    workload and kernel class, if it was taken on the current kernel sources;
+    else None."""
+    path = os.path.join(TRAFFIC_DIR, f"traffic_{cls}_{workload}.json")
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             rec = json.load(f)
         if rec.get("class") != cls or rec.get("kernel_sources_sha256_16") != src_hash(rec["kernel_sources"]):
             return None
@@ -79,9 +78,27 @@ def committed_traffic(cls):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, lens, T, K_refresh, policy, sample_layers=9):
-    """Time the oracle (as it is) on the first layers of the workload model at
-    full width and extrapolate to the whole decode."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, lens, T, K_refresh, policy):
+    """Time the oracle (as it is) on a bounded sample of the workload and
+    extrapolate to the whole decode.
+
+    Sample: the first S layers of the workload model at full width for the
+    shortest and the longest prompt of the batch (one sequence when all are
+    equal): one FullForward, one CachedForward, the LM head and one decision
+    each.  Per sequence b the per-layer times are interpolated linearly in its
+    row count between the two samples and scaled to all layers; the decode is
+    R refreshes, T - R cached forwards and T decisions per sequence."""
     import dataclasses
 
     import numpy as np
@@ -96,45 +113,67 @@ def cpu_baseline(w, lens, T, K_refresh, policy, sample_layers=9):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         cores = os.cpu_count() or 1
-    S = min(sample_layers, w.model.n_layers)
+    sample = sorted({int(np.argmin(lens)), int(np.argmax(lens))})
+    S = min(9 if len(sample) == 1 else 4, w.model.n_layers)
     mS = dataclasses.replace(w.model, n_layers=S)
     log(f"cpu baseline: generating {S} layers of host weights")
     W = model_weights(mS, seed=w.weight_seed)
-    p = prompts(w, lens)[0]
+    ps = prompts(w, lens)
     G = w.decode.resp_len
+    L = w.model.n_layers
     g = np.full(G, mS.mask_id)
     g[: G // 8] = np.arange(G // 8)
-    t0 = time.perf_counter()
-    z, cache, (hid, c) = om.full_forward(W, mS, p, g, keep_hidden=True)
-    t_fullS = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    zc, _ = om.cached_forward(W, mS, g, cache, len(p))
-    t_cachedS = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    on.linear(c, W["lm_head"])
-    t_head = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    od.decide(zc.astype(np.float32), g, mS.mask_id, w.decode.unmask_per_step, w.decode.remask_threshold)
-    t_dec = time.perf_counter() - t0
-    L = w.model.n_layers
-    t_full = L / S * max(t_fullS - t_head, 0.0) + t_head
-    t_cached = L / S * max(t_cachedS - t_head, 0.0) + t_head
+    per = {}
+    measured = 0.0
+    for b in sample:
+        p = ps[b]
+        t0 = time.perf_counter()
+        z, cache, (hid, c) = om.full_forward(W, mS, p, g, keep_hidden=True)
+        t_fullS = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        zc, _ = om.cached_forward(W, mS, g, cache, len(p))
+        t_cachedS = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        on.linear(c, W["lm_head"])
+        t_head = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        od.decide(zc.astype(np.float32), g, mS.mask_id, w.decode.unmask_per_step, w.decode.remask_threshold)
+        t_dec = time.perf_counter() - t0
+        measured += t_fullS + t_cachedS + t_head + t_dec
+        # per-layer times (the head is measured once and counted once per forward)
+        per[len(p)] = (max(t_fullS - t_head, 0.0) / S, max(t_cachedS - t_head, 0.0) / S, t_head, t_dec)
+        log(f"cpu baseline: P {len(p)}: {S}-layer full {t_fullS:.2f}s cached {t_cachedS:.2f}s "
+            f"head {t_head:.2f}s decide {t_dec:.2f}s")
+    Ps = sorted(per)
+
+    def at(P, i):
+        if len(Ps) == 1:
+            return per[Ps[0]][i]
+        lo, hi = Ps[0], Ps[-1]
+        return per[lo][i] + (P - lo) * (per[hi][i] - per[lo][i]) / (hi - lo)
+
     R = T if policy == "always" else math.ceil(T / max(K_refresh, 1))
-    total = R * t_full + (T - R) * t_cached + T * t_dec
-    measured = t_fullS + t_cachedS + t_head + t_dec
-    log(f"cpu baseline: {S}-layer full {t_fullS:.2f}s cached {t_cachedS:.2f}s head {t_head:.2f}s "
-        f"decide {t_dec:.2f}s -> decode {total:.1f}s extrapolated")
+    total = 0.0
+    for P in lens:
+        t_full = L * at(P, 0) + at(P, 2)
+        t_cached = L * at(P, 1) + at(P, 2)
+        total += R * t_full + (T - R) * t_cached + T * at(P, 3)
+    log(f"cpu baseline: decode {total:.1f}s extrapolated")
+    plist = " and ".join(str(len(ps[b])) for b in sample)
     return {"value": T / total, "unit": "steps/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"the first {S} layers of the workload model at full width: one FullForward over "
-                       f"{len(p) + G} rows, one CachedForward over {G} rows, the LM head over {G} rows and "
-                       f"one decision over {G}x{w.model.vocab} logits, float64 NumPy ({measured:.1f} s); "
-                       f"per-layer cost extrapolated to {L} layers and the {T}-step schedule with {R} refreshes"),
+            "cpu_model": cpu_model(),
+            "sample": (f"the first {S} of {L} layers of the workload model at full width, for the prompt(s) of "
+                       f"length {plist} of the batch: one FullForward, one CachedForward over {G} rows, the "
+                       f"LM head over {G} rows and one decision over {G}x{w.model.vocab} logits each, float64 "
+                       f"NumPy ({measured:.1f} s); per-layer times interpolated linearly in the prompt length "
+                       f"for the {len(lens)} sequence(s), scaled to {L} layers and the {T}-decision schedule "
+                       f"with {R} refreshes per sequence"),
             "measured_s": round(measured, 2)}
 
 
 def sweep(kind, reps=10):
     """Per-update and radius sweeps on the LLaDA-8B-shaped random-init model
-    (the paper's prompt-length and radius studies, App. F and App. B):
+    (the paper's prompt-length and radius studies, App. E and App. B):
       update:   FullForward vs CachedForward per-update time at G = 256 for
                 P in {128, 256, 512, 1024, 2048} (mean of `reps` synchronised calls)
       response: the same at P = 512 for G in {64, 128, 256, 512}
@@ -213,19 +252,51 @@ def sweep(kind, reps=10):
     print(json.dumps(out), flush=True)
 
 
+def roofline_of(t, peak_f, two_term, timing_every, traffic=None):
+    """Roofline object of one timed kernel class: algorithmic flops / bytes of the timed launches
+    over their HIP-event time; the binding unit follows the executed work (two-term GEMMs issue
+    2x the algorithmic MFMA work); attainable = min(peak, AI * HBM) at the algorithmic AI."""
+    sec = t["ms"] / 1e3
+    n = max(t["launches"], 1)
+    ridge = peak_f * 1e12 / (PEAK_HBM_GBS * 1e9)
+    exec_flops = t["flops"] * (2 if two_term else 1)
+    tflops = t["flops"] / sec / 1e12
+    gbs = t["bytes"] / sec / 1e9
+    ai = t["flops"] / max(t["bytes"], 1.0)
+    attainable_tflops = min(peak_f, ai * PEAK_HBM_GBS / 1e3)
+    if exec_flops > 0 and exec_flops / max(t["bytes"], 1.0) >= ridge:
+        r = {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak_f, "unit": "TFLOP/s"}
+    else:
+        r = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    r["frac"] = round(r["achieved"] / r["peak"], 4)
+    r["traffic"] = traffic
+    r.update({"launches": t["launches"], "avg_us": round(t["ms"] * 1e3 / n, 2),
+              "algorithmic_bytes_per_launch": round(t["bytes"] / n),
+              "algorithmic_flops_per_launch": round(t["flops"] / n),
+              "algorithmic_hbm_GBps": round(gbs, 1), "algorithmic_tflops": round(tflops, 2),
+              "arithmetic_intensity": round(ai, 1),
+              "attainable_tflops": round(attainable_tflops, 1),
+              "attainable_frac": round(tflops / attainable_tflops, 4) if attainable_tflops > 0 else None,
+              "two_term_activation": bool(two_term),
+              "executed_mfma_frac": round(exec_flops / sec / 1e12 / peak_f, 4),
+              "timing": f"HIP events around every {timing_every}th launch of the class in the timed "
+                        f"region, on the library's stream"})
+    return r
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="llada_p512")
+    ap.add_argument("--steps", type=int, default=10, help="timed refresh periods")
+    ap.add_argument("--warmup", type=int, default=2, help="untimed refresh periods before the timed ones")
+    ap.add_argument("--workload", default="llada_ragged16")
     ap.add_argument("--policy", default="age", choices=["age", "hamming", "always"])
+    ap.add_argument("--single-term", default="",
+                    help="comma-separated projections (qkv,o,gateup,down,head) with single-bf16 activations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-refresh", action="store_true")
     ap.add_argument("--timing-every", type=int, default=7,
                     help="time every n-th launch of the measured kernel classes (1 = all)")
-    ap.add_argument("--decode-steps", type=int, default=0,
-                    help="profiling only: override the workload's denoising steps per decode")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="profiling only: end with a 1 GiB device copy (known HBM traffic) for PMC scaling")
     ap.add_argument("--sweep", choices=["update", "response", "radius"],
@@ -234,6 +305,7 @@ def main():
                     help="run the cache-validity probe (shadow full forwards at cached steps) on the "
                          "workload instead of the throughput bench (prints its own JSON object)")
     ap.add_argument("--probe-every", type=int, default=4, help="probe every n-th cached forward")
+    ap.add_argument("--probe-steps", type=int, default=0, help="probe: decisions to run (0 = the workload's T)")
     args = ap.parse_args()
     if args.sweep:
         sweep(args.sweep)
@@ -242,6 +314,8 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    import dataclasses
 
     import numpy as np
     import torch
@@ -252,15 +326,15 @@ def main():
     from synth.workloads import get_workload
 
     w = get_workload(args.workload)
+    if args.single_term:
+        w = w.with_model(single_term=tuple(x for x in args.single_term.split(",") if x))
     m, dec = w.model, w.decode
     B, G, T, k = dec.batch, dec.resp_len, dec.steps, dec.unmask_per_step
-    if args.decode_steps:
-        T = args.decode_steps
     Kr = dec.refresh_every
     lens = prompt_lengths(w)
     pol = {"age": archer.AGE, "hamming": archer.HAMMING, "always": archer.ALWAYS}[args.policy]
     log(f"bench: workload {w.name} B={B} P={lens if len(lens) <= 4 else (min(lens), max(lens))} G={G} T={T} "
-        f"k={k} policy={args.policy} K={Kr}")
+        f"k={k} policy={args.policy} K={Kr} single_term={list(m.single_term)}")
     t0 = time.perf_counter()
     Wd = model_weights_cuda(m, seed=w.weight_seed)
     if m.dtype == "bf16":
@@ -270,18 +344,19 @@ def main():
     log(f"bench: device weights ready in {time.perf_counter() - t0:.1f}s")
     ctx = archer.Context(m, Wd, B, max(lens), sum(lens), G)
     prompt = torch.from_numpy(np.concatenate(prompts(w, lens)).astype(np.int32)).cuda()
-    resp = torch.full((B, G), m.mask_id, dtype=torch.int32, device="cuda")
+    resp0 = torch.full((B, G), m.mask_id, dtype=torch.int32, device="cuda")
     if args.probe:
         from paper_2608_08086_amd import probe
 
         # the shadow context's prompt cache is the scratch cache of the fresh forwards
         shadow = archer.Context(m, Wd, B, max(lens), sum(lens), G)
+        Tp = args.probe_steps or T
         t0 = time.perf_counter()
-        _, tr, recs = probe.shadow_probe(ctx, shadow, prompt, lens, resp, policy=pol, K=Kr, steps=T, k=k,
+        _, tr, recs = probe.shadow_probe(ctx, shadow, prompt, lens, resp0, policy=pol, K=Kr, steps=Tp, k=k,
                                          tau=dec.remask_threshold, every=args.probe_every)
         torch.cuda.synchronize()
         out = {"probe": "decision-level cache validity (non-intervening shadow full forwards)",
-               "workload": f"{w.name}: {w.note}", "policy": args.policy, "K": Kr, "steps": T,
+               "workload": f"{w.name}: {w.note}", "policy": args.policy, "K": Kr, "steps": Tp,
                "probe_every_cached_forward": args.probe_every, "wall_s": round(time.perf_counter() - t0, 3),
                "refresh_fraction": round(float(tr["refreshed"].mean()), 4),
                "data": "synthetic: random-init weights and prompts; values are not comparable to the paper's",
@@ -289,22 +364,32 @@ def main():
         print(json.dumps(out))
         return
 
-    def decode(policy, K):
-        resp.fill_(m.mask_id)
-        return ctx.decode(prompt, lens, resp, policy=policy, K=K, steps=T, k=k, tau=dec.remask_threshold,
-                          trace=True)
+    period = max(1, min(Kr, T))
 
-    # warm-up, with every kernel class timed once to find the dominant one
+    def runner(policy, K):
+        """One bench step = `period` decisions of a decode session (with their forwards)."""
+        st = {"t": 0}
+        tr = ctx.session_begin(prompt, lens, resp0, policy=policy, K=K, steps=T, k=k,
+                               tau=dec.remask_threshold, trace=True)
+
+        def step():
+            st["t"] = ctx.session_advance(period)
+            if st["t"] >= T:
+                # the schedule is complete: the next decode's forward 0 closes this period
+                ctx.session_begin(prompt, lens, resp0, policy=policy, K=K, steps=T, k=k,
+                                  tau=dec.remask_threshold, trace=False)
+                st["t"] = 0
+        return step, tr
+
+    step, tr = runner(pol, Kr)
+    # warm-up, with every kernel class timed in the first period to find the dominant one
+    args.warmup = max(args.warmup, 1)
     for i in range(args.warmup):
         if i == 0:
             ctx.timing_begin(range(archer.K_COUNT))
-        decode(pol, Kr)
+        step()
         if i == 0:
             warm = ctx.timing_end()
-    if args.warmup == 0:
-        ctx.timing_begin(range(archer.K_COUNT))
-        decode(pol, Kr)
-        warm = ctx.timing_end()
     dom = max(warm, key=lambda n: warm[n]["ms"])
     log("bench: warm-up ms per class " + ", ".join(f"{n}={v['ms']:.1f}" for n, v in warm.items() if v["launches"]))
 
@@ -312,54 +397,50 @@ def main():
     # a sample of the launches (every 7th of each class: 7 is coprime with the
     # layer count and the refresh period, so every layer and both pass kinds
     # are sampled) -- each event pair idles the GPU for a few microseconds
-    ctx.timing_begin(sorted({archer.K_NAMES.index(dom), archer.K_ATTN}), every=args.timing_every)
+    measured = sorted({archer.K_NAMES.index(c) for c in GEMM_CLASSES} | {archer.K_ATTN, archer.K_NAMES.index(dom)})
+    ctx.timing_begin(measured, every=args.timing_every)
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        _, tr = decode(pol, Kr)
+        step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     tims = ctx.timing_end()
-    tim = tims[dom]
-    refreshed = int(tr["refreshed"].sum().item())
-    log(f"bench: {args.steps} decodes in {wall:.3f}s -> {args.steps * T / wall:.1f} steps/s; "
-        f"refreshes per decode {refreshed}/{T * B}")
+    sps = args.steps * period / wall
+    log(f"bench: {args.steps} refresh periods of {period} decisions in {wall:.3f}s -> {sps:.2f} steps/s")
+
+    # refresh fraction of the timed forwards (those of the first decode's trace)
+    ref = tr["refreshed"].cpu().numpy()
+    lo = args.warmup * period + 1
+    hi = min(T, (args.warmup + args.steps) * period + 1)
+    refresh_fraction = float(ref[lo:hi].mean()) if hi > lo else None
 
     full_sps = None
     if not args.no_full_refresh and args.policy != "always":
+        fstep, _ = runner(archer.ALWAYS, 0)
+        fstep()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        decode(archer.ALWAYS, 0)
+        fstep()
         torch.cuda.synchronize()
-        full_wall = time.perf_counter() - t0
-        full_sps = T / full_wall
-        log(f"bench: full refresh every step: {full_sps:.1f} steps/s")
+        full_sps = period / (time.perf_counter() - t0)
+        log(f"bench: refresh at every forward: {full_sps:.2f} steps/s")
 
-    sps = args.steps * T / wall
-    tok = args.steps * B * G / wall
+    tok = sps * B * G / T
     peak_f = PEAK_BF16_TFLOPS if m.dtype == "bf16" else PEAK_FP32_TFLOPS
-    ridge = peak_f * 1e12 / (PEAK_HBM_GBS * 1e9)
-    sec = tim["ms"] / 1e3
-    nl = max(tim["launches"], 1)
-    exec_flops = tim["flops"] * (2 if (m.dtype == "bf16" and dom in TWO_TERM) else 1)
-    # the binding unit follows the executed work: two-term GEMMs issue 2x the
-    # algorithmic MFMA work, which moves them past the ridge
-    if exec_flops > 0 and exec_flops / max(tim["bytes"], 1.0) >= ridge:
-        roof = {"bound": "mfma", "achieved": round(tim["flops"] / sec / 1e12, 2), "peak": peak_f,
-                "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": round(tim["bytes"] / sec / 1e9, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = committed_traffic(dom)
-    roof.update({"kernel": KERNEL_OF_CLASS.get(dom, dom), "class": dom, "launches": tim["launches"],
-                 "avg_us": round(tim["ms"] * 1e3 / nl, 2),
-                 "algorithmic_bytes_per_launch": round(tim["bytes"] / nl),
-                 "algorithmic_flops_per_launch": round(tim["flops"] / nl),
-                 "algorithmic_hbm_GBps": round(tim["bytes"] / sec / 1e9, 1),
-                 "algorithmic_tflops": round(tim["flops"] / sec / 1e12, 2),
-                 "executed_mfma_frac": round(exec_flops / sec / 1e12 / peak_f, 4),
-                 "timing": f"HIP events around every {args.timing_every}th launch of the class in the timed "
-                           f"region, on the library's stream"})
+    single = set(m.single_term)
+
+    def two_term(cls):
+        return m.dtype == "bf16" and cls in GEMM_CLASSES and SINGLE_TERM_OF[cls] not in single
+
+    gemm_roofs = {}
+    for cls in GEMM_CLASSES:
+        if tims[cls]["launches"]:
+            gemm_roofs[cls] = roofline_of(tims[cls], peak_f, two_term(cls), args.timing_every,
+                                          committed_traffic(w.name, cls))
+    # the dominant class: the most time in the timed region (event time x sampling stride)
+    dom_t = max((c for c in tims if tims[c]["launches"]), key=lambda c: tims[c]["ms"])
+    roof = roofline_of(tims[dom_t], peak_f, two_term(dom_t), args.timing_every, committed_traffic(w.name, dom_t))
+    roof = {"class": dom_t, **roof}
 
     # the cache-reading attention of the cached passes, against the HBM roofline
     at = tims["attn"]
@@ -368,7 +449,8 @@ def main():
         asec = at["ms"] / 1e3
         att_roof = {"bound": "hbm", "achieved": round(at["bytes"] / asec / 1e9, 1), "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": round(at["bytes"] / asec / 1e9 / PEAK_HBM_GBS, 4),
-                    "kernel": KERNEL_OF_CLASS["attn"], "class": "attn", "launches": at["launches"],
+                    "traffic": committed_traffic(w.name, "attn"),
+                    "class": "attn", "launches": at["launches"],
                     "avg_us": round(at["ms"] * 1e3 / at["launches"], 2),
                     "algorithmic_bytes_per_launch": round(at["bytes"] / at["launches"]),
                     "algorithmic_flops_per_launch": round(at["flops"] / at["launches"]),
@@ -383,16 +465,20 @@ def main():
         "ms_per_step": round(wall / args.steps * 1e3, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": m.dtype,
         "data": "synthetic: seeded random-init weights N(0, 0.02) drawn on the GPU, uniform-random prompt tokens",
-        "config": {"workload": f"{w.name}: {w.note}", "batch": B, "prompt_len": lens[0] if len(set(lens)) == 1
-                   else [min(lens), max(lens)], "resp_len": G, "denoising_steps_per_decode": T,
+        "config": {"workload": f"{w.name}: {w.note}", "batch": B,
+                   "prompt_len": lens[0] if len(set(lens)) == 1 else [min(lens), max(lens)],
+                   "prompt_total": sum(lens), "resp_len": G, "denoising_steps_per_decode": T,
                    "unmask_per_step": k, "policy": args.policy, "K": Kr,
+                   "bench_step": f"one refresh period: {period} decisions with their forwards",
+                   "single_term_activations": sorted(single),
                    "weight_layout": "kblock" if m.dtype == "bf16" else "rowmajor"},
-        "response_tok_per_s": round(tok, 2),
-        "recomputed_positions_per_s": round(tok * T, 1),
-        "refresh_fraction": round(refreshed / (T * B), 4),
+        "response_tok_per_s": round(tok, 3),
+        "recomputed_positions_per_s": round(sps * B * G, 1),
+        "refresh_fraction": None if refresh_fraction is None else round(refresh_fraction, 4),
         "full_refresh_steps_per_s": None if full_sps is None else round(full_sps, 3),
         "speedup_vs_full_refresh": None if full_sps is None else round(sps / full_sps, 3),
         "roofline": roof,
+        "gemm_rooflines": gemm_roofs,
         "attention_roofline": att_roof,
         "warmup_ms_by_class": {n: round(v["ms"], 2) for n, v in warm.items() if v["launches"]},
     }

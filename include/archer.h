@@ -64,7 +64,9 @@ typedef enum { ARCHER_REFRESH_HAMMING = 0, ARCHER_REFRESH_AGE = 1, ARCHER_REFRES
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab, mask_id;
   float rms_eps, rope_theta;
-  int32_t dtype;              /* archer_dtype of weights, activations and caches */
+  int32_t dtype;              /* archer_dtype of weights and activations; ARCHER_BF16
+                                 models store queries, keys and values (and so the
+                                 prompt cache) as fp16, ARCHER_FP32 models as fp32 */
 } archer_model_cfg;
 
 /* Layouts of the projection matrices (lm_head, w_qkv, w_o, w_gate, w_up,

@@ -29,8 +29,10 @@ archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, con
 /* Non-causal attention of one sequence over two key segments, the anchored
  * attention of Eq. archer-attention: every query of head h attends to the nk1
  * keys of segment 1 followed by the nk2 keys of segment 2 of key/value head
- * h / (Hq / Hkv), scale 1 / sqrt(hd).
- *   Q   [Hq][Mq][hd]                    O  [Mq][Hq hd] (element type dtype)
+ * h / (Hq / Hkv), scale 1 / sqrt(hd).  Q, K and V are fp16 for ARCHER_BF16
+ * (as the bf16 model path stores them) and fp32 for ARCHER_FP32; O has the
+ * element type dtype (bf16 / fp32).
+ *   Q   [Hq][Mq][hd]                    O  [Mq][Hq hd]
  *   K1  [Hkv][ld1][hd]   Vt1 [Hkv][hd][ld1]   (segment 1, keys 0..nk1-1)
  *   K2  [Hkv][ld2][hd]   Vt2 [Hkv][hd][ld2]   (segment 2, keys 0..nk2-1)
  * V is stored transposed (Vt[h][d][key]).  ld1, ld2 multiples of 64,
@@ -48,14 +50,20 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
                                   int32_t ld2, void *O, void *workspace, size_t ws_bytes,
                                   void *hip_stream);
 
-/* Kernel classes for timing. */
+/* Kernel classes for timing.  The projection classes _QKV, _O, _GATEUP and
+ * _DOWN are the launches of CachedForward passes (M = G per sequence); their
+ * _FULL twins are the same projections in FullForward (refresh) passes
+ * (M = P_b + G per sequence).  The LM head runs on the response rows in both
+ * passes and has one class. */
 enum {
   ARCHER_K_EMBED = 0, ARCHER_K_NORM = 1, ARCHER_K_GEMM_QKV = 2,
   ARCHER_K_ATTN = 3 /* attention of CachedForward passes (with its split-KV merge) */,
   ARCHER_K_ATTN_FULL = 4 /* attention of FullForward (refresh) passes */,
   ARCHER_K_GEMM_O = 5, ARCHER_K_GEMM_GATEUP = 6,
   ARCHER_K_GEMM_DOWN = 7, ARCHER_K_GEMM_HEAD = 8, ARCHER_K_DECIDE = 9,
-  ARCHER_K_COUNT = 10
+  ARCHER_K_GEMM_QKV_FULL = 10, ARCHER_K_GEMM_O_FULL = 11, ARCHER_K_GEMM_GATEUP_FULL = 12,
+  ARCHER_K_GEMM_DOWN_FULL = 13,
+  ARCHER_K_COUNT = 14
 };
 
 /* Start recording HIP events around launches of the classes in class_mask
@@ -86,7 +94,8 @@ archer_status archer_timing_end(archer_ctx *ctx, int64_t *launches, double *tota
  *                         two-term pair; the copy is hi + lo (exact in fp32).
  *   ARCHER_READ_RESIDUAL  fp32 [n][d]: the residual stream after the last layer
  *                         for the same rows.
- *   ARCHER_READ_PROMPT_K  [Hkv][P_b][hd] of the model's element type: the cached
+ *   ARCHER_READ_PROMPT_K  [Hkv][P_b][hd] of the cache's element type (fp16 for
+ *                         ARCHER_BF16 models, fp32 for ARCHER_FP32): the cached
  *   ARCHER_READ_PROMPT_V  post-RoPE prompt K / prompt V of layer `layer`,
  *                         sequence `seq` -- C_p of Eq. app-cached (App. "Formal
  *                         Analysis"), one layer of it.

@@ -19,6 +19,11 @@ fraction q_K = R / T of Eq. theory-speedup.
 
 Batches are decoded sequence by sequence: each sequence has its own anchor
 g_r, anchor step r and distance D_t.
+
+``force`` overrides the predicate at chosen forwards ({t: True} refreshes,
+{t: False} reuses the anchored cache): the two branches of the matched-state
+feedback intervention (the paper's mechanism appendix) continue one decoder
+state with an immediate refresh and with the old cache.
 """
 
 from __future__ import annotations
@@ -45,7 +50,7 @@ class Trace:
 
 def decode(W: dict, m, prompt: np.ndarray, g0: np.ndarray, *, steps: int, k: int,
            tau: float, policy: str, K: float, remask: bool = True,
-           keep_logits: bool = False):
+           keep_logits: bool = False, force: dict | None = None):
     """Decode one sequence for ``steps`` decisions.  Returns ``(g_final, Trace)``."""
     prompt = np.asarray(prompt).copy()
     P = len(prompt)
@@ -59,6 +64,8 @@ def decode(W: dict, m, prompt: np.ndarray, g0: np.ndarray, *, steps: int, k: int
         else:
             D, A = controller.hamming(g, g_r), t - r
             refresh = controller.should_refresh(policy, K, D, A)
+            if force is not None and t in force:
+                refresh = bool(force[t])
         if refresh:
             z, cache, _ = full_forward(W, m, prompt, g)
             g_r, r = g.copy(), t

@@ -24,24 +24,33 @@ absolute positions (prompt 0..P-1, response P..P+G-1).  The prompt K is
 cached after RoPE (positions never change, so this equals caching it before).
 
 Precision (the paper fixes none).  bf16 models: weights are bf16, and the
-oracle rounds to bf16 exactly where the bf16 path stores single-bf16 values:
-the post-RoPE queries and keys and the values (hence the prompt cache).  The
-bf16 path carries every other activation (normalised inputs of the
-projections, attention output, SwiGLU product, final normalised hidden
-state) at about 16 significant bits, so the oracle keeps those unrounded;
-the residual stream and the logits are not rounded either.  fp32 models
-round nowhere.
+oracle rounds exactly where the bf16 path stores values with few bits: the
+post-RoPE queries and keys and the values (hence the prompt cache) are
+stored as fp16, and the activation operand of every projection named in
+``m.single_term`` ("qkv": the normalised attention input, "o": the attention
+output, "gateup": the normalised MLP input, "down": the SwiGLU product,
+"head": the final normalised hidden state) as a single bf16 value.  The bf16
+path carries the other activations, and the attention probabilities, at 16
+or more significant bits, so the oracle keeps those unrounded; the residual
+stream and the logits are not rounded either.  fp32 models round nowhere.
 """
 
 from __future__ import annotations
 
 import numpy as np
 
-from .numerics import attention, linear, rms_norm, rope, round_bf16, silu, weights_f64
+from .numerics import attention, linear, rms_norm, rope, round_bf16, round_fp16, silu, weights_f64
 
 
-def _rnd(m, x):
-    return round_bf16(x) if m.dtype == "bf16" else x
+def _qkv_store(m, x):
+    """Queries, keys and values as the path stores them (fp16 for bf16 models)."""
+    return round_fp16(x) if m.dtype == "bf16" else x
+
+
+def _operand(m, name, x):
+    """Activation operand of projection ``name``: single bf16 where the model says so."""
+    single = m.dtype == "bf16" and name in getattr(m, "single_term", ())
+    return round_bf16(x) if single else x
 
 
 def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
@@ -73,14 +82,14 @@ def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
     for l in range(m.n_layers):
         Wl = W["layers"][l]
         # attention block
-        a = rms_norm(x, Wl["attn_norm"], m.rms_eps)
+        a = _operand(m, "qkv", rms_norm(x, Wl["attn_norm"], m.rms_eps))
         qkv = linear(a, Wl["w_qkv"])
         q = qkv[:, : hq * hd].reshape(n, hq, hd)
         k = qkv[:, hq * hd: (hq + hkv) * hd].reshape(n, hkv, hd)
         v = qkv[:, (hq + hkv) * hd:].reshape(n, hkv, hd)
-        q = _rnd(m, rope(q, positions, m.rope_theta))
-        k = _rnd(m, rope(k, positions, m.rope_theta))
-        v = _rnd(m, v)
+        q = _qkv_store(m, rope(q, positions, m.rope_theta))
+        k = _qkv_store(m, rope(k, positions, m.rope_theta))
+        v = _qkv_store(m, v)
         k_rows = k.transpose(1, 0, 2)          # [Hkv][n][hd]
         v_rows = v.transpose(1, 0, 2)
         kv.append((k_rows, v_rows))
@@ -92,17 +101,17 @@ def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
         o = np.empty((n, hq, hd))
         for h in range(hq):
             o[:, h, :] = attention(q[:, h, :], k_all[h // group], v_all[h // group])
-        o = o.reshape(n, hq * hd)
+        o = _operand(m, "o", o.reshape(n, hq * hd))
         x = x + linear(o, Wl["w_o"])
         # SwiGLU MLP block
-        b = rms_norm(x, Wl["mlp_norm"], m.rms_eps)
+        b = _operand(m, "gateup", rms_norm(x, Wl["mlp_norm"], m.rms_eps))
         gate = linear(b, Wl["w_gate"])
         up = linear(b, Wl["w_up"])
-        hmid = silu(gate) * up
+        hmid = _operand(m, "down", silu(gate) * up)
         x = x + linear(hmid, Wl["w_down"])
         if keep_hidden:
             hidden.append(x.copy())
-    c = rms_norm(x[out_rows], W["final_norm"], m.rms_eps)
+    c = _operand(m, "head", rms_norm(x[out_rows], W["final_norm"], m.rms_eps))
     z = linear(c, W["lm_head"])
     if keep_hidden:
         return z, kv, (np.stack(hidden), c)

@@ -4,7 +4,8 @@ The paper treats the backbone Phi_theta abstractly (Sec. 4.1); the operations
 below are those of the named backbones' architecture family (pre-norm
 bidirectional transformer with RMSNorm, rotate-half RoPE, SwiGLU MLP).  The
 paper fixes no precision, so the oracle computes in float64 and emulates the
-bf16 storage points of the bf16 path with :func:`round_bf16`.
+storage points of the bf16 path with :func:`round_bf16` and
+:func:`round_fp16`.
 """
 
 from __future__ import annotations
@@ -41,6 +42,13 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
         f = (f + np.uint32(0x7FFF) + ((f >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
         out[tiny] = f.view(np.float32).astype(np.float64)
     return out
+
+
+def round_fp16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest IEEE half-precision value (ties to
+    even; 11 significant bits, subnormals below 2^-14, overflow to inf), by
+    NumPy's float64 -> float16 conversion, which rounds once."""
+    return np.asarray(x, dtype=np.float64).astype(np.float16).astype(np.float64)
 
 
 def rms_norm(x: np.ndarray, gain: np.ndarray, eps: float) -> np.ndarray:

@@ -26,9 +26,10 @@ HAMMING, AGE, ALWAYS = 0, 1, 2
 LAYOUT_ROWMAJOR, LAYOUT_KBLOCK = 0, 1
 NEVER = 2**31 - 1
 K_EMBED, K_NORM, K_GEMM_QKV, K_ATTN, K_ATTN_FULL, K_GEMM_O, K_GEMM_GATEUP, K_GEMM_DOWN, K_GEMM_HEAD, K_DECIDE = range(10)
-K_COUNT = 10
+K_GEMM_QKV_FULL, K_GEMM_O_FULL, K_GEMM_GATEUP_FULL, K_GEMM_DOWN_FULL = range(10, 14)
+K_COUNT = 14
 K_NAMES = ["embed", "norm", "gemm_qkv", "attn", "attn_full", "gemm_o", "gemm_gateup", "gemm_down",
-           "gemm_head", "decide"]
+           "gemm_head", "decide", "gemm_qkv_full", "gemm_o_full", "gemm_gateup_full", "gemm_down_full"]
 
 EXPORTED = [
     "archer_workspace_bytes", "archer_init", "archer_refresh_prompt", "archer_step", "archer_decide",
@@ -160,6 +161,11 @@ def torch_dtype(dtype: int):
     return torch.bfloat16 if dtype == BF16 else torch.float32
 
 
+def qkv_dtype(dtype: int):
+    """Element type of stored queries, keys and values (the prompt cache): fp16 for bf16 models."""
+    return torch.float16 if dtype == BF16 else torch.float32
+
+
 class Context:
     """One archer_ctx: a model's weights (device tensors), limits and workspace."""
 
@@ -199,6 +205,8 @@ class Context:
         _check(lib.archer_init(C.byref(self.cfg), C.byref(self.cw), C.byref(self.lim), C.c_void_p(self._ws_ptr),
                                nbytes, _stream(), C.byref(h)))
         self.h = h
+        if getattr(shape, "single_term", ()):
+            self.set_single_term(shape.single_term)
 
     def close(self):
         if getattr(self, "h", None):
@@ -322,7 +330,7 @@ class Context:
         shape = (m.n_kv_heads, prompt_len, m.head_dim)
         out = []
         for what in (READ_PROMPT_K, READ_PROMPT_V):
-            t = torch.empty(shape, dtype=torch_dtype(self.dtype), device="cuda")
+            t = torch.empty(shape, dtype=qkv_dtype(self.dtype), device="cuda")
             _check(lib.archer_read_state(self.h, what, layer, seq, _ptr(t), t.numel() * t.element_size()))
             out.append(t)
         return out[0], out[1]
@@ -409,11 +417,14 @@ def op_gemm(A, Wt, dtype=BF16, A_lo=None):
 
 
 def op_attention(Q, K1, Vt1, nk1, K2, Vt2, nk2, dtype=BF16):
-    """Q [Hq][Mq][hd]; K1 [Hkv][ld1][hd], Vt1 [Hkv][hd][ld1]; same for segment 2.  Returns O [Mq][Hq*hd]."""
+    """Q [Hq][Mq][hd]; K1 [Hkv][ld1][hd], Vt1 [Hkv][hd][ld1]; same for segment 2 (fp16 for BF16,
+    fp32 for FP32).  Returns O [Mq][Hq*hd] (bf16 for BF16, fp32 for FP32)."""
     Hq, Mq, hd = Q.shape
     Hkv, ld1, _ = K1.shape
     ld2 = K2.shape[1]
-    O = torch.empty(Mq, Hq * hd, dtype=Q.dtype, device="cuda")
+    for t in (Q, K1, Vt1, K2, Vt2):
+        assert t.dtype == qkv_dtype(dtype), "queries, keys and values: fp16 for BF16, fp32 for FP32"
+    O = torch.empty(Mq, Hq * hd, dtype=torch_dtype(dtype), device="cuda")
     nbytes = lib.archer_op_attention_ws_bytes(dtype, Mq, Hq, hd, ((nk1 + 63) // 64) * 64 + nk2)
     ws = torch.empty(max(nbytes, 1) + 256, dtype=torch.uint8, device="cuda")
     wp = ws.data_ptr() + ((-ws.data_ptr()) % 256)

@@ -2,7 +2,12 @@
 // row of a sequence attends to that sequence's cached prompt keys followed by
 // its fresh response keys, with no mask other than key validity.
 //
-// bf16 kernel: flash-style online softmax with MFMA.  A workgroup owns
+// bf16-model kernel: flash-style online softmax with MFMA.  Queries, keys and
+// values are fp16 (the bf16 path stores them so; see qkv_t in common.h), the
+// scores S = Q K^T are fp16 MFMAs with fp32 accumulation, and P V multiplies
+// the two-term fp16 probabilities (hi + lo) with two MFMAs, so that the
+// rounding of the probabilities does not limit the attention output.  The
+// output is the two-term bf16 activation of the O projection.  A workgroup owns
 // 16 * QB * NW query rows (256, 128 or 64) of one (sequence, query head) and
 // a contiguous range of 64-key tiles; with split-KV the splits' unnormalised
 // partial results are combined by attn_merge_kernel.  With 8 waves, two waves
@@ -33,14 +38,13 @@ typedef __attribute__((address_space(3))) void lds_void;
 // is raised (and the accumulators rescaled) when a tile's maximum exceeds it
 // by more than this.  Zero is the plain online softmax (probabilities <= 1).
 // A lazy threshold of 8 (probabilities below 2^8, most tiles skipping the
-// rescale) computes the same softmax and was 1-5 % faster, but measured
-// against the float64 reference it raised the largest logit error of a
-// two-layer LLaDA-8B-shaped model from 5.8e-3 to 9.5e-3 at P 512 and from
-// 1.26e-2 to 1.65e-2 at P 4096.  The reason: with threshold 0 the key that
-// sets the maximum gets probability 2^0 = 1, exact in bf16, so the dominant
-// term of a peaked softmax enters P V without rounding; with a lazy threshold
+// rescale) computes the same softmax and was 1-5 % faster, but, measured
+// when the probabilities entered P V as single bf16 values, it raised the
+// largest logit error of a two-layer LLaDA-8B-shaped model from 5.8e-3 to
+// 9.5e-3 at P 512: with threshold 0 the key that sets the maximum gets
+// probability 2^0 = 1, which needs no rounding, while with a lazy threshold
 // the dominant probabilities are arbitrary values in (1, 2^8) and carry the
-// full bf16 rounding.
+// full rounding.
 constexpr float ATT_RESCALE_LOG2 = 0.0f;
 
 // LDS layout of one 64-key stage.  K: row r (key) holds HD/8 16-byte chunks,
@@ -157,10 +161,10 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
   const int t0 = split * ntiles / nsplit, t1 = (split + 1) * ntiles / nsplit, nt = t1 - t0;
   const int kvh = h / (a.hq / a.hkv);
 
-  const bf16* Kc = (const bf16*)a.Kc + (size_t)kvh * a.ldcache * HD;
-  const bf16* Vtc = (const bf16*)a.Vtc + (size_t)kvh * HD * a.ldcache;
-  const bf16* Kf = (const bf16*)a.Kf + (size_t)kvh * a.ldfresh * HD;
-  const bf16* Vtf = (const bf16*)a.Vtf + (size_t)kvh * HD * a.ldfresh;
+  const f16* Kc = (const f16*)a.Kc + (size_t)kvh * a.ldcache * HD;
+  const f16* Vtc = (const f16*)a.Vtc + (size_t)kvh * HD * a.ldcache;
+  const f16* Kf = (const f16*)a.Kf + (size_t)kvh * a.ldfresh * HD;
+  const f16* Vtf = (const f16*)a.Vtf + (size_t)kvh * HD * a.ldfresh;
   const int coff = pl.cache_off[s], foff = b * G;
   const unsigned k_lds = att_lds_addr(Ks), v_lds = att_lds_addr(Vs);
 
@@ -173,8 +177,8 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
     const int kb0 = ct ? k0 : k0 - ppad;
     const int kvalid = ct ? P : G;
     const bool part = kb0 + KT > kvalid;
-    const bf16* Kbase = (ct ? Kc + (size_t)coff * HD : Kf + (size_t)foff * HD) + (size_t)kb0 * HD;
-    const bf16* Vbase = (ct ? Vtc + coff : Vtf + foff) + kb0;
+    const f16* Kbase = (ct ? Kc + (size_t)coff * HD : Kf + (size_t)foff * HD) + (size_t)kb0 * HD;
+    const f16* Vbase = (ct ? Vtc + coff : Vtf + foff) + kb0;
     const int vld = ct ? a.ldcache : a.ldfresh;
     const unsigned kofs = k_lds + (unsigned)(st * KSL * 16), vofs = v_lds + (unsigned)(st * VSL * 16);
 #pragma unroll
@@ -225,14 +229,14 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
   // s_getreg returns the 2-bit field SIMD_ID (bits 5:4 of HW_ID) already shifted down
   if (lane == 0) simd_of[w] = __builtin_amdgcn_s_getreg((1 << 11) | (4 << 6) | 4) & 3;
 
-  bf16x8 qf[QB][DS];
+  f16x8 qf[QB][DS];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     // rows past the sequence read its last row; their outputs are never stored
     const int qrow = min(rbeg + qt * QT + w * 16 * QB + qb * 16 + lc, rend - 1);
-    const bf16* Qp = (const bf16*)a.Q + ((size_t)h * a.ldq + qrow) * HD;
+    const f16* Qp = (const f16*)a.Q + ((size_t)h * a.ldq + qrow) * HD;
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) qf[qb][ds] = __builtin_bit_cast(bf16x8, *(const u32x4*)(Qp + ds * 32 + lg * 8));
+    for (int ds = 0; ds < DS; ++ds) qf[qb][ds] = __builtin_bit_cast(f16x8, *(const u32x4*)(Qp + ds * 32 + lg * 8));
   }
   // wait for the Q fragments and the first two stages together, so that no
   // wait the compiler places for Q inside the loop drains later stages
@@ -252,7 +256,11 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
     for (int i = 0; i < DB; ++i) o[qb][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   f32x4 sc[QB][4];
-  bf16x8 pb[2][QB];
+  // probabilities as the two-term pair hi = fp16(p), lo = fp16(p - hi): P V
+  // multiplies both (two MFMAs per fragment), so a probability enters with
+  // about 22 significant bits instead of 11 (at most 2^-24 absolute below
+  // fp16's normal range)
+  f16x8 pb[2][QB], plo[2][QB];
 
   // S^T = K Q^T of local tile i: sc[qb][kb][e] = raw score of key kb*16 + 4*lg + e, query lc of block qb
   auto scores = [&](int st) __attribute__((always_inline)) {
@@ -261,13 +269,13 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
 #pragma unroll
     for (int kp = 0; kp < 4; kp += 2) {
       // the fragments of two key blocks are requested before the first is used
-      bf16x8 kf[2][DS];
+      f16x8 kf[2][DS];
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
         const int r = att_key_row(kp + k2, lc);
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds)
-          kf[k2][ds] = __builtin_bit_cast(bf16x8, Kcur[r * KCPR + ((ds * 4 + lg) ^ att_kswz<KCPR>(r))]);
+          kf[k2][ds] = __builtin_bit_cast(f16x8, Kcur[r * KCPR + ((ds * 4 + lg) ^ att_kswz<KCPR>(r))]);
       }
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2)
@@ -275,13 +283,13 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
         for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb)
-            sc[qb][kp + k2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[k2][ds], qf[qb][ds],
+            sc[qb][kp + k2] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[k2][ds], qf[qb][ds],
                                                                       ds == 0 ? zero : sc[qb][kp + k2], 0, 0, 0);
     }
     att_mfma_pipeline<4 * DS, QB>();
   };
   // online softmax of local tile i (running maxima in log2 units); leaves the
-  // bf16 probabilities in pb as the B operand of O^T = V^T P^T
+  // two-term fp16 probabilities in pb / plo as the B operands of O^T = V^T P^T
   auto softmax = [&](int i) __attribute__((always_inline)) {
     const int k0 = (t0 + i) * KT;
     const bool ct = k0 < ppad;
@@ -349,30 +357,35 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pb[ks][qb][e] = (bf16)sc[qb][2 * ks][e];
-          pb[ks][qb][4 + e] = (bf16)sc[qb][2 * ks + 1][e];
+          const f16 h0 = (f16)sc[qb][2 * ks][e], h1 = (f16)sc[qb][2 * ks + 1][e];
+          pb[ks][qb][e] = h0;
+          pb[ks][qb][4 + e] = h1;
+          plo[ks][qb][e] = (f16)(sc[qb][2 * ks][e] - (float)h0);
+          plo[ks][qb][4 + e] = (f16)(sc[qb][2 * ks + 1][e] - (float)h1);
         }
   };
-  // O^T += V^T P^T for local tile i (probabilities in pb)
+  // O^T += V^T P^T for local tile i (probabilities in pb + plo)
   auto pv_update = [&](int st) __attribute__((always_inline)) {
     const u32x4* Vcur = Vs + st * VSL;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       // keys 32 ks + 8 lg .. + 7 of row d: logical chunk 4 ks + lg.  The
       // eight fragments of a k-step are requested before the first is used.
-      bf16x8 vf[DB];
+      f16x8 vf[DB];
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const int d = db * 16 + lc;
-        vf[db] = __builtin_bit_cast(bf16x8, Vcur[d * 8 + ((4 * ks + lg) ^ att_vswz(d))]);
+        vf[db] = __builtin_bit_cast(f16x8, Vcur[d * 8 + ((4 * ks + lg) ^ att_vswz(d))]);
       }
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db], pb[ks][qb], o[qb][db], 0, 0, 0);
+        for (int qb = 0; qb < QB; ++qb) {
+          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[db], pb[ks][qb], o[qb][db], 0, 0, 0);
+          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[db], plo[ks][qb], o[qb][db], 0, 0, 0);
+        }
     }
-    att_mfma_pipeline<2 * DB, QB>();
+    att_mfma_pipeline<2 * DB, 2 * QB>();
   };
 
   // Ping-pong schedule.  A wave's tile i is an MFMA half M(i) = [PV(i - 1);

@@ -7,6 +7,9 @@
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 #define ARCHER_MAXB 64
@@ -46,10 +49,21 @@ __device__ __forceinline__ int plan_find(const int* off, int n, int v) {
 
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+__device__ __forceinline__ float to_f32(f16 x) { return (float)x; }
 
 template <class T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+template <> __device__ __forceinline__ f16 from_f32<f16>(float x) { return (f16)x; }
+
+// Element type of the stored queries, keys and values -- and so of the prompt
+// cache -- for activation type T: fp16 on the bf16 path (three more significant
+// bits than bf16 in the same two bytes; a single rounding of each of them
+// feeds every later layer, so its precision sets the error growth with
+// depth), fp32 on the fp32 path.
+template <class T> struct QkvOf { using type = T; };
+template <> struct QkvOf<bf16> { using type = f16; };
+template <class T> using qkv_t = typename QkvOf<T>::type;
 
 // Two-term bf16 representation of an fp32 activation: v ~= hi + lo with
 // hi = bf16(v) and lo = bf16(v - hi), about 16 significant bits.  The bf16

@@ -360,7 +360,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.Kf = c->at<char>(L.Kf); a.Vtf = c->at<char>(L.Vtf); a.ldfresh = L.ldfresh;
       a.hq = hq; a.hkv = hkv; a.hd = hd;
       a.row_pos = row_pos; a.row_dst = row_dst; a.rope = c->at<float2>(L.rope);
-      if ((st = gemm(c, ARCHER_K_GEMM_QKV, EPI_QKV, a))) return st;
+      if ((st = gemm(c, full ? ARCHER_K_GEMM_QKV_FULL : ARCHER_K_GEMM_QKV, EPI_QKV, a))) return st;
     }
     {
       AttnArgs a;
@@ -391,7 +391,7 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.A2 = o2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.X = x; a.ldx = d;
       fuse_norm(a, c->mlp_norm[l], act2_mlp);
-      if ((st = gemm(c, ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
+      if ((st = gemm(c, full ? ARCHER_K_GEMM_O_FULL : ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
       normed = gemm_fuses_norm(a);
     }
     if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2_mlp, L.Mmax))) return st;
@@ -401,14 +401,14 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.A2 = act2_mlp; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.W2 = c->w_up[l];
       a.H = c->at<char>(L.H); a.H2 = h2; a.ldh = tiled ? L.Mmax : F; a.h_tiled = tiled;
-      if ((st = gemm(c, ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
+      if ((st = gemm(c, full ? ARCHER_K_GEMM_GATEUP_FULL : ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
     }
     {
       GemmArgs a = gargs(c->at<char>(L.H), tiled ? L.Mmax : F, c->w_down[l], c->w_tiled ? d : F, rows, d, F);
       a.A2 = h2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.X = x; a.ldx = d;
       if (l + 1 < m.n_layers) fuse_norm(a, c->attn_norm[l + 1], act2_qkv);
-      if ((st = gemm(c, ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
+      if ((st = gemm(c, full ? ARCHER_K_GEMM_DOWN_FULL : ARCHER_K_GEMM_DOWN, EPI_RESID, a))) return st;
       normed = gemm_fuses_norm(a);
     }
   }
@@ -900,7 +900,7 @@ archer_status archer_read_state(archer_ctx* c, int32_t what, int32_t layer, int3
     void* kd = what == ARCHER_READ_PROMPT_K ? dst : nullptr;
     void* vd = what == ARCHER_READ_PROMPT_V ? dst : nullptr;
     if (is_bf16(c))
-      launch_read_cache<bf16>(K, Vt, L.ldcache, c->cache_off[seq], P, m.n_kv_heads, m.head_dim, kd, vd, c->stream);
+      launch_read_cache<f16>(K, Vt, L.ldcache, c->cache_off[seq], P, m.n_kv_heads, m.head_dim, kd, vd, c->stream);
     else
       launch_read_cache<float>(K, Vt, L.ldcache, c->cache_off[seq], P, m.n_kv_heads, m.head_dim, kd, vd, c->stream);
     HIPCHK(hipGetLastError());

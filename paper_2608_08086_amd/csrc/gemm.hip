@@ -308,6 +308,7 @@ __global__ __launch_bounds__(NORM_THREADS) void gemm_reduce_resid_norm_kernel(Ge
 template <class T, int HD>
 __global__ __launch_bounds__(256) void gemm_reduce_qkv_kernel(GemmArgs a, int nvb) {
   static_assert(sizeof(T) == 2, "bf16 activations");
+  using Q = qkv_t<T>;   // stored q, k, v
   const size_t plane = (size_t)a.M * a.N;
   if ((int)blockIdx.x >= nvb) {
     // four consecutive pairs (j .. j + 3) of one head per thread
@@ -327,24 +328,24 @@ __global__ __launch_bounds__(256) void gemm_reduce_qkv_kernel(GemmArgs a, int nv
     // RoPE of the four pairs with epi_qkv's expressions, one 8-byte store per half
     const int dst = a.row_dst[row];
     const float2* cs = a.rope + (size_t)a.row_pos[row] * (HD / 2) + j;
-    T* p;
-    if (head < a.hq) p = (T*)a.Qb + ((size_t)head * a.ldq + row) * HD;
-    else if (dst_is_fresh(dst)) p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * HD;
-    else p = (T*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * HD;
-    bf16x4 o1, o2;
+    Q* p;
+    if (head < a.hq) p = (Q*)a.Qb + ((size_t)head * a.ldq + row) * HD;
+    else if (dst_is_fresh(dst)) p = (Q*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * HD;
+    else p = (Q*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * HD;
+    f16x4 o1, o2;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const float2 o = rope_rotate(v1[e], v2[e], cs[e]);
-      o1[e] = from_f32<T>(o.x);
-      o2[e] = from_f32<T>(o.y);
+      o1[e] = from_f32<Q>(o.x);
+      o2[e] = from_f32<Q>(o.y);
     }
-    *(bf16x4*)(p + j) = o1;
-    *(bf16x4*)(p + j + HD / 2) = o2;
+    *(f16x4*)(p + j) = o1;
+    *(f16x4*)(p + j + HD / 2) = o2;
     return;
   }
   constexpr int RT = 32, TPR = HD / 4, RG = 256 / TPR, RPT = RT / RG;
   static_assert(RPT >= 1 && RT % RG == 0, "row tiling");
-  __shared__ T tile[HD][RT + 2];
+  __shared__ Q tile[HD][RT + 2];
   const int mb = (a.M + RT - 1) / RT;
   const int vh = blockIdx.x / mb, r0 = (blockIdx.x % mb) * RT;
   const int d4 = (threadIdx.x % TPR) * 4, rg = threadIdx.x / TPR;
@@ -369,16 +370,16 @@ __global__ __launch_bounds__(256) void gemm_reduce_qkv_kernel(GemmArgs a, int nv
 #pragma unroll
   for (int k = 0; k < RPT; ++k)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) tile[d4 + e][rg + k * RG] = from_f32<T>(v[k][e]);
+    for (int e = 0; e < 4; ++e) tile[d4 + e][rg + k * RG] = from_f32<Q>(v[k][e]);
   __syncthreads();
   for (int i = threadIdx.x; i < RT * HD; i += blockDim.x) {
     const int dd = i / RT, rr = i % RT, row = r0 + rr;
     if (row < a.M) {
       const int dst = a.row_dst[row];
-      T* vt;
+      Q* vt;
       int ld, col;
-      if (dst_is_fresh(dst)) { vt = (T*)a.Vtf; ld = a.ldfresh; col = dst; }
-      else { vt = (T*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
+      if (dst_is_fresh(dst)) { vt = (Q*)a.Vtf; ld = a.ldfresh; col = dst; }
+      else { vt = (Q*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
       vt[((size_t)vh * HD + dd) * ld + col] = tile[dd][rr];
     }
   }

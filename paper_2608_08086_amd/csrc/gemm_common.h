@@ -64,27 +64,29 @@ __device__ __forceinline__ float2 rope_rotate(float v1, float v2, float2 cs) {
 }
 
 // head in [0, hq + 2 hkv): q heads, k heads, v heads; v1 / v2 = dims j, j + hd/2
+// (q, k and v are stored as qkv_t<T>)
 template <class T>
 __device__ __forceinline__ void epi_qkv(const GemmArgs& a, int row, int head, int j, float v1, float v2) {
+  using Q = qkv_t<T>;
   const int hd = a.hd;
   const int dst = a.row_dst[row];
   if (head < a.hq + a.hkv) {
     const float2 o = rope_rotate(v1, v2, a.rope[(size_t)a.row_pos[row] * (hd / 2) + j]);
     const float o1 = o.x, o2 = o.y;
-    T* p;
-    if (head < a.hq) p = (T*)a.Qb + ((size_t)head * a.ldq + row) * hd;
-    else if (dst_is_fresh(dst)) p = (T*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * hd;
-    else p = (T*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * hd;
-    p[j] = from_f32<T>(o1);
-    p[j + hd / 2] = from_f32<T>(o2);
+    Q* p;
+    if (head < a.hq) p = (Q*)a.Qb + ((size_t)head * a.ldq + row) * hd;
+    else if (dst_is_fresh(dst)) p = (Q*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * hd;
+    else p = (Q*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * hd;
+    p[j] = from_f32<Q>(o1);
+    p[j + hd / 2] = from_f32<Q>(o2);
   } else {
     const int vh = head - a.hq - a.hkv;
-    T* vt;
+    Q* vt;
     int ld, col;
-    if (dst_is_fresh(dst)) { vt = (T*)a.Vtf; ld = a.ldfresh; col = dst; }
-    else { vt = (T*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
-    vt[((size_t)vh * hd + j) * ld + col] = from_f32<T>(v1);
-    vt[((size_t)vh * hd + j + hd / 2) * ld + col] = from_f32<T>(v2);
+    if (dst_is_fresh(dst)) { vt = (Q*)a.Vtf; ld = a.ldfresh; col = dst; }
+    else { vt = (Q*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
+    vt[((size_t)vh * hd + j) * ld + col] = from_f32<Q>(v1);
+    vt[((size_t)vh * hd + j + hd / 2) * ld + col] = from_f32<Q>(v2);
   }
 }
 

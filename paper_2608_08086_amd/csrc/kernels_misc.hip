@@ -406,7 +406,7 @@ void launch_read_cache(const void* K, const void* Vt, int ld, int off, int P, in
   read_cache_kernel<T><<<blocks, 256, 0, st>>>((const T*)K, (const T*)Vt, ld, off, P, hkv, hd, (T*)Kd, (T*)Vd);
 }
 template void launch_read_cache<float>(const void*, const void*, int, int, int, int, int, void*, void*, hipStream_t);
-template void launch_read_cache<bf16>(const void*, const void*, int, int, int, int, int, void*, void*, hipStream_t);
+template void launch_read_cache<f16>(const void*, const void*, int, int, int, int, int, void*, void*, hipStream_t);
 
 // Activation rows (hi and optional lo term, layout act_at(row, k, ld, tiled))
 // -> fp32 row-major [n][d] holding hi + lo.  The sum is exact in fp32: lo is

@@ -8,22 +8,21 @@ to the fresh logits, and the two actions and next states are compared.
 Disagreement is then binned by the anchor distance D_t and related to D_t
 and the cache age A_t by partial Spearman correlations.
 
-The main trajectory is driven here through the library's calls
-(archer_refresh_prompt / archer_step / archer_decide, with the controller of
-Algorithm 1 as archer_decode applies it, per sequence), so it is the same
-trajectory archer_decode produces; the shadow forwards run on a second
-context over the same weights, whose prompt cache is the scratch cache, and
-change nothing on the main trajectory.  All model and decoder arithmetic runs
-in the library's kernels; this module only orders the calls and computes the
-statistics of the recorded integers.
+The main trajectory is archer_decode's own: the probe runs it as a decode
+session (archer_session_begin / archer_session_advance, one decision at a
+time), so the refresh decisions come from the library's controller.  Before
+each decision that follows a cached forward, it reads that forward's logits
+and the current state, runs a FullForward of the same state on a second
+context over the same weights (whose prompt cache is the scratch cache) and
+applies the decoder to both sets of logits there; nothing on the main
+context changes.  All model and decoder arithmetic runs in the library's
+kernels; this module only orders the calls and computes the statistics of
+the recorded integers.
 """
 
 from __future__ import annotations
 
 import numpy as np
-import torch
-
-from . import archer
 
 # D_t bins of the paper's calibration table, plus everything above
 D_BINS = ((0, 3), (4, 7), (8, 11), (12, 14), (15, None))
@@ -44,57 +43,34 @@ def shadow_probe(ctx, shadow, prompt, prompt_len, g0, *, policy, K, steps, k=1, 
     """
     B, G = g0.shape
     T = int(steps)
-    g = g0.clone()
-    logits = ctx.new_logits(B)
-    ctx.refresh_prompt(prompt, prompt_len, g, logits=logits)
-    r = np.zeros(B, dtype=np.int64)
-    refreshed = np.zeros((T, B), dtype=np.int32)
-    dist = np.zeros((T, B), dtype=np.int32)
-    age = np.zeros((T, B), dtype=np.int32)
-    refreshed[0, :] = 1
+    tr = ctx.session_begin(prompt, prompt_len, g0, policy=policy, K=K, steps=T, k=k, tau=tau,
+                           max_remask=max_remask, trace=True)
     probes = []
-    pending = None    # (forward index, sequences probed, fresh next state) for the coming decision
     n_cached = 0
     for t in range(T):
-        final = t == T - 1
-        g_next, d_anchor, _, _ = ctx.decide(logits, g, k=k, tau=tau, max_remask=max_remask, final=final)
-        if pending is not None:
-            s, seqs, g_fresh, Ds, As = pending
-            a = g_next.cpu().numpy()
-            f = g_fresh.cpu().numpy()
-            for b, D, A in zip(seqs, Ds, As):
-                diff = int(np.sum(a[b] != f[b]))
-                probes.append(dict(b=int(b), t=int(s), D=int(D), A=int(A), disagree=int(diff > 0), dH=diff))
-            pending = None
-        if final:
-            g = g_next
-            break
-        s = t + 1
-        D = d_anchor.cpu().numpy().astype(np.int64)
-        A = s - r
-        dist[s] = D
-        age[s] = A
-        if policy == archer.ALWAYS:
-            ref = np.ones(B, dtype=bool)
-        elif policy == archer.AGE:
-            ref = A >= K
-        else:
-            ref = D >= K
-        r[ref] = s
-        refreshed[s] = ref.astype(np.int32)
-        if ref.any():
-            ctx.refresh_prompt(prompt, prompt_len, g_next, seq_sel=ref.tolist(), logits=logits)
-        if (~ref).any():
-            ctx.step(g_next, seq_sel=(~ref).tolist(), logits=logits)
-            if n_cached % every == 0:
-                seqs = np.nonzero(~ref)[0]
-                z_fresh = shadow.refresh_prompt(prompt, prompt_len, g_next)
-                g_fresh, _, _, _ = shadow.decide(z_fresh, g_next, k=k, tau=tau, max_remask=max_remask,
-                                                 final=s == T - 1)
-                pending = (s, seqs, g_fresh, D[seqs], A[seqs])
-            n_cached += 1
-        g = g_next
-    return g, dict(refreshed=refreshed, dist=dist, age=age), probes
+        # forward t has run; decision t (on its logits z_t and the state g_t) comes next
+        if t > 0:
+            cached = np.nonzero(tr["refreshed"][t].cpu().numpy() == 0)[0]
+            if len(cached):
+                if n_cached % every == 0:
+                    g_t = ctx.session_response()
+                    z_c = ctx.read_logits(B)
+                    z_f = shadow.refresh_prompt(prompt, prompt_len, g_t)
+                    final = t == T - 1
+                    a_c = shadow.decide(z_c, g_t, k=k, tau=tau, max_remask=max_remask, final=final)[0]
+                    a_f = shadow.decide(z_f, g_t, k=k, tau=tau, max_remask=max_remask, final=final)[0]
+                    a_c, a_f = a_c.cpu().numpy(), a_f.cpu().numpy()
+                    D = tr["dist"][t].cpu().numpy()
+                    A = tr["age"][t].cpu().numpy()
+                    for b in cached:
+                        diff = int(np.sum(a_c[b] != a_f[b]))
+                        probes.append(dict(b=int(b), t=int(t), D=int(D[b]), A=int(A[b]), disagree=int(diff > 0),
+                                           dH=diff))
+                n_cached += 1
+        ctx.session_advance(1)
+    g = ctx.session_response()
+    trace = {name: tr[name].cpu().numpy() for name in ("refreshed", "dist", "age")}
+    return g, trace, probes
 
 
 def _ranks(x):

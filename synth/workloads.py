@@ -3,7 +3,7 @@
 The paper evaluates LLaDA-8B-Instruct, Dream-v0-Instruct-7B and
 DiffuCoder-7B with batch 1 and a 256-token response block (Sec. 6 and
 App. G.4, implementation details); its prompt-length study sweeps prompts of
-128..2048 tokens at a 256-token response (App. F, table of per-update cost).
+128..2048 tokens at a 256-token response (App. E, table of per-update cost).
 No trained weights or benchmark prompts are used here: every workload is a
 random-init model of the named architecture fed seeded uniform-random prompt
 tokens, which stand in for the paper's code / math prompts.
@@ -33,6 +33,10 @@ class ModelShape:
     rms_eps: float = 1e-5
     rope_theta: float = 10000.0
     init_std: float = 0.02
+    # bf16 models: projections whose activation operand is a single bf16 value
+    # (names from "qkv", "o", "gateup", "down", "head"); the others take the
+    # two-term (about 16-bit) activation
+    single_term: tuple = ()
 
     @property
     def mask_id(self) -> int:

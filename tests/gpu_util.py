@@ -41,6 +41,12 @@ def rand_bf16(shape, seed, stream, scale=1.0):
     return dev_bits(bits), bf16_bits_to_f32(bits).astype(np.float64)
 
 
+def rand_f16(shape, seed, stream, scale=1.0):
+    """(device tensor, float64 values) of an N(0, scale^2) tensor rounded to fp16."""
+    v = normal_tensor(shape, seed, stream, scale, "fp32").astype(np.float16)
+    return torch.from_numpy(np.ascontiguousarray(v)).cuda(), v.astype(np.float64)
+
+
 def rand_f32(shape, seed, stream, scale=1.0):
     v = normal_tensor(shape, seed, stream, scale, "fp32")
     return dev_f32(v), v.astype(np.float64)

@@ -6,7 +6,8 @@
 * archer_decode of the tiny fp32 workload under the age, Hamming and always
   rules: the free-run trajectory (schedule, D_t, A_t, unmasked positions and
   tokens, remasked positions, final response) equals the oracle's until a
-  margin-exempt step (expected: none);
+  margin-exempt step (there is none: every decision is asserted bit-exact),
+  with the rollback decoder and the no-rollback one (max_remask 0);
 * a teacher-forced bf16 decode: at every step the GPU receives the oracle's
   state; logits agree within 2e-2 and decisions are bit-exact wherever the
   decision margin exceeds the logit error (the condition of Prop. app-decision).
@@ -109,11 +110,14 @@ def _gpu_traj(tr, b, k):
     return out
 
 
-@pytest.mark.parametrize("policy,K", [("age", 4), ("hamming", 4), ("hamming", 1), ("always", 0)])
-def test_tiny_decode_matches_oracle(policy, K):
+@pytest.mark.parametrize("policy,K,max_remask", [("age", 4, 1), ("hamming", 4, 1), ("hamming", 1, 1),
+                                                ("always", 0, 1), ("age", 4, 0), ("hamming", 3, 0)])
+def test_tiny_decode_matches_oracle(policy, K, max_remask):
+    """Free run of the fp32 workload: every step's record and the final response equal the
+    oracle's, with no margin-exempt step (max_remask 0 is the no-rollback decoder)."""
     w = get_workload("tiny")
     m, dec = w.model, w.decode
-    say(f"tiny fp32 decode policy={policy} K={K}")
+    say(f"tiny fp32 decode policy={policy} K={K} max_remask={max_remask}")
     a = archer()
     W = model_weights(m, seed=w.weight_seed)
     p = prompts(w)[0]
@@ -121,23 +125,29 @@ def test_tiny_decode_matches_oracle(policy, K):
     ctx = make_ctx(m, W, 1, len(p), len(p), G)
     pol = {"age": a.AGE, "hamming": a.HAMMING, "always": a.ALWAYS}[policy]
     resp = dev_i32(np.full((1, G), m.mask_id))
-    out, tr = ctx.decode(dev_i32(p), [len(p)], resp, policy=pol, K=K, steps=T, k=k, tau=dec.remask_threshold)
+    out, tr = ctx.decode(dev_i32(p), [len(p)], resp, policy=pol, K=K, steps=T, k=k, tau=dec.remask_threshold,
+                         max_remask=max_remask)
     g_o, tr_o = odec.decode(W, m, p, np.full(G, m.mask_id), steps=T, k=k, tau=dec.remask_threshold,
                             policy={"age": oc.AGE, "hamming": oc.HAMMING, "always": oc.ALWAYS}[policy], K=K,
-                            keep_logits=True)
+                            remask=max_remask == 1, keep_logits=True)
     gt = _gpu_traj(tr, 0, k)
+    remasks = 0
     for t in range(T):
         g_next = tr_o.states[t + 1] if t + 1 < T else g_o
         U = list(tr_o.unmask[t])[:k]            # the trace lists at most k positions per step
         want = dict(ref=int(tr_o.refreshed[t]), dist=int(tr_o.dist[t]), age=int(tr_o.age[t]),
                     U=U, tok=[int(g_next[i]) for i in U], Rm=list(tr_o.remask[t]))
-        if gt[t] != want:
-            mD = od.decision_margin(tr_o.logits[t], tr_o.states[t], m.mask_id, k, dec.remask_threshold,
-                                    final=t == T - 1)
-            assert mD <= 1e-4, f"step {t}: gpu {gt[t]} oracle {want} margin {mD}"
-            say(f"  margin-exempt divergence at step {t} (m_D={mD:.2e})")
-            return
+        mD = od.decision_margin(tr_o.logits[t], tr_o.states[t], m.mask_id, k, dec.remask_threshold,
+                                final=t == T - 1, remask=max_remask == 1)
+        # the fp32 workload has no margin-exempt step: every decision is bit-exact
+        assert gt[t] == want, f"step {t}: gpu {gt[t]} oracle {want} margin {mD:.2e}"
+        remasks += len(want["Rm"])
+    if max_remask == 0:
+        assert remasks == 0
+    else:
+        assert remasks > 0        # the rollback branch is exercised
     assert out.cpu().numpy()[0].tolist() == g_o.tolist()
+    assert m.mask_id not in g_o.tolist()
 
 
 def test_teacher_forced_bf16_decode():

@@ -9,7 +9,7 @@ the oracle computes one by one.
 import numpy as np
 import pytest
 
-from gpu_util import archer, host, rand_bf16, rand_f32, say
+from gpu_util import archer, host, rand_bf16, rand_f16, rand_f32, say
 from oracle import numerics as on
 
 pytestmark = pytest.mark.gpu
@@ -106,7 +106,8 @@ def test_gemm_full_size_sampled(N, K):
 
 def _attn_case(dtype, Mq, Hq, Hkv, hd, nk1, nk2, seed, rows=None, heads=None, q_scale=1.0):
     a = archer()
-    rand = rand_bf16 if dtype == a.BF16 else rand_f32
+    # the bf16 model path stores queries, keys and values as fp16
+    rand = rand_f16 if dtype == a.BF16 else rand_f32
     ld1 = (nk1 + 63) // 64 * 64
     ld2 = (nk2 + 63) // 64 * 64
     Q, Q64 = rand((Hq, Mq, hd), seed, 1, q_scale)
@@ -136,8 +137,11 @@ def _attn_case(dtype, Mq, Hq, Hkv, hd, nk1, nk2, seed, rows=None, heads=None, q_
 def test_attention_bf16_matches_oracle(Mq, Hq, Hkv, hd, nk1, nk2):
     say(f"attention bf16 Mq={Mq} Hq={Hq} Hkv={Hkv} hd={hd} nk1={nk1} nk2={nk2}")
     a = archer()
-    # bf16 probabilities in the P.V product and a bf16 output: |err| <~ 2^-8 max|v|
-    assert _attn_case(a.BF16, Mq, Hq, Hkv, hd, nk1, nk2, 11) < 2e-2
+    # fp16 inputs and two-term probabilities in P V; the op returns the output's bf16 hi term
+    # only (the model path also keeps the lo term), so |err| <~ 2^-9 max|o|
+    err = _attn_case(a.BF16, Mq, Hq, Hkv, hd, nk1, nk2, 11)
+    say(f"  max abs err {err:.3e}")
+    assert err < 2e-2
 
 
 @pytest.mark.parametrize("Mq,Hq,Hkv,nk1,nk2", [(256, 4, 4, 512, 256), (256, 4, 4, 4096, 256)])
@@ -169,4 +173,6 @@ def test_attention_full_size_sampled(Mq, Hq, Hkv, nk1, nk2):
     rng = np.random.default_rng(1)
     rows = np.sort(rng.choice(Mq, 24, replace=False))
     heads = sorted(rng.choice(Hq, 4, replace=False).tolist())
-    assert _attn_case(a.BF16, Mq, Hq, Hkv, 128, nk1, nk2, 13, rows=rows, heads=heads) < 2e-2
+    err = _attn_case(a.BF16, Mq, Hq, Hkv, 128, nk1, nk2, 13, rows=rows, heads=heads)
+    say(f"  max abs err {err:.3e}")
+    assert err < 2e-2

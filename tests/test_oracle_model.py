@@ -1,7 +1,8 @@
 """Pins of the oracle model Phi_theta (no GPU).
 
 * a scalar-loop float64 transformer written independently here (pure Python,
-  its own bf16 rounding via frexp) must match ``oracle.model.transformer``;
+  its own fp16 and bf16 rounding via frexp) must match
+  ``oracle.model.transformer``, with and without single-term operands;
 * permutation consistency of bidirectional attention, by brute force over all
   orders of tiny inputs;
 * CachedForward(g; C_p(g)) equals FullForward(p, g) (D_t = 0 case of
@@ -29,12 +30,30 @@ def _bf16(x):
     return round(mant * 256.0) / 256.0 * 2.0 ** e   # round() ties to even on floats
 
 
+def _fp16(x):
+    """IEEE half rounding written from its definition: 11 significant bits,
+    spacing 2^-24 below 2^-14, ties to even (Python's round on floats)."""
+    if x == 0.0 or not math.isfinite(x):
+        return x
+    if abs(x) < 2.0 ** -14:
+        return round(x * 2.0 ** 24) / 2.0 ** 24
+    mant, e = math.frexp(x)
+    r = round(mant * 2048.0) / 2048.0 * 2.0 ** e
+    return r if abs(r) <= 65504.0 else math.copysign(math.inf, x)
+
+
 def _w(a):
     return on.weights_f64(a).tolist()
 
 
 def _loop_model(W, m, tokens, positions, out_rows):
-    rnd = _bf16 if m.dtype == "bf16" else (lambda t: t)
+    ident = lambda t: t   # noqa: E731
+    rnd = _fp16 if m.dtype == "bf16" else ident
+
+    def op(name, row):
+        """Activation operand of a projection: single bf16 where the model says so."""
+        single = m.dtype == "bf16" and name in m.single_term
+        return [_bf16(t) for t in row] if single else row
     d, hq, hkv, hd, F = m.d_model, m.n_heads, m.n_kv_heads, m.head_dim, m.d_ff
     n = len(tokens)
     emb = _w(W["tok_emb"])
@@ -61,7 +80,7 @@ def _loop_model(W, m, tokens, positions, out_rows):
         wqkv, wo, wg, wu, wd = (_w(L[k]) for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down"))
         Q, K, V = [], [], []
         for i in range(n):
-            a = norm(x[i], L["attn_norm"])
+            a = op("qkv", norm(x[i], L["attn_norm"]))
             y = matvec(wqkv, a)
             Q.append([[rnd(t) for t in rot(y[h * hd:(h + 1) * hd], positions[i])] for h in range(hq)])
             K.append([[rnd(t) for t in rot(y[(hq + h) * hd:(hq + h + 1) * hd], positions[i])] for h in range(hkv)])
@@ -76,25 +95,27 @@ def _loop_model(W, m, tokens, positions, out_rows):
                 p = [math.exp(t - mx) for t in s]
                 tot = sum(p)
                 o += [sum(p[j] / tot * V[j][kh][c] for j in range(n)) for c in range(hd)]
-            proj = matvec(wo, o)
+            proj = matvec(wo, op("o", o))
             xi = [x[i][c] + proj[c] for c in range(d)]
-            b = norm(xi, L["mlp_norm"])
+            b = op("gateup", norm(xi, L["mlp_norm"]))
             gate, up = matvec(wg, b), matvec(wu, b)
             hmid = [gate[f] / (1.0 + math.exp(-gate[f])) * up[f] for f in range(F)]
-            down = matvec(wd, hmid)
+            down = matvec(wd, op("down", hmid))
             newx.append([xi[c] + down[c] for c in range(d)])
         x = newx
     head = _w(W["lm_head"])
     z = []
     for i in out_rows:
-        c = norm(x[i], W["final_norm"])
+        c = op("head", norm(x[i], W["final_norm"]))
         z.append(matvec(head, c))
     return np.array(z)
 
 
-@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_transformer_matches_scalar_loops(dtype):
-    m = tiny_shape(dtype)
+@pytest.mark.parametrize("dtype,single", [("fp32", ()), ("bf16", ()),
+                                          ("bf16", ("qkv", "o", "gateup", "down", "head")),
+                                          ("bf16", ("o", "head"))])
+def test_transformer_matches_scalar_loops(dtype, single):
+    m = tiny_shape(dtype, single_term=single)
     W = random_weights(m, seed=3)
     tokens = np.array([1, 4, 9, 2, 9, 0])
     positions = np.arange(6)

@@ -33,6 +33,32 @@ def test_round_bf16_ties_and_direct_rounding():
         assert on.round_bf16(np.array([x]))[0] == want, x
 
 
+# --- fp16 rounding (queries, keys and values of bf16 models) ------------------
+
+def _fp16_values():
+    """Every finite non-negative fp16 value, ascending, built from its bit fields."""
+    sub = np.arange(1024) * 2.0 ** -24                                   # exponent field 0
+    norm = [(1 + np.arange(1024) / 1024) * 2.0 ** (e - 15) for e in range(1, 31)]
+    return np.concatenate([sub] + norm)
+
+
+def test_round_fp16_exact_values_midpoints_and_overflow():
+    h = _fp16_values()
+    assert len(h) == 31744 and h[-1] == 65504.0
+    np.testing.assert_array_equal(on.round_fp16(h), h)
+    np.testing.assert_array_equal(on.round_fp16(-h), -h)
+    mid = (h[:-1] + h[1:]) / 2                          # exact in float64
+    even = np.where(np.arange(len(h) - 1) % 2 == 0, h[:-1], h[1:])   # the neighbour with an even significand
+    np.testing.assert_array_equal(on.round_fp16(mid), even)
+    up = np.nextafter(mid, np.inf)
+    down = np.nextafter(mid, -np.inf)
+    np.testing.assert_array_equal(on.round_fp16(up), h[1:])
+    np.testing.assert_array_equal(on.round_fp16(down), h[:-1])
+    # beyond the largest finite value: ties to even at 65520 (the next, unrepresentable, step) go to inf
+    assert on.round_fp16(np.array([65519.99]))[0] == 65504.0
+    assert on.round_fp16(np.array([65520.0]))[0] == np.inf
+
+
 # --- bf16 bit patterns -> float64 (every bf16 weight the oracle reads) -------
 
 def test_weights_f64_matches_torch_bf16_view_on_every_bit_pattern():
