@@ -8,8 +8,10 @@ Every comparison is against the float64 oracle on host weights from synth.gen:
   C_p (Eq. app-cached) of the first, a middle and the last layer; the same at
   depth 2 and 8 (contexts over the first layers of the same weights), which
   gives the error-versus-depth curve;
-* Dream-7B shape (GQA 28 / 4 heads, F 18944, V 152064), two layers at full
-  width, batch 2, P 1024, G 512: both passes, hidden state and C_p;
+* the long-prompt workload at its real depth: P 4096, 32 layers;
+* Dream-7B shape (GQA 28 / 4 heads, F 18944, V 152064): all 28 layers at
+  batch 1, and two layers at batch 2, P 1024, G 512: both passes, hidden
+  state and C_p;
 * the ragged batch of the batched workload (16 sequences, the workload's
   seeded prompt lengths in [256, 2048]), two layers at full width, in the
   bench's launch configuration for that batch (one split per pass, folded
@@ -182,8 +184,79 @@ def test_llada_depth_curve_2_and_8(llada32):
         ctx.close()
 
 
+def test_llada_depth_32_long_prompt(llada32):
+    """The long-prompt workload at its real depth: P 4096, G 256, 32 layers -- the 4352-row
+    refresh pass (one split, folded split-K) and the cached pass (split-KV over 4352 keys)."""
+    a = archer()
+    st = llada32
+    w = get_workload("llada_p4096")
+    m, G = st["m"], st["G"]
+    P = w.decode.prompt_len
+    p = prompts(w)[0]
+    ctx = _ctx(m, st["Wd"], 1, P, P, G)
+    g0 = np.full(G, m.mask_id)
+    g0[:64] = (np.arange(64) * 37) % (m.vocab - 1)
+    g1 = g0.copy()
+    g1[128:192] = (np.arange(64) * 13 + 3) % (m.vocab - 1)
+    say("depth 32, P 4096: GPU FullForward and CachedForward")
+    z = host(ctx.refresh_prompt(dev_i32(p), [P], dev_i32(g0[None])))[0]
+    kv = ctx.read_prompt_kv(31, 0, P)
+    zc = host(ctx.step(dev_i32(g1[None])))[0]
+    hid = host(ctx.read_rows(a.READ_HIDDEN, 1))
+    res = host(ctx.read_rows(a.READ_RESIDUAL, 1))
+    ctx.close()
+    t0 = time.time()
+    z_ref, cache, _ = om.full_forward(st["W"], m, p, g0)
+    say(f"  oracle FullForward over 4352 rows: {time.time() - t0:.1f} s")
+    _err("P 4096 depth 32 full logits", z, z_ref)
+    _cmp_cache("P 4096 depth 32 C_p layer 31 K", kv[0], cache[31][0])
+    _cmp_cache("P 4096 depth 32 C_p layer 31 V", kv[1], cache[31][1])
+    zc_ref, (stack, hid_ref) = om.cached_forward(st["W"], m, g1, cache, P, keep_hidden=True)
+    _err("P 4096 depth 32 cached logits", zc, zc_ref)
+    _err("P 4096 depth 32 cached normalised hidden", hid, hid_ref)
+    _resid("P 4096 depth 32 cached residual", res, stack[-1])
+
+
 # ----------------------------------------------------------------------------------------------
-# Dream-7B shape (GQA), two layers at full width
+# Dream-7B shape (GQA): all 28 layers at batch 1, two layers at batch 2
+
+
+def test_dream_all_28_layers():
+    a = archer()
+    w = get_workload("dream_gqa")
+    m = w.model
+    P, G = w.decode.prompt_len, w.decode.resp_len
+    t0 = time.time()
+    say(f"Dream shape, {m.n_layers} layers, B 1, P {P}, G {G}: generating host weights")
+    W = model_weights(m, seed=w.weight_seed)
+    say(f"  host weights in {time.time() - t0:.1f} s")
+    Wd = _device_weights(W)
+    p = prompts(w)[0]
+    ctx = _ctx(m, Wd, 1, P, P, G)
+    rng = np.random.default_rng(73)
+    g0 = np.full(G, m.mask_id)
+    idx = rng.choice(G, G // 4, replace=False)
+    g0[idx] = rng.integers(0, m.vocab - 1, len(idx))
+    g1 = g0.copy()
+    idx = rng.choice(G, G // 8, replace=False)
+    g1[idx] = rng.integers(0, m.vocab - 1, len(idx))
+    z = host(ctx.refresh_prompt(dev_i32(p), [P], dev_i32(g0[None])))[0]
+    hid = host(ctx.read_rows(a.READ_HIDDEN, 1))
+    res = host(ctx.read_rows(a.READ_RESIDUAL, 1))
+    kv = ctx.read_prompt_kv(m.n_layers - 1, 0, P)
+    zc = host(ctx.step(dev_i32(g1[None])))[0]
+    ctx.close()
+    del Wd
+    t0 = time.time()
+    z_ref, cache, (stack, h_ref) = om.full_forward(W, m, p, g0, keep_hidden=True)
+    say(f"  oracle FullForward: {time.time() - t0:.1f} s")
+    _err("Dream depth 28 full logits", z, z_ref)
+    _err("Dream depth 28 full normalised hidden", hid, h_ref)
+    _resid("Dream depth 28 full residual", res, stack[-1][P:])
+    _cmp_cache("Dream depth 28 C_p layer 27 K", kv[0], cache[-1][0])
+    _cmp_cache("Dream depth 28 C_p layer 27 V", kv[1], cache[-1][1])
+    zc_ref, _ = om.cached_forward(W, m, g1, cache, P)
+    _err("Dream depth 28 cached logits", zc, zc_ref)
 
 
 def test_dream_two_layers_full_width_batch2():
