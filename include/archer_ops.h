@@ -50,6 +50,24 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
                                   int32_t ld2, void *O, void *workspace, size_t ws_bytes,
                                   void *hip_stream);
 
+/* archer_op_attention for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels, launch configuration and results, with the
+ * split-KV partials in a fixed scratch array that the library holds in each
+ * device's memory (64 MiB per device, for the life of the process) instead
+ * of a caller workspace.  Arguments as archer_op_attention without the
+ * workspace; hip_stream must belong to the calling thread's current device.
+ * Allocates nothing: ARCHER_E_SHAPE (before any launch) when the shape's
+ * split-KV partials, archer_op_attention_ws_bytes, exceed 64 MiB.  All calls
+ * on one device share its array: calls that overlap in time on one device
+ * (other streams, other threads) race, and must be serialised by the caller.
+ * The array is fully rewritten before it is read in every call, so nothing
+ * carries over from the previous call. */
+archer_status archer_op_attention_noalloc(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd,
+                                          const void *Q, const void *K1, const void *Vt1, int32_t nk1,
+                                          int32_t ld1, const void *K2, const void *Vt2, int32_t nk2,
+                                          int32_t ld2, void *O, void *hip_stream);
+
 /* Kernel classes for timing.  The projection classes _QKV, _O, _GATEUP and
  * _DOWN are the launches of CachedForward passes (M = G per sequence); their
  * _FULL twins are the same projections in FullForward (refresh) passes

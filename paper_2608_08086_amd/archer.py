@@ -37,7 +37,7 @@ EXPORTED = [
     "archer_op_attention_ws_bytes", "archer_op_attention", "archer_timing_begin", "archer_timing_end",
     "archer_pack_weight", "archer_session_begin", "archer_session_advance", "archer_session_response",
     "archer_session_state_bytes", "archer_session_save", "archer_session_restore", "archer_read_state",
-    "archer_set_single_term",
+    "archer_set_single_term", "archer_op_attention_noalloc",
 ]
 FORWARD_CONTROLLER, FORWARD_REFRESH, FORWARD_CACHED = 0, 1, 2
 READ_LOGITS, READ_HIDDEN, READ_RESIDUAL, READ_PROMPT_K, READ_PROMPT_V = range(5)
@@ -128,6 +128,9 @@ lib.archer_read_state.restype = C.c_int
 lib.archer_read_state.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, P, C.c_size_t]
 lib.archer_set_single_term.restype = C.c_int
 lib.archer_set_single_term.argtypes = [P, C.c_uint32]
+lib.archer_op_attention_noalloc.restype = C.c_int
+lib.archer_op_attention_noalloc.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, P, P, P,
+                                            C.c_int32, C.c_int32, P, P, C.c_int32, C.c_int32, P, P]
 lib.archer_timing_begin.restype = C.c_int
 lib.archer_timing_begin.argtypes = [P, C.c_uint32, C.c_int32]
 lib.archer_timing_end.restype = C.c_int
@@ -430,4 +433,19 @@ def op_attention(Q, K1, Vt1, nk1, K2, Vt2, nk2, dtype=BF16):
     wp = ws.data_ptr() + ((-ws.data_ptr()) % 256)
     _check(lib.archer_op_attention(dtype, Mq, Hq, Hkv, hd, _ptr(Q), _ptr(K1), _ptr(Vt1), nk1, ld1, _ptr(K2),
                                    _ptr(Vt2), nk2, ld2, _ptr(O), C.c_void_p(wp), nbytes, _stream()))
+    return O
+
+
+def op_attention_noalloc(Q, K1, Vt1, nk1, K2, Vt2, nk2, dtype=BF16, O=None):
+    """archer_op_attention_noalloc: as op_attention, with the split-KV partials in the library's
+    fixed scratch array (no workspace).  O may be given (preallocated); returns it."""
+    Hq, Mq, hd = Q.shape
+    Hkv, ld1, _ = K1.shape
+    ld2 = K2.shape[1]
+    for t in (Q, K1, Vt1, K2, Vt2):
+        assert t.dtype == qkv_dtype(dtype), "queries, keys and values: fp16 for BF16, fp32 for FP32"
+    if O is None:
+        O = torch.empty(Mq, Hq * hd, dtype=torch_dtype(dtype), device="cuda")
+    _check(lib.archer_op_attention_noalloc(dtype, Mq, Hq, Hkv, hd, _ptr(Q), _ptr(K1), _ptr(Vt1), nk1, ld1,
+                                           _ptr(K2), _ptr(Vt2), nk2, ld2, _ptr(O), _stream()))
     return O

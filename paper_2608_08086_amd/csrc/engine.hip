@@ -13,6 +13,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1013,10 +1014,14 @@ size_t archer_op_attention_ws_bytes(int32_t dtype, int32_t Mq, int32_t Hq, int32
   return align_up((size_t)ns * Hq * Mq * hd * 4, 256) + align_up((size_t)ns * Hq * Mq * 2 * 4, 256);
 }
 
-archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd, const void* Q,
-                                  const void* K1, const void* Vt1, int32_t nk1, int32_t ld1, const void* K2,
-                                  const void* Vt2, int32_t nk2, int32_t ld2, void* O, void* workspace,
-                                  size_t ws_bytes, void* hip_stream) {
+}  // extern "C"
+
+namespace {
+
+archer_status op_attention_impl(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd, const void* Q,
+                                const void* K1, const void* Vt1, int32_t nk1, int32_t ld1, const void* K2,
+                                const void* Vt2, int32_t nk2, int32_t ld2, void* O, void* workspace,
+                                size_t ws_bytes, void* hip_stream) {
   if (!Q || !K1 || !Vt1 || !K2 || !Vt2 || !O) return fail(ARCHER_E_ARG, "null operand");
   if (Mq < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || (hd != 64 && hd != 128)) return fail(ARCHER_E_SHAPE, "bad head shape");
   if (nk1 < 1 || nk2 < 1 || ld1 % 64 || ld2 % 64 || nk1 > ld1 || nk2 > ld2) return fail(ARCHER_E_SHAPE, "bad key segments");
@@ -1059,4 +1064,71 @@ archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t
   return ARCHER_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+archer_status archer_op_attention(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd, const void* Q,
+                                  const void* K1, const void* Vt1, int32_t nk1, int32_t ld1, const void* K2,
+                                  const void* Vt2, int32_t nk2, int32_t ld2, void* O, void* workspace,
+                                  size_t ws_bytes, void* hip_stream) {
+  return op_attention_impl(dtype, Mq, Hq, Hkv, hd, Q, K1, Vt1, nk1, ld1, K2, Vt2, nk2, ld2, O, workspace, ws_bytes,
+                           hip_stream);
+}
+
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The attention op for callers that cannot allocate device memory.  Its
+// split-KV partials live in `scratch`, a fixed array of this library in every
+// device's memory, instead of a caller workspace.  Host code never passes the
+// array's name to a kernel or a copy: it looks up each device's address once
+// (with that device current) and passes that address.
+namespace {
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+// Device address of the current device's `scratch` (looked up on the first call per device).
+archer_status scratch_address(void** out) {
+  int dev = 0;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(ARCHER_E_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(ARCHER_E_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ARCHER_OK;
+}
+}  // namespace
+
+extern "C" archer_status archer_op_attention_noalloc(int32_t dtype, int32_t Mq, int32_t Hq, int32_t Hkv, int32_t hd,
+                                                     const void* Q, const void* K1, const void* Vt1, int32_t nk1,
+                                                     int32_t ld1, const void* K2, const void* Vt2, int32_t nk2,
+                                                     int32_t ld2, void* O, void* hip_stream) {
+  if (Mq < 1 || Hq < 1 || hd < 1 || nk1 < 1 || nk2 < 1) return fail(ARCHER_E_SHAPE, "bad attention shape");
+  const int nkeys = ((nk1 + 63) & ~63) + nk2;
+  const int ns = op_attn_nsplit(dtype, Mq, Hq, nkeys);
+  void* ws = nullptr;
+  if (ns > 1) {
+    const size_t need = archer_op_attention_ws_bytes(dtype, Mq, Hq, hd, nkeys);
+    if (need > kScratchBytes)
+      return fail(ARCHER_E_SHAPE, "archer_op_attention_noalloc: this shape needs " + std::to_string(need) +
+                                      " bytes of split-KV scratch, more than the library's fixed " +
+                                      std::to_string(kScratchBytes) + " bytes; use archer_op_attention");
+    const archer_status st = scratch_address(&ws);
+    if (st) return st;
+  }
+  return op_attention_impl(dtype, Mq, Hq, Hkv, hd, Q, K1, Vt1, nk1, ld1, K2, Vt2, nk2, ld2, O, ws, kScratchBytes,
+                           hip_stream);
+}
