@@ -126,6 +126,11 @@ typedef struct {
   int32_t unmask_per_step;    /* k >= 1                                          */
   float remask_threshold;     /* tau                                             */
   int32_t max_remask;         /* 0 or 1                                          */
+  int32_t keep_logits;        /* nonzero: every forward also stores its fp32 logits in the
+                                 workspace (archer_read_state ARCHER_READ_LOGITS).  Zero:
+                                 bf16 models whose LM head runs the fused-statistics
+                                 epilogue write only the decoder's row statistics, not the
+                                 [B][G][V] logits (decisions are the same bits either way) */
 } archer_decode_cfg;
 
 /* Optional per-step record of archer_decode (device pointers; any may be NULL). */

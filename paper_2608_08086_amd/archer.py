@@ -74,7 +74,7 @@ class DecideCfg(C.Structure):
 class DecodeCfg(C.Structure):
     _fields_ = [("policy", C.c_int32), ("K", C.c_int32), ("steps", C.c_int32),
                 ("unmask_per_step", C.c_int32), ("remask_threshold", C.c_float),
-                ("max_remask", C.c_int32)]
+                ("max_remask", C.c_int32), ("keep_logits", C.c_int32)]
 
 
 class Trace(C.Structure):
@@ -262,10 +262,10 @@ class Context:
         return tens, Trace(*[t.data_ptr() for t in tens.values()])
 
     def decode(self, prompt, prompt_len, response, *, policy, K, steps, k=1, tau=0.1, max_remask=1,
-               trace=True):
+               trace=True, keep_logits=False):
         B = len(prompt_len)
         pl = (C.c_int32 * B)(*prompt_len)
-        dc = DecodeCfg(policy, int(min(K, NEVER)), steps, k, tau, max_remask)
+        dc = DecodeCfg(policy, int(min(K, NEVER)), steps, k, tau, max_remask, 1 if keep_logits else 0)
         tens, tr = self._trace(steps, B, k) if trace else (None, None)
         _check(lib.archer_decode(self.h, B, _ptr(prompt), pl, _ptr(response), C.byref(dc),
                                  C.byref(tr) if tr is not None else None))
@@ -273,12 +273,12 @@ class Context:
 
     # -- the resumable session (Algorithm 1 a few decisions at a time) --------------------------
     def session_begin(self, prompt, prompt_len, response_init, *, policy, K, steps, k=1, tau=0.1,
-                      max_remask=1, trace=True):
+                      max_remask=1, trace=True, keep_logits=False):
         """Start a session; returns the trace tensors (or None).  prompt and the trace tensors are
         kept alive by the context while the session may use them."""
         B = len(prompt_len)
         pl = (C.c_int32 * B)(*prompt_len)
-        dc = DecodeCfg(policy, int(min(K, NEVER)), steps, k, tau, max_remask)
+        dc = DecodeCfg(policy, int(min(K, NEVER)), steps, k, tau, max_remask, 1 if keep_logits else 0)
         tens, tr = self._trace(steps, B, k) if trace else (None, None)
         self._session = (prompt, tens, tr)
         self.B = B

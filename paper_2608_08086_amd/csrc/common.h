@@ -159,6 +159,27 @@ __device__ __forceinline__ void rms_normalize_row(const float* xr, const float* 
   }
 }
 
+// Decision statistics of the logits (the decoder's m = max, xhat = argmax,
+// log-sum-exp and log p(current token)) are built from partials.  One partial
+// covers the columns of a row that one LM-head multiply wave holds in one
+// column tile of BN columns: wave half h (0 or 1) holds, in lane group lg
+// (0..3), the columns
+//   stat_col(BN, h, lg, cb, e) = (cb / (CB/2)) * (BN/2) + h * (BN/4) + (cb % (CB/2)) * 16 + 4 lg + e
+// of the tile, cb < CB = BN / 32, e < 4.  A partial is (m, s, argmax) with m
+// the largest non-MASK logit, argmax the smallest column attaining it and
+// s = sum over lg of its lane sums, combined as (s0 + s1) + (s2 + s3), each lane
+// sum adding stat_exp(z, m) over cb then e in increasing order.  The LM-head
+// epilogue and the stand-alone kernel that reads stored logits produce the
+// same bits, and one kernel merges the partials of a row, so a decision does
+// not depend on which of the two produced them.
+__host__ __device__ __forceinline__ int stat_col(int BN, int h, int lg, int cb, int e) {
+  const int hcb = BN / 64;   // CB / 2
+  return (cb / hcb) * (BN / 2) + h * (BN / 4) + (cb % hcb) * 16 + 4 * lg + e;
+}
+__device__ __forceinline__ float stat_exp(float z, float m) {
+  return __builtin_amdgcn_exp2f((z - m) * 1.4426950408889634f);
+}
+
 // dst-row encoding of the K/V destination of a pass row: >= 0 is a row of the
 // fresh (response) K/V buffers, < 0 encodes prompt-cache row (-1 - v).
 __device__ __forceinline__ bool dst_is_fresh(int v) { return v >= 0; }

@@ -41,6 +41,8 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 struct Layout {
   size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML;
   size_t part, row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
+  size_t tstat, targ, zg;   // decision statistics partials [Rmax][npmax], current-token logits [Rmax]
+  int npmax;
   int ldcache, ldfresh, Mmax, Rmax, max_pos, ldq;
   int part_rows;   // rows the split-K partial buffer holds
   size_t cache_layer_elems;
@@ -127,6 +129,11 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
   L.xhat = take((size_t)L.Rmax * 4);
   L.ell = take((size_t)L.Rmax * 4);
   L.qv = take((size_t)L.Rmax * 4);
+  // statistics partials: at most two per 128 columns (the smallest column tile)
+  L.npmax = 2 * ((c->vocab + 127) / 128);
+  L.tstat = take((size_t)L.Rmax * L.npmax * sizeof(float2));
+  L.targ = take((size_t)L.Rmax * L.npmax * 4);
+  L.zg = take((size_t)L.Rmax * 4);
   L.err = take(256);
   L.total = off;
   return L;
@@ -163,6 +170,10 @@ struct archer_ctx {
   // projection classes (bits ARCHER_K_GEMM_*) whose activation operand is a
   // single bf16 value instead of the two-term pair
   uint32_t single_mask = 0;
+  // decision statistics: column tile of their partials (that of the LM-head
+  // GEMM when its epilogue produces them, stat_fused) and partials per row
+  int stat_tile = 128, np = 0;
+  bool stat_fused = false;
   // the most recent forward pass (for archer_read_state)
   SeqPlan last{};
   bool have_last = false;
@@ -175,6 +186,7 @@ struct archer_ctx {
     const int32_t* prompt = nullptr;
     int T = 0, t = 0;          // decisions in the schedule / made so far
     int cur = 0;               // g buffer (gbuf0 / gbuf1) holding the current response
+    bool keep = true;          // forwards store their logits in the workspace
     int r[ARCHER_MAXB] = {0};  // step of each sequence's anchor
   } ses;
   // timing
@@ -266,7 +278,7 @@ archer_status gemm(archer_ctx* c, int cls, int epi, GemmArgs& a) {
   gemm_prepare(c, a);
   const double es = (double)c->esz;
   double bytes = (double)a.M * a.K * es * (a.A2 ? 2 : 1) + (double)a.N * a.K * es;
-  if (epi == EPI_STORE) bytes += (double)a.M * a.N * 4;
+  if (epi == EPI_STORE) bytes += (a.C ? (double)a.M * a.N * 4 : 0.0) + (a.tstat ? (double)a.M * c->np * 12 : 0.0);
   else if (epi == EPI_RESID) bytes += 2.0 * a.M * a.N * 4 + (gemm_fuses_norm(a) ? (double)a.M * a.N * es * 2 : 0.0);
   else if (epi == EPI_SWIGLU) bytes += (double)a.M * (a.N / 2) * es * (a.H2 ? 2 : 1);
   else bytes += (double)a.M * a.N * es;
@@ -285,8 +297,10 @@ GemmArgs gargs(const void* A, int lda, const void* W, int ldw, int M, int N, int
 }
 
 // One forward over the selected sequences (full = FullForward, else CachedForward).
+// stats: the LM head also writes the decision statistics partials of the
+// response rows (contexts with stat_fused); logits may then be null.
 archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel, const int32_t* prompt,
-                          const int32_t* resp, float* logits) {
+                          const int32_t* resp, float* logits, bool stats = false) {
   if (sel.empty()) return ARCHER_OK;
   const archer_model_cfg& m = c->cfg;
   const Layout& L = c->L;
@@ -420,6 +434,12 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
                        m.vocab, d);
     a.A2 = cn2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
     a.C = logits; a.ldc = m.vocab; a.out_row = c->at<int>(L.out_row);
+    if (stats && c->stat_fused) {
+      a.tstat = c->at<float2>(L.tstat); a.targ = c->at<int>(L.targ); a.zg = c->at<float>(L.zg);
+      a.tg = resp; a.mask_id = m.mask_id;
+    } else if (!logits) {
+      return fail(ARCHER_E_STATE, "a forward without logits needs the fused decision statistics");
+    }
     if ((st = gemm(c, ARCHER_K_GEMM_HEAD, EPI_STORE, a))) return st;
   }
   HIPCHK(hipGetLastError());
@@ -429,19 +449,27 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   return ARCHER_OK;
 }
 
+// fused: the partials of these logits were written by the LM head of the
+// forward that produced them (same bits as the stand-alone kernel would give)
 archer_status decide_impl(archer_ctx* c, const float* logits, const int32_t* g_in, int32_t* g_out, int k,
                           float tau, int max_remask, int final_step, int32_t* dist, int32_t* unmask_pos,
                           int32_t* remask_pos, int32_t* tr_dist, int32_t* tr_unmask, int32_t* tr_utok,
-                          int32_t* tr_remask) {
+                          int32_t* tr_remask, bool fused = false) {
   const int B = c->batch, G = c->lim.resp_len, V = c->cfg.vocab;
   const int rows = B * G;
   const float log_tau = (float)std::log((double)tau);
-  return timed(c, ARCHER_K_DECIDE, (double)rows * V * 4, 0.0, [&] {
-    launch_rowstats(rows, logits, V, c->cfg.mask_id, g_in, c->at<int>(c->L.xhat), c->at<float>(c->L.ell),
-                    c->at<float>(c->L.qv), c->stream);
-    launch_select(B, g_in, g_out, c->at<int>(c->L.g_anchor), c->at<int>(c->L.xhat), c->at<float>(c->L.ell),
-                  c->at<float>(c->L.qv), G, c->cfg.mask_id, k, log_tau, max_remask, final_step,
-                  dist ? dist : c->at<int>(c->L.dist), unmask_pos, remask_pos, tr_dist, tr_unmask, tr_utok,
+  const Layout& L = c->L;
+  float2* tstat = c->at<float2>(L.tstat);
+  int* targ = c->at<int>(L.targ);
+  float* zg = c->at<float>(L.zg);
+  return timed(c, ARCHER_K_DECIDE, fused ? (double)rows * c->np * 12 : (double)rows * V * 4, 0.0, [&] {
+    if (!fused) launch_tile_stats(rows, logits, V, c->stat_tile, c->np, c->cfg.mask_id, g_in, tstat, targ, zg,
+                                  c->stream);
+    launch_finalize_stats(rows, c->np, tstat, targ, zg, g_in, V, c->cfg.mask_id, c->at<int>(L.xhat),
+                          c->at<float>(L.ell), c->at<float>(L.qv), c->stream);
+    launch_select(B, g_in, g_out, c->at<int>(L.g_anchor), c->at<int>(L.xhat), c->at<float>(L.ell),
+                  c->at<float>(L.qv), G, c->cfg.mask_id, k, log_tau, max_remask, final_step,
+                  dist ? dist : c->at<int>(L.dist), unmask_pos, remask_pos, tr_dist, tr_unmask, tr_utok,
                   tr_remask, c->stream);
     return 0;
   });
@@ -525,7 +553,7 @@ struct SnapHeader {
   archer_decode_cfg cfg;
   archer_trace tr;
   const int32_t* prompt;
-  int32_t T, t, cur, r[ARCHER_MAXB];
+  int32_t T, t, cur, keep, r[ARCHER_MAXB];
 };
 static_assert(sizeof(SnapHeader) <= kSnapHdr, "snapshot header");
 
@@ -544,6 +572,9 @@ std::vector<SnapRegion> snapshot_regions(const archer_ctx* c) {
   add(c->ses.cur ? L.gbuf1 : L.gbuf0, g);
   add(L.g_anchor, g);
   add(L.logits, z);
+  add(L.tstat, (size_t)L.Rmax * L.npmax * sizeof(float2));
+  add(L.targ, (size_t)L.Rmax * L.npmax * 4);
+  add(L.zg, (size_t)L.Rmax * 4);
   add(L.Kc, kv);
   add(L.Vtc, kv);
   return r;
@@ -576,6 +607,7 @@ void fill_header(const archer_ctx* c, SnapHeader& h) {
   h.T = c->ses.T;
   h.t = c->ses.t;
   h.cur = c->ses.cur;
+  h.keep = c->ses.keep ? 1 : 0;
 }
 
 }  // namespace
@@ -631,6 +663,18 @@ archer_status archer_init(const archer_model_cfg* cfg, const archer_weights* w, 
     c->w_up.push_back(w->w_up[l]);
     c->w_down.push_back(w->w_down[l]);
   }
+  if (cfg->dtype == ARCHER_BF16) {
+    // the LM head of a full batch of response rows, as run_forward launches it
+    GemmArgs h = gargs(c->at<char>(L.Cn), L.Rmax, c->lm_head, c->w_tiled ? cfg->vocab : cfg->d_model, L.Rmax,
+                       cfg->vocab, cfg->d_model);
+    h.A2 = c->at<char>(L.Cn2); h.a_tiled = 1; h.w_tiled = c->w_tiled;
+    h.ksplit = gemm_ksplit(cfg->vocab, cfg->d_model);
+    h.C = c->at<float>(L.logits); h.ldc = cfg->vocab;
+    const int bn = gemm_stats_bn(h);
+    c->stat_fused = bn > 0;
+    if (bn > 0) c->stat_tile = bn;
+  }
+  c->np = 2 * ((cfg->vocab + c->stat_tile - 1) / c->stat_tile);
   launch_rope_table(c->at<float2>(L.rope), L.max_pos, cfg->head_dim, (double)cfg->rope_theta, c->stream);
   hipError_t he = hipMemsetAsync(c->at<int>(L.err), 0, 256, c->stream);
   if (he == hipSuccess) he = hipGetLastError();
@@ -707,6 +751,7 @@ archer_status archer_session_begin(archer_ctx* c, int32_t batch, const int32_t* 
   S.T = dc->steps;
   S.t = 0;
   S.cur = 0;
+  S.keep = dc->keep_logits != 0 || !c->stat_fused;
   for (int b = 0; b < ARCHER_MAXB; ++b) S.r[b] = 0;
   int* g0 = c->at<int>(c->L.gbuf0);
   HIPCHK(hipMemcpyAsync(g0, response_init, (size_t)B * G * 4, hipMemcpyDeviceToDevice, c->stream));
@@ -717,7 +762,8 @@ archer_status archer_session_begin(archer_ctx* c, int32_t batch, const int32_t* 
   launch_store_rows(S.tr.dist, nullptr, zeros, zeros, B, c->stream);
   std::vector<int> all(B);
   for (int b = 0; b < B; ++b) all[b] = b;
-  if ((st = run_forward(c, true, all, prompt, g0, c->at<float>(c->L.logits)))) return st;
+  float* logits = S.keep ? c->at<float>(c->L.logits) : nullptr;
+  if ((st = run_forward(c, true, all, prompt, g0, logits, true))) return st;
   for (int b = 0; b < B; ++b) c->has_cache[b] = true;
   S.active = true;
   return ARCHER_OK;
@@ -733,7 +779,7 @@ archer_status archer_session_advance(archer_ctx* c, int32_t n, int32_t first_for
   const int B = c->batch, T = S.T, k = S.cfg.unmask_per_step;
   const archer_trace& tr = S.tr;
   int* g[2] = {c->at<int>(c->L.gbuf0), c->at<int>(c->L.gbuf1)};
-  float* logits = c->at<float>(c->L.logits);
+  float* logits = S.keep ? c->at<float>(c->L.logits) : nullptr;
   archer_status st;
   for (int i = 0; i < n && S.t < T; ++i) {
     const int t = S.t;
@@ -744,7 +790,7 @@ archer_status archer_session_advance(archer_ctx* c, int32_t n, int32_t first_for
     int32_t* trt = tr.unmask_tok ? tr.unmask_tok + (size_t)t * B * k : nullptr;
     int32_t* trr = tr.remask_pos ? tr.remask_pos + (size_t)t * B : nullptr;
     st = decide_impl(c, logits, g[S.cur], g[S.cur ^ 1], k, S.cfg.remask_threshold, S.cfg.max_remask,
-                     final ? 1 : 0, nullptr, nullptr, nullptr, trd, tru, trt, trr);
+                     final ? 1 : 0, nullptr, nullptr, nullptr, trd, tru, trt, trr, c->stat_fused);
     if (st) return st;
     S.cur ^= 1;
     S.t = t + 1;
@@ -772,8 +818,8 @@ archer_status archer_session_advance(archer_ctx* c, int32_t n, int32_t first_for
     }
     launch_store_rows(tr.refreshed ? tr.refreshed + (size_t)s * B : nullptr,
                       tr.age ? tr.age + (size_t)s * B : nullptr, ref_row, age_row, B, c->stream);
-    if ((st = run_forward(c, true, full, S.prompt, g[S.cur], logits))) return st;
-    if ((st = run_forward(c, false, cached, nullptr, g[S.cur], logits))) return st;
+    if ((st = run_forward(c, true, full, S.prompt, g[S.cur], logits, true))) return st;
+    if ((st = run_forward(c, false, cached, nullptr, g[S.cur], logits, true))) return st;
   }
   HIPCHK(hipGetLastError());
   if (t_out) *t_out = S.t;
@@ -836,6 +882,7 @@ archer_status archer_session_restore(archer_ctx* c, const void* src, size_t byte
   c->ses.T = h.T;
   c->ses.t = h.t;
   c->ses.cur = h.cur;
+  c->ses.keep = h.keep != 0;
   const char* s = (const char*)src;
   for (const SnapRegion& r : snapshot_regions(c))
     HIPCHK(hipMemcpyAsync(c->ws + r.ws_off, s + r.snap_off, r.bytes, hipMemcpyDeviceToDevice, c->stream));
@@ -862,7 +909,8 @@ archer_status archer_read_state(archer_ctx* c, int32_t what, int32_t layer, int3
   const int G = c->lim.resp_len, d = m.d_model;
   const size_t es = c->esz;
   if (what == ARCHER_READ_LOGITS) {
-    if (c->batch == 0) return fail(ARCHER_E_STATE, "no batch yet");
+    if (!c->ses.active) return fail(ARCHER_E_STATE, "no active decode session");
+    if (!c->ses.keep) return fail(ARCHER_E_STATE, "the session keeps no logits (archer_decode_cfg.keep_logits = 0)");
     const size_t need = (size_t)c->batch * G * m.vocab * 4;
     if (bytes < need) return fail(ARCHER_E_ARG, "dst too small");
     HIPCHK(hipMemcpyAsync(dst, c->at<float>(L.logits), need, hipMemcpyDeviceToDevice, c->stream));

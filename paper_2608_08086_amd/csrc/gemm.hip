@@ -511,7 +511,7 @@ int gemm_partial_wanted(int cfg, const GemmArgs& a) {
 bool gemm_args_ok(int epi, const GemmArgs& a) {
   if (!a.A || !a.W || a.M <= 0 || a.N <= 0 || a.K <= 0 || a.ksplit < 1) return false;
   switch (epi) {
-    case EPI_STORE: return a.C && a.ldc >= a.N;
+    case EPI_STORE: return (a.C && a.ldc >= a.N) || (a.tstat && a.targ && a.zg && a.tg);
     case EPI_RESID: return a.X && a.ldx >= a.N;
     case EPI_SWIGLU: return a.H && a.W2 && a.N % 2 == 0;
     case EPI_QKV:

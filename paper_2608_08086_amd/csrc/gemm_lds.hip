@@ -274,6 +274,56 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   }
   // accumulator (rb, cb)[e]: row wm*WM + 16*rb + lc, tile column tb[cb] + e,
   // tb[cb] = tc[cb] - lc + 4*lg (tc evaluated at lane lc = 4*lg)
+  if constexpr (EPI == EPI_STORE && !FOLD && WGN == 2) {
+    // decision statistics partial (tile tile_n, wave half wn) of each row, from
+    // the fp32 results (the values the logits store would write); columns
+    // tb[cb] + e are stat_col(BN, wn, lg, cb, e).  All lanes take part in the
+    // shuffles; rows past M (clamped loads) are computed and not written.
+    if (a.tstat) {
+      const int np = 2 * (a.N / BN);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int row = m0 + wm * WM + rb * 16 + lc;
+        const int rowc = min(row, a.M - 1);
+        const int orow = a.out_row ? a.out_row[rowc] : rowc;
+        const int cur = a.tg[orow];
+        float mx = -INFINITY;
+        int ix = 0x7fffffff;
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int col = tile_n * BN + tc[cb] - lc + 4 * lg + e;
+            const float v = acc[rb][cb][e];
+            if (col != a.mask_id && (v > mx || (v == mx && col < ix))) { mx = v; ix = col; }
+          }
+#pragma unroll
+        for (int o = 16; o <= 32; o <<= 1) {
+          const float m2 = __shfl_xor(mx, o, 64);
+          const int i2 = __shfl_xor(ix, o, 64);
+          if (m2 > mx || (m2 == mx && i2 < ix)) { mx = m2; ix = i2; }
+        }
+        float sum = 0.f;
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int col = tile_n * BN + tc[cb] - lc + 4 * lg + e;
+            const float v = acc[rb][cb][e];
+            if (col != a.mask_id) sum += stat_exp(v, mx);
+            if (col == cur && row < a.M) a.zg[orow] = v;
+          }
+        sum += __shfl_xor(sum, 16, 64);   // (s0 + s1), (s2 + s3)
+        sum += __shfl_xor(sum, 32, 64);   // (s0 + s1) + (s2 + s3)
+        if (lg == 0 && row < a.M) {
+          const size_t pi = (size_t)orow * np + 2 * tile_n + wn;
+          a.tstat[pi] = make_float2(mx, sum);
+          a.targ[pi] = ix;
+        }
+      }
+      if (!a.C) return;
+    }
+  }
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int row = m0 + wm * WM + rb * 16 + lc;
@@ -599,6 +649,13 @@ void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
 }
 
 }  // namespace
+
+int gemm_stats_bn(const GemmArgs& a) {
+  // the configurations whose kernel is gemm_lds_kernel with a 2 x 2 wave grid
+  const int cfg = gemm_pick_cfg(a, EPI_STORE) - GEMM_NCFG;
+  if ((cfg != 0 && cfg != 1) || a.ksplit != 1 || !gemm_lds_cfg_ok(cfg, a)) return 0;
+  return kLds[cfg].BN;
+}
 
 bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
   if (c < 0 || c >= GEMM_NCFG_LDS) return false;

@@ -126,93 +126,100 @@ template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const
 //   m = max z, xhat = smallest id attaining m, s = sum exp(z - m),
 //   ell = -log s (= m - lse, log top probability),
 //   q = z[g] - m - log s (log probability of the current token; decided rows).
-// One block of 1024 threads per row; each thread scans a strided slice with an
-// online (max, sum) pair, then a fixed-order tree combines the threads.
-__device__ __forceinline__ void stat_combine(float& m, float& s, int& id, float m2, float s2, int id2) {
-  if (s2 == 0.f) return;
-  if (s == 0.f) { m = m2; s = s2; id = id2; return; }
-  if (m2 > m) {
-    s = s * expf(m - m2) + s2;
-    m = m2;
-    id = id2;
-  } else if (m2 < m) {
-    s = s + s2 * expf(m2 - m);
-  } else {
-    s = s + s2;
-    id = min(id, id2);
+// Built from partials (stat_col in common.h).  The LM head produces them in
+// its epilogue; tile_stats_kernel produces the same bits from stored logits.
+// Thread (row, partial p): tile p / 2, wave half p % 2; its four lane groups'
+// sums are formed one after the other and combined as the epilogue's
+// xor-shuffles combine them.  Columns past V (a last partial tile) are skipped.
+__global__ __launch_bounds__(256) void tile_stats_kernel(const float* __restrict__ logits, int V, int BN, int np,
+                                                         int mask_id, const int* __restrict__ g, int rows,
+                                                         float2* __restrict__ tstat, int* __restrict__ targ,
+                                                         float* __restrict__ zg) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)rows * np) return;
+  const int row = (int)(idx / np), p = (int)(idx % np);
+  const int c0 = (p >> 1) * BN, h = p & 1, CB = BN / 32;
+  const float* z = logits + (size_t)row * V;
+  const int cur = g[row];
+  float mx = -INFINITY;
+  int ix = 0x7fffffff;
+  for (int lg = 0; lg < 4; ++lg)
+    for (int cb = 0; cb < CB; ++cb)
+      for (int e = 0; e < 4; ++e) {
+        const int col = c0 + stat_col(BN, h, lg, cb, e);
+        if (col >= V || col == mask_id) continue;
+        const float v = z[col];
+        if (v > mx || (v == mx && col < ix)) { mx = v; ix = col; }
+      }
+  float sl[4];
+  for (int lg = 0; lg < 4; ++lg) {
+    float sum = 0.f;
+    for (int cb = 0; cb < CB; ++cb)
+      for (int e = 0; e < 4; ++e) {
+        const int col = c0 + stat_col(BN, h, lg, cb, e);
+        if (col >= V) continue;
+        const float v = z[col];
+        if (col != mask_id) sum += stat_exp(v, mx);
+        if (col == cur) zg[row] = v;
+      }
+    sl[lg] = sum;
   }
+  tstat[(size_t)row * np + p] = make_float2(mx, (sl[0] + sl[1]) + (sl[2] + sl[3]));
+  targ[(size_t)row * np + p] = ix;
 }
 
-constexpr int RS_THREADS = 1024;   // threads per row
-constexpr int RS_BATCH = 8;        // float4 loads of a thread in flight before any is consumed
+void launch_tile_stats(int rows, const float* logits, int V, int BN, int np, int mask_id, const int* g,
+                       float2* tstat, int* targ, float* zg, hipStream_t st) {
+  const long n = (long)rows * np;
+  tile_stats_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(logits, V, BN, np, mask_id, g, rows, tstat, targ,
+                                                                 zg);
+}
 
-__global__ __launch_bounds__(RS_THREADS) void rowstats_kernel(const float* __restrict__ logits, int V,
-                                                              int mask_id, const int* __restrict__ g,
-                                                              int* __restrict__ xhat, float* __restrict__ ell,
-                                                              float* __restrict__ qv) {
-  __shared__ float sm[RS_THREADS], ss[RS_THREADS];
-  __shared__ int sid[RS_THREADS];
-  const int row = blockIdx.x;
-  const float* z = logits + (size_t)row * V;
-  float m = -INFINITY, s = 0.f;
+// Merge of a row's partials, one wave per row: lane l takes partials
+// l, l + 64, ... in order; M and xhat are order-free (max; smallest column at
+// the max), the sum s = sum_p s_p exp(m_p - M) runs per lane in partial
+// order and then over a fixed xor tree, read from lane 0.
+constexpr int FS_ROWS = 4;   // rows (waves) per block
+__global__ __launch_bounds__(64 * FS_ROWS) void finalize_stats_kernel(const float2* __restrict__ tstat,
+                                                                      const int* __restrict__ targ,
+                                                                      const float* __restrict__ zg,
+                                                                      const int* __restrict__ g, int np, int V,
+                                                                      int mask_id, int rows, int* __restrict__ xhat,
+                                                                      float* __restrict__ ell,
+                                                                      float* __restrict__ qv) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * FS_ROWS + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float2* ts = tstat + (size_t)row * np;
+  const int* ta = targ + (size_t)row * np;
+  float m = -INFINITY;
+  for (int p = lane; p < np; p += 64) m = fmaxf(m, ts[p].x);
+  const float M = wave_max(m);
   int id = 0x7fffffff;
-  // thread t scans the float4 chunks t, t + RS_THREADS, ... in increasing
-  // order, RS_BATCH chunks requested at a time
-  for (int base = threadIdx.x * 4; base < V; base += RS_THREADS * 4 * RS_BATCH) {
-    float4 t[RS_BATCH];
-#pragma unroll
-    for (int u = 0; u < RS_BATCH; ++u) {
-      const int v0 = base + u * RS_THREADS * 4;
-      if (v0 < V) t[u] = *(const float4*)(z + v0);
-    }
-#pragma unroll
-    for (int u = 0; u < RS_BATCH; ++u) {
-      const int v0 = base + u * RS_THREADS * 4;
-      if (v0 >= V) break;
-      const float e[4] = {t[u].x, t[u].y, t[u].z, t[u].w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int v = v0 + k;
-        if (v == mask_id) continue;
-        const float zv = e[k];
-        if (zv > m) {
-          s = s * expf(m - zv) + 1.f;
-          m = zv;
-          id = v;
-        } else {
-          s += expf(zv - m);
-        }
-      }
-    }
+  float s = 0.f;
+  for (int p = lane; p < np; p += 64) {
+    const float2 t = ts[p];
+    if (t.x == M) id = min(id, ta[p]);
+    if (t.y > 0.f) s += t.y * stat_exp(t.x, M);
   }
-  sm[threadIdx.x] = m;
-  ss[threadIdx.x] = s;
-  sid[threadIdx.x] = id;
-  __syncthreads();
-  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
-    if (threadIdx.x < w) {
-      float a = sm[threadIdx.x], b = ss[threadIdx.x];
-      int c = sid[threadIdx.x];
-      stat_combine(a, b, c, sm[threadIdx.x + w], ss[threadIdx.x + w], sid[threadIdx.x + w]);
-      sm[threadIdx.x] = a;
-      ss[threadIdx.x] = b;
-      sid[threadIdx.x] = c;
-    }
-    __syncthreads();
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    id = min(id, __shfl_xor(id, o, 64));
+    s += __shfl_xor(s, o, 64);
   }
-  if (threadIdx.x == 0) {
-    const float M = sm[0], S = ss[0];
-    const float logs = logf(S);
-    xhat[row] = sid[0];
+  if (lane == 0) {
+    const float logs = logf(s);
+    xhat[row] = id;
     ell[row] = -logs;
     const int cur = g[row];
-    qv[row] = (cur != mask_id && cur >= 0 && cur < V) ? (z[cur] - M) - logs : 0.f;
+    qv[row] = (cur != mask_id && cur >= 0 && cur < V) ? (zg[row] - M) - logs : 0.f;
   }
 }
 
-void launch_rowstats(int rows, const float* logits, int V, int mask_id, const int* g, int* xhat, float* ell,
-                     float* qv, hipStream_t st) {
-  rowstats_kernel<<<rows, RS_THREADS, 0, st>>>(logits, V, mask_id, g, xhat, ell, qv);
+void launch_finalize_stats(int rows, int np, const float2* tstat, const int* targ, const float* zg, const int* g,
+                           int V, int mask_id, int* xhat, float* ell, float* qv, hipStream_t st) {
+  finalize_stats_kernel<<<(unsigned)((rows + FS_ROWS - 1) / FS_ROWS), 64 * FS_ROWS, 0, st>>>(
+      tstat, targ, zg, g, np, V, mask_id, rows, xhat, ell, qv);
 }
 
 // ---------------------------------------------------------------------------

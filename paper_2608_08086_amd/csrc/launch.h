@@ -21,7 +21,11 @@ struct GemmArgs {
   int M, N, K;
   int ksplit;                            // K slices (bf16): a function of (N, K) only, see gemm_ksplit
   float* part;                           // fp32 partials [ksplit][M][N] for the per-slice launch, or null
-  float* C; int ldc; const int* out_row; // EPI_STORE
+  float* C; int ldc; const int* out_row; // EPI_STORE (C may be null when tstat is set: statistics only)
+  // EPI_STORE with decision statistics (LM head; see stat_col in common.h):
+  // partials tstat / targ [logits row][2 N / BN], the current token's logit
+  // zg [logits row]; tg = current tokens [logits row]
+  float2* tstat; int* targ; float* zg; const int* tg; int mask_id;
   float* X; int ldx;                     // EPI_RESID
   // EPI_RESID with a split-K reduction: optionally RMSNorm the updated rows of
   // X (gain ngain, epsilon neps) into the two-term activation (nout, nout2)
@@ -73,8 +77,13 @@ void launch_embed(const SeqPlan& pl, const void* emb, int d, int V, int mask_id,
 template <class T>
 void launch_rmsnorm(const SeqPlan& pl, int gather, int nrows, const float* x, const float* gain, void* out,
                     void* out2, int ld, int tiled, int d, float eps, int* out_row, hipStream_t st);
-void launch_rowstats(int rows, const float* logits, int V, int mask_id, const int* g, int* xhat, float* ell,
-                     float* qv, hipStream_t st);
+// Decision statistics: partials from stored logits (stat_col order, tiles of
+// BN columns, np = 2 ceil(V / BN) per row), then the per-row merge into
+// xhat (argmax), ell (log top probability) and qv (log p of the current token).
+void launch_tile_stats(int rows, const float* logits, int V, int BN, int np, int mask_id, const int* g,
+                       float2* tstat, int* targ, float* zg, hipStream_t st);
+void launch_finalize_stats(int rows, int np, const float2* tstat, const int* targ, const float* zg, const int* g,
+                           int V, int mask_id, int* xhat, float* ell, float* qv, hipStream_t st);
 void launch_select(int B, const int* g_in, int* g_out, const int* g_anchor, const int* xhat, const float* ell,
                    const float* qv, int G, int mask_id, int k, float log_tau, int max_remask, int final_step,
                    int* dist, int* unmask_pos, int* remask_pos, int* tr_dist, int* tr_unmask, int* tr_utok,
@@ -105,6 +114,9 @@ int gemm_pick_cfg(const GemmArgs& a, int epi);
 int gemm_partial_wanted(int cfg, const GemmArgs& a);
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st);
 int launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t st);
+// Column tile of the LM-head GEMM when it can also produce the decision
+// statistics partials (bf16, one slice, a 2 x 2 wave grid), else 0.
+int gemm_stats_bn(const GemmArgs& a);
 // true if launch_gemm_bf16 runs this EPI_RESID GEMM with a separate split-K
 // reduction, which then also applies the RMSNorm described by a.ngain
 bool gemm_fuses_norm(const GemmArgs& a);

@@ -44,7 +44,7 @@ def shadow_probe(ctx, shadow, prompt, prompt_len, g0, *, policy, K, steps, k=1, 
     B, G = g0.shape
     T = int(steps)
     tr = ctx.session_begin(prompt, prompt_len, g0, policy=policy, K=K, steps=T, k=k, tau=tau,
-                           max_remask=max_remask, trace=True)
+                           max_remask=max_remask, trace=True, keep_logits=True)
     probes = []
     n_cached = 0
     for t in range(T):

@@ -9,7 +9,11 @@
   forced forward, step by step;
 * ARCHER_READ_LOGITS returns the logits the session decides on (equal to a
   FullForward of the same state on a second context), and the session calls
-  refuse wrong states and foreign snapshots.
+  refuse wrong states and foreign snapshots;
+* the fused decision statistics: archer_decode, whose LM head writes only the
+  statistics partials, equals the same schedule driven call by call
+  (archer_refresh_prompt / archer_step with logits, archer_decide computing
+  the partials from them) bitwise, for 128- and 192-column head tiles.
 """
 
 import numpy as np
@@ -36,7 +40,8 @@ def _tiny():
 
 
 def _bf16_batch():
-    m = ModelShape(n_layers=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=1024,
+    # vocab 16384: the LM head runs one slice, so sessions use the fused decision statistics
+    m = ModelShape(n_layers=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=16384,
                    dtype="bf16", init_std=0.05)
     W = model_weights(m, seed=31)
     lens = [70, 129, 33]
@@ -88,7 +93,7 @@ def test_snapshot_restore_replays_bitwise():
     ctx = make_ctx(m, W, B, max(lens), sum(lens), G)
     prompt = dev_i32(np.concatenate(ps))
     g0 = dev_i32(np.full((B, G), m.mask_id, np.int32))
-    tr = ctx.session_begin(prompt, lens, g0, policy=a.AGE, K=4, steps=T, k=2, tau=0.1)
+    tr = ctx.session_begin(prompt, lens, g0, policy=a.AGE, K=4, steps=T, k=2, tau=0.1, keep_logits=True)
     ctx.session_advance(s)
     snap = ctx.session_save()
     z_at_s = ctx.read_logits(B).clone()
@@ -146,6 +151,10 @@ def test_read_logits_and_session_errors():
         ctx.session_advance(1)
     assert e.value.status == a.E_STATE
     ctx.session_begin(prompt, lens, dev_i32(g0), policy=a.AGE, K=4, steps=8)
+    with pytest.raises(a.ArcherError) as e:          # this session keeps no logits
+        ctx.read_logits(B)
+    assert e.value.status == a.E_STATE
+    ctx.session_begin(prompt, lens, dev_i32(g0), policy=a.AGE, K=4, steps=8, keep_logits=True)
     z = other.refresh_prompt(prompt, lens, dev_i32(g0))
     assert torch.equal(ctx.read_logits(B), z)
     # hidden / residual rows of the last pass: one FullForward of all three sequences
@@ -162,4 +171,54 @@ def test_read_logits_and_session_errors():
     with pytest.raises(a.ArcherError) as e:
         ctx.session_save()
     assert e.value.status == a.E_STATE
+    ctx.sync()
+
+
+@pytest.mark.parametrize("vocab,policy", [(16384, "age"), (18432, "age"), (18432, "hamming")])
+def test_fused_statistics_decode_equals_call_driven(vocab, policy):
+    """The LM head runs one slice (enough column tiles), so its epilogue produces the statistics:
+    vocab 16384 in 128-column tiles, 18432 (a multiple of 192) in 192-column tiles."""
+    a = archer()
+    m = ModelShape(n_layers=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=vocab,
+                   dtype="bf16", init_std=0.05)
+    say(f"fused statistics vs call-driven decisions, vocab {vocab}, {policy}")
+    W = model_weights(m, seed=33)
+    lens, G, T, k, tau, K = [45, 101], 32, 20, 2, 0.1, 3
+    rng = np.random.default_rng(34)
+    ps = [rng.integers(0, m.vocab - 1, n).astype(np.int32) for n in lens]
+    prompt = dev_i32(np.concatenate(ps))
+    B = len(lens)
+    pol = {"age": a.AGE, "hamming": a.HAMMING}[policy]
+    ctx = make_ctx(m, W, B, max(lens), sum(lens), G)
+    out, tr = ctx.decode(prompt, lens, dev_i32(np.full((B, G), m.mask_id)), policy=pol, K=K, steps=T, k=k,
+                         tau=tau)
+    # the fused path ran: the session kept no logits (only contexts with fused statistics may)
+    with pytest.raises(a.ArcherError) as e:
+        ctx.read_logits(B)
+    assert e.value.status == a.E_STATE
+    # the same algorithm through the call-level API (stand-alone statistics from stored logits)
+    drv = make_ctx(m, W, B, max(lens), sum(lens), G)
+    g = dev_i32(np.full((B, G), m.mask_id))
+    z = drv.refresh_prompt(prompt, lens, g)
+    r = np.zeros(B, dtype=np.int64)
+    refreshed = [np.ones(B, dtype=np.int32)]
+    for t in range(T):
+        final = t == T - 1
+        g_next, dist, _, _ = drv.decide(z, g, k=k, tau=tau, final=final)
+        if final:
+            g = g_next
+            break
+        s = t + 1
+        D = dist.cpu().numpy()
+        ref = (D >= K) if policy == "hamming" else (s - r >= K)
+        r[ref] = s
+        refreshed.append(ref.astype(np.int32))
+        if ref.any():
+            drv.refresh_prompt(prompt, lens, g_next, seq_sel=ref.tolist(), logits=z)
+        if (~ref).any():
+            drv.step(g_next, seq_sel=(~ref).tolist(), logits=z)
+        g = g_next
+    np.testing.assert_array_equal(out.cpu().numpy(), g.cpu().numpy())
+    np.testing.assert_array_equal(tr["refreshed"].cpu().numpy(), np.stack(refreshed))
+    assert 0 < np.stack(refreshed)[1:].sum() < (T - 1) * B
     ctx.sync()
