@@ -408,11 +408,16 @@ def main():
     sps = args.steps * period / wall
     log(f"bench: {args.steps} refresh periods of {period} decisions in {wall:.3f}s -> {sps:.2f} steps/s")
 
-    # refresh fraction of the timed forwards (those of the first decode's trace)
+    # refresh fraction of the timed forwards: those of the first decode's trace,
+    # plus, if the timed steps reached the end of its schedule, the next
+    # decode's forward 0 that closed that period (later decodes repeat it)
     ref = tr["refreshed"].cpu().numpy()
     lo = args.warmup * period + 1
-    hi = min(T, (args.warmup + args.steps) * period + 1)
-    refresh_fraction = float(ref[lo:hi].mean()) if hi > lo else None
+    wrapped = (args.warmup + args.steps) * period >= T
+    hi = T if wrapped else (args.warmup + args.steps) * period + 1
+    n_ref = float(ref[lo:hi].sum()) + (B if wrapped else 0)
+    n_fwd = (hi - lo) * B + (B if wrapped else 0)
+    refresh_fraction = n_ref / n_fwd if n_fwd > 0 else None
 
     full_sps = None
     if not args.no_full_refresh and args.policy != "always":

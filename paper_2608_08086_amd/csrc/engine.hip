@@ -111,7 +111,7 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
     const int F = c->d_ff, qkv = (hq + 2 * hkv) * hd;
     const int NK[5][2] = {{qkv, d}, {d, hq * hd}, {2 * F, d}, {d, F}, {c->vocab, d}};
     for (auto& nk : NK) {
-      const int S = gemm_ksplit(nk[0], nk[1]);
+      const int S = gemm_ksplit(nk[0], nk[1], L.Rmax);
       if (S > 1) sn = std::max(sn, (size_t)S * nk[0]);
     }
   }
@@ -270,7 +270,7 @@ SeqPlan build_plan(const archer_ctx* c, bool full, const std::vector<int>& sel) 
 // split-K slice count and partial buffer of a bf16 projection
 void gemm_prepare(archer_ctx* c, GemmArgs& a) {
   if (!is_bf16(c)) return;
-  a.ksplit = gemm_ksplit(a.N, a.K);
+  a.ksplit = gemm_ksplit(a.N, a.K, c->L.Rmax);
   if (a.M <= c->L.part_rows) a.part = c->at<float>(c->L.part);
 }
 
@@ -668,7 +668,7 @@ archer_status archer_init(const archer_model_cfg* cfg, const archer_weights* w, 
     GemmArgs h = gargs(c->at<char>(L.Cn), L.Rmax, c->lm_head, c->w_tiled ? cfg->vocab : cfg->d_model, L.Rmax,
                        cfg->vocab, cfg->d_model);
     h.A2 = c->at<char>(L.Cn2); h.a_tiled = 1; h.w_tiled = c->w_tiled;
-    h.ksplit = gemm_ksplit(cfg->vocab, cfg->d_model);
+    h.ksplit = gemm_ksplit(cfg->vocab, cfg->d_model, L.Rmax);
     h.C = c->at<float>(L.logits); h.ldc = cfg->vocab;
     const int bn = gemm_stats_bn(h);
     c->stat_fused = bn > 0;
@@ -1041,7 +1041,7 @@ archer_status archer_op_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, con
   if (A_lo && dtype != ARCHER_BF16) return fail(ARCHER_E_ARG, "A_lo is only meaningful for bf16");
   GemmArgs a = gargs(A, K, W, K, M, N, K);
   a.A2 = A_lo;
-  if (dtype == ARCHER_BF16) a.ksplit = gemm_ksplit(N, K);
+  if (dtype == ARCHER_BF16) a.ksplit = gemm_ksplit(N, K, M);
   a.C = Y; a.ldc = N;
   int rc;
   if (dtype == ARCHER_BF16) rc = launch_gemm_bf16(EPI_STORE, a, (hipStream_t)hip_stream);

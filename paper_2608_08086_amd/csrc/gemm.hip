@@ -458,9 +458,14 @@ const int kCfgBM[GEMM_NCFG] = {128, 256, 128, 256, 64, 64, 128};
 
 }  // namespace
 
-int gemm_ksplit(int N, int K) {
-  // slice count from (N, K) only: enough slices that a 256-row launch of
-  // 128 x 128 tiles fills the 256 CUs, within the K granularity
+int gemm_ksplit(int N, int K, int rows) {
+  // One slice when the smallest launch has enough 128-row tiles to fill the
+  // GPU on its own (rows >= 2048: at least 16 row tiles); otherwise enough
+  // slices that a 256-row launch of 128 x 128 tiles fills the 256 CUs,
+  // within the K granularity.  The count is fixed per context (rows is the
+  // context's response-row capacity), never per launch, so every pass of a
+  // context sums every output in the same order.
+  if (rows >= 2048) return 1;
   const int tiles = 2 * std::max(N / 128, 1);
   int S = 1;
   while (S < 8 && tiles * S < 256 && K % (2 * S * 64) == 0) S *= 2;

@@ -143,6 +143,41 @@ __device__ __forceinline__ void epi_tile_pair4(const GemmArgs& a, int tile_n, in
 #pragma unroll
       for (int e = 0; e < 4; ++e) epi_swiglu<T>(a, row, f + e, v1[e], v2[e]);
     }
+  } else if constexpr (EPI == EPI_QKV && sizeof(T) == 2) {
+    // four consecutive rotation pairs j .. j + 3 of one head (r and hd / 2 are
+    // multiples of 4): q / k halves as one 8-byte store each, v as four
+    // transposed element stores per half; the values of epi_qkv
+    using Q = qkv_t<T>;
+    const int half = a.hd / 2, p0 = tile_n * (BN / 2) + r;
+    const int head = p0 / half, j = p0 % half;
+    const int dst = a.row_dst[row];
+    if (head < a.hq + a.hkv) {
+      const float2* cs = a.rope + (size_t)a.row_pos[row] * half + j;
+      Q* p;
+      if (head < a.hq) p = (Q*)a.Qb + ((size_t)head * a.ldq + row) * a.hd;
+      else if (dst_is_fresh(dst)) p = (Q*)a.Kf + ((size_t)(head - a.hq) * a.ldfresh + dst) * a.hd;
+      else p = (Q*)a.Kc + ((size_t)(head - a.hq) * a.ldcache + dst_cache_row(dst)) * a.hd;
+      f16x4 o1, o2;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float2 o = rope_rotate(v1[e], v2[e], cs[e]);
+        o1[e] = from_f32<Q>(o.x);
+        o2[e] = from_f32<Q>(o.y);
+      }
+      *(f16x4*)(p + j) = o1;
+      *(f16x4*)(p + j + half) = o2;
+    } else {
+      const int vh = head - a.hq - a.hkv;
+      Q* vt;
+      int ld, col;
+      if (dst_is_fresh(dst)) { vt = (Q*)a.Vtf; ld = a.ldfresh; col = dst; }
+      else { vt = (Q*)a.Vtc; ld = a.ldcache; col = dst_cache_row(dst); }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt[((size_t)vh * a.hd + j + e) * ld + col] = from_f32<Q>(v1[e]);
+        vt[((size_t)vh * a.hd + j + e + half) * ld + col] = from_f32<Q>(v2[e]);
+      }
+    }
   } else {
 #pragma unroll
     for (int e = 0; e < 4; ++e) epi_tile_pair<EPI, T, BN>(a, tile_n, r + e, row, v1[e], v2[e]);

@@ -19,7 +19,7 @@ struct GemmArgs {
   const void* W; const void* W2; int ldw; // [N][K] (SWIGLU: W = gate [F][K], W2 = up [F][K], N = 2F)
   int w_tiled;                           //   k-block-major W (ldw = rows of each matrix), see act_at
   int M, N, K;
-  int ksplit;                            // K slices (bf16): a function of (N, K) only, see gemm_ksplit
+  int ksplit;                            // K slices (bf16): fixed per (N, K, context), see gemm_ksplit
   float* part;                           // fp32 partials [ksplit][M][N] for the per-slice launch, or null
   float* C; int ldc; const int* out_row; // EPI_STORE (C may be null when tstat is set: statistics only)
   // EPI_STORE with decision statistics (LM head; see stat_col in common.h):
@@ -104,7 +104,7 @@ void launch_read_act(const void* hi, const void* lo, int n, int d, int ld, int t
 // (gemm_lds.hip).  All give the same bits for the same (N, K) split.
 constexpr int GEMM_NCFG = 7;
 constexpr int GEMM_NCFG_LDS = 9;
-int gemm_ksplit(int N, int K);
+int gemm_ksplit(int N, int K, int rows);
 bool gemm_lds_cfg_ok(int c, const GemmArgs& a);
 int gemm_lds_tiles(int c, const GemmArgs& a);
 int launch_gemm_lds_cfg(int epi, int c, bool partial, const GemmArgs& a, hipStream_t st);
