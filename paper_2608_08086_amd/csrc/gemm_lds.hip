@@ -210,6 +210,64 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   // its second set of accumulators, run out of registers with the reads in
   // flight between the MFMAs, and keep the burst).
   constexpr bool PIPE = NA == 2 && CB <= 4 && !FOLD;
+  // Two-term 64 x 128 wave tiles (one K slice): a second fragment set does
+  // not fit beside the 128 accumulator registers, so one set is refilled in
+  // place.  The lo-term fragments of tile g are read during its hi-term
+  // MFMAs; after X_g the lo-term MFMAs run weight block by weight block, and
+  // each weight fragment of tile g + 1 is read as soon as the MFMAs of its
+  // block have taken the old one (the hi-term fragments of tile g + 1 go in
+  // among the first blocks).
+  constexpr bool ROLL = NA == 2 && CB == 8 && MODE == 0;
+  auto tile_roll = [&](int g, bool more) {
+    if constexpr (ROLL) {
+      const char* stg = smem + (g % NST) * STAGE;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[0][cb], fa[0][0][rb], acc[rb][cb], 0, 0, 0);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) fa[0][1][rb] = *(const bf16x8*)(stg + A_SL * 16 + a_lo[rb]);
+#pragma unroll
+      for (int i = 0; i < RB; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, RB * CB - RB, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (more) {
+        __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
+        gl_barrier();                               // X_g
+        const char* stn = smem + ((g + 1) % NST) * STAGE;
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[0][cb], fa[0][1][rb], acc[rb][cb], 0, 0, 0);
+          fb[0][cb] = *(const bf16x8*)(stn + b_lo[cb]);
+          if (cb < RB) fa[0][0][cb] = *(const bf16x8*)(stn + a_lo[cb]);
+        }
+        static_assert(RB <= CB, "the hi-term reads go in among the first RB blocks");
+#pragma unroll
+        for (int cb = 0; cb < RB; ++cb) {
+          __builtin_amdgcn_sched_group_barrier(0x008, RB, 0);   // the MFMAs of block cb
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);    // its weight and one hi-term fragment
+        }
+#pragma unroll
+        for (int cb = RB; cb < CB; ++cb) {
+          __builtin_amdgcn_sched_group_barrier(0x008, RB, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[0][cb], fa[0][1][rb], acc[rb][cb], 0, 0, 0);
+      }
+    }
+  };
   auto tile_body = [&](int g, int cur) {
     mfma_term(cur, 0);
     if constexpr (PIPE) {
@@ -251,10 +309,23 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
     }
   };
   gl_barrier();                                   // X_-1: tile 0 landed
-  read_frags(0, 0);
-  for (int g = 0; g < ntot; g += 2) {             // fragment buffer parity static in the two halves
-    tile_body(g, 0);
-    if (g + 1 < ntot) tile_body(g + 1, 1);
+  if constexpr (ROLL) {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) fb[0][cb] = *(const bf16x8*)(smem + b_lo[cb]);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) fa[0][0][rb] = *(const bf16x8*)(smem + a_lo[rb]);
+  } else {
+    read_frags(0, 0);
+  }
+  if constexpr (ROLL) {
+    // the last tile peeled off: no branch in the loop body
+    for (int g = 0; g + 1 < ntot; ++g) tile_roll(g, true);
+    tile_roll(ntot - 1, false);
+  } else {
+    for (int g = 0; g < ntot; g += 2) {           // fragment buffer parity static in the two halves
+      tile_body(g, 0);
+      if (g + 1 < ntot) tile_body(g + 1, 1);
+    }
   }
 
   if constexpr (PARTIAL) {
@@ -631,6 +702,7 @@ const LdsCfg kLds[GEMM_NCFG_LDS] = {
     {128, 192},   // 6: decoupled loaders, 4 A stages, 7 weight stages
     {128, 128},   // 7: decoupled loaders, 4 A stages, 10 weight stages
     {128, 128},   // 8: decoupled loaders, 3 A stages, 12 weight stages
+    {128, 256},   // 9: 2 x 2 multiply waves of 64 x 128, 4 stages, fragments refilled in place
 };
 
 template <int EPI>
@@ -644,7 +716,13 @@ void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
     case 5: ws_cfg<128, 192, 2, 2, 3, 8, EPI>(a, partial, st); break;
     case 6: ws_cfg<128, 192, 2, 2, 4, 7, EPI>(a, partial, st); break;
     case 7: ws_cfg<128, 128, 2, 2, 4, 10, EPI>(a, partial, st); break;
-    default: ws_cfg<128, 128, 2, 2, 3, 12, EPI>(a, partial, st); break;
+    case 8: ws_cfg<128, 128, 2, 2, 3, 12, EPI>(a, partial, st); break;
+    default: {
+      // one K slice, two-term activations only (the in-place refill needs both terms)
+      const int grid = gemm_grid_size(a.N / 256, (a.M + 127) / 128, 1);
+      gemm_lds_kernel<128, 256, 2, 2, 4, EPI, true, 0><<<grid, 512, 0, st>>>(a);
+      break;
+    }
   }
 }
 
@@ -653,7 +731,7 @@ void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
 int gemm_stats_bn(const GemmArgs& a) {
   // the configurations whose kernel is gemm_lds_kernel with a 2 x 2 wave grid
   const int cfg = gemm_pick_cfg(a, EPI_STORE) - GEMM_NCFG;
-  if ((cfg != 0 && cfg != 1) || a.ksplit != 1 || !gemm_lds_cfg_ok(cfg, a)) return 0;
+  if ((cfg != 0 && cfg != 1 && cfg != 9) || a.ksplit != 1 || !gemm_lds_cfg_ok(cfg, a)) return 0;
   return kLds[cfg].BN;
 }
 
@@ -661,6 +739,7 @@ bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
   if (c < 0 || c >= GEMM_NCFG_LDS) return false;
   const LdsCfg& k = kLds[c];
   if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * BK)) return false;
+  if (c == 9 && (!a.A2 || a.ksplit != 1)) return false;
   // 32-bit lane offsets
   if ((size_t)a.N * (a.w_tiled ? BK : a.ldw) * 2 >= (1ull << 32) || (size_t)a.M * (a.a_tiled ? BK : a.lda) * 2 >= (1ull << 32))
     return false;

@@ -38,9 +38,10 @@ def test_gemm_f32_matches_oracle(M, N, K):
     np.testing.assert_allclose(Y, on.linear(A64, W64), rtol=0, atol=1e-4)
 
 
-@pytest.mark.parametrize("M,N,K", [(37, 192, 320), (256, 512, 4096)])
+@pytest.mark.parametrize("M,N,K", [(37, 192, 320), (256, 512, 4096), (300, 65536, 256)])
 def test_gemm_two_term_activation_matches_oracle(M, N, K):
-    """A = hi + lo (bf16 pair of an fp32 activation) against the unrounded activation."""
+    """A = hi + lo (bf16 pair of an fp32 activation) against the unrounded activation; N 65536
+    runs the 128 x 256 tiles (enough column tiles), with a ragged last row tile."""
     say(f"gemm two-term bf16 M={M} N={N} K={K}")
     a = archer()
     import torch

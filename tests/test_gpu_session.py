@@ -174,10 +174,11 @@ def test_read_logits_and_session_errors():
     ctx.sync()
 
 
-@pytest.mark.parametrize("vocab,policy", [(16384, "age"), (18432, "age"), (18432, "hamming")])
+@pytest.mark.parametrize("vocab,policy", [(16384, "age"), (18432, "age"), (18432, "hamming"), (65536, "age")])
 def test_fused_statistics_decode_equals_call_driven(vocab, policy):
     """The LM head runs one slice (enough column tiles), so its epilogue produces the statistics:
-    vocab 16384 in 128-column tiles, 18432 (a multiple of 192) in 192-column tiles."""
+    vocab 16384 in 128-column tiles, 18432 (a multiple of 192) in 192-column tiles, 65536 (256
+    tiles of 256 columns) in 256-column tiles."""
     a = archer()
     m = ModelShape(n_layers=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512, vocab=vocab,
                    dtype="bf16", init_std=0.05)
