@@ -5,8 +5,8 @@
 // bf16-model kernel: flash-style online softmax with MFMA.  Queries, keys and
 // values are fp16 (the bf16 path stores them so; see qkv_t in common.h), the
 // scores S = Q K^T are fp16 MFMAs with fp32 accumulation, and P V multiplies
-// the two-term fp16 probabilities (hi + lo) with two MFMAs, so that the
-// rounding of the probabilities does not limit the attention output.  The
+// the probabilities rounded to fp16 (11 significant bits: an absolute error
+// of at most 2^-12 |v| in the output, whatever the key count).  The
 // output is the two-term bf16 activation of the O projection.  A workgroup owns
 // 16 * QB * NW query rows (256, 128 or 64) of one (sequence, query head) and
 // a contiguous range of 64-key tiles; with split-KV the splits' unnormalised
@@ -256,11 +256,9 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
     for (int i = 0; i < DB; ++i) o[qb][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   f32x4 sc[QB][4];
-  // probabilities as the two-term pair hi = fp16(p), lo = fp16(p - hi): P V
-  // multiplies both (two MFMAs per fragment), so a probability enters with
-  // about 22 significant bits instead of 11 (at most 2^-24 absolute below
-  // fp16's normal range)
-  f16x8 pb[2][QB], plo[2][QB];
+  // probabilities as fp16 (p <= 1; below fp16's normal range at most 2^-25
+  // absolute), the B operands of O^T = V^T P^T
+  f16x8 pb[2][QB];
 
   // S^T = K Q^T of local tile i: sc[qb][kb][e] = raw score of key kb*16 + 4*lg + e, query lc of block qb
   auto scores = [&](int st) __attribute__((always_inline)) {
@@ -289,7 +287,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
     att_mfma_pipeline<4 * DS, QB>();
   };
   // online softmax of local tile i (running maxima in log2 units); leaves the
-  // two-term fp16 probabilities in pb / plo as the B operands of O^T = V^T P^T
+  // fp16 probabilities in pb as the B operands of O^T = V^T P^T
   auto softmax = [&](int i) __attribute__((always_inline)) {
     const int k0 = (t0 + i) * KT;
     const bool ct = k0 < ppad;
@@ -357,14 +355,11 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const f16 h0 = (f16)sc[qb][2 * ks][e], h1 = (f16)sc[qb][2 * ks + 1][e];
-          pb[ks][qb][e] = h0;
-          pb[ks][qb][4 + e] = h1;
-          plo[ks][qb][e] = (f16)(sc[qb][2 * ks][e] - (float)h0);
-          plo[ks][qb][4 + e] = (f16)(sc[qb][2 * ks + 1][e] - (float)h1);
+          pb[ks][qb][e] = (f16)sc[qb][2 * ks][e];
+          pb[ks][qb][4 + e] = (f16)sc[qb][2 * ks + 1][e];
         }
   };
-  // O^T += V^T P^T for local tile i (probabilities in pb + plo)
+  // O^T += V^T P^T for local tile i (probabilities in pb)
   auto pv_update = [&](int st) __attribute__((always_inline)) {
     const u32x4* Vcur = Vs + st * VSL;
 #pragma unroll
@@ -382,10 +377,9 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
           o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[db], pb[ks][qb], o[qb][db], 0, 0, 0);
-          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[db], plo[ks][qb], o[qb][db], 0, 0, 0);
         }
     }
-    att_mfma_pipeline<2 * DB, 2 * QB>();
+    att_mfma_pipeline<2 * DB, QB>();
   };
 
   // Ping-pong schedule.  A wave's tile i is an MFMA half M(i) = [PV(i - 1);

@@ -138,7 +138,7 @@ def _attn_case(dtype, Mq, Hq, Hkv, hd, nk1, nk2, seed, rows=None, heads=None, q_
 def test_attention_bf16_matches_oracle(Mq, Hq, Hkv, hd, nk1, nk2):
     say(f"attention bf16 Mq={Mq} Hq={Hq} Hkv={Hkv} hd={hd} nk1={nk1} nk2={nk2}")
     a = archer()
-    # fp16 inputs and two-term probabilities in P V; the op returns the output's bf16 hi term
+    # fp16 inputs and fp16 probabilities in P V; the op returns the output's bf16 hi term
     # only (the model path also keeps the lo term), so |err| <~ 2^-9 max|o|
     err = _attn_case(a.BF16, Mq, Hq, Hkv, hd, nk1, nk2, 11)
     say(f"  max abs err {err:.3e}")
