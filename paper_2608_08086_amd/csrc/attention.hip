@@ -20,7 +20,7 @@
 // permuted (att_key_row) so that the probabilities a lane holds for two key
 // blocks are 8 consecutive keys, which is exactly the B operand of
 // O^T = V^T P^T and whose V^T partner is one 16-byte LDS read.  Row
-// statistics need only two xor-shuffles across the four lane groups.
+// statistics need only two lane-swap steps across the four lane groups.
 #include <algorithm>
 
 #include "launch.h"
@@ -122,6 +122,26 @@ __device__ __forceinline__ void att_mfma_pipeline() {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
   __builtin_amdgcn_sched_group_barrier(0x008, MPR * AHEAD, 0);
+}
+
+// Reductions over the four 16-lane groups of a wave (lanes l, l ^ 16, l ^ 32,
+// l ^ 48) with the lane-swap instructions (v_permlane16_swap_b32 exchanges
+// the odd 16-lane rows of one operand with the even rows of the other,
+// v_permlane32_swap_b32 the upper half with the lower half): with both
+// operands x, the two results hold x and its partner in every lane, so one
+// max / add finishes each level, on the VALU instead of an LDS permute.  The
+// sums give every lane the same bits as x + partner (fp addition commutes).
+__device__ __forceinline__ float att_max_groups(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float att_sum_groups(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Key (within a 64-key tile) of row r of the score MFMA's A operand for key
@@ -312,8 +332,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) m = fmaxf(m, sc[qb][kb][e]);
-      m = fmaxf(m, __shfl_xor(m, 16, 64));
-      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      m = att_max_groups(m);
       mt[qb] = m * a.scale_log2;
       grow |= mt[qb] > m_run[qb] + ATT_RESCALE_LOG2;   // the query's own rule
     }
@@ -449,8 +468,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
   // o[qb][db][e]: dimension db*16 + 4*lg + e of query lc of block qb
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    l_run[qb] += __shfl_xor(l_run[qb], 16, 64);
-    l_run[qb] += __shfl_xor(l_run[qb], 32, 64);
+    l_run[qb] = att_sum_groups(l_run[qb]);
   }
   if (nsplit == 1) {
 #pragma unroll
