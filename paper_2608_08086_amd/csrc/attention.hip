@@ -286,7 +286,9 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kp = 0; kp < 4; kp += 2) {
-      // the fragments of two key blocks are requested before the first is used
+      // the fragments of two key blocks are requested before the first is
+      // used; the MFMAs go dimension step by dimension step over both key
+      // blocks, so four independent accumulation chains are in flight
       f16x8 kf[2][DS];
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
@@ -296,9 +298,9 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
           kf[k2][ds] = __builtin_bit_cast(f16x8, Kcur[r * KCPR + ((ds * 4 + lg) ^ att_kswz<KCPR>(r))]);
       }
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
+      for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
-        for (int ds = 0; ds < DS; ++ds)
+        for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb)
             sc[qb][kp + k2] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[k2][ds], qf[qb][ds],
