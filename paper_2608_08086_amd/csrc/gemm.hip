@@ -480,12 +480,22 @@ int gemm_pick_cfg(const GemmArgs& a, int epi) {
   // tile is not used for slices folded in one workgroup (its second
   // accumulator set does not fit the registers of two waves per SIMD).
   // 128 x 256 tiles (64 x 128 wave tiles: fewer LDS bytes per MFMA) for
-  // two-term launches of one K slice with a full round of 256 workgroups; the
-  // LM head decides on N alone, so that the column tile of its fused decision
-  // statistics does not depend on the row count of a pass.
+  // two-term launches of one K slice, where they take fewer rounds of 256
+  // workgroups (one per CU) times the time of a tile: measured on the LLaDA-8B
+  // projections, a 128 x 192 tile takes 1.5x and a 128 x 256 tile 1.77x the
+  // time of a 128 x 128 tile.  The LM head decides on N alone, so that the
+  // column tile of its fused decision statistics does not depend on the row
+  // count of a pass.
   if (a.A2 && a.ksplit == 1 && a.N % 256 == 0 && gemm_lds_cfg_ok(9, a)) {
-    const bool many = epi == EPI_STORE ? a.N / 256 >= 256 : (long)(a.N / 256) * ((a.M + 127) / 128) >= 256;
-    if (many) return GEMM_NCFG + 9;
+    bool wide;
+    if (epi == EPI_STORE) {
+      wide = a.N / 256 >= 256;
+    } else {
+      const long mt = (a.M + 127) / 128;
+      const auto cost = [&](int bn, double t) { return (double)((a.N / bn * mt + 255) / 256) * t; };
+      wide = cost(256, 1.77) < (a.N % 192 == 0 ? cost(192, 1.5) : cost(128, 1.0));
+    }
+    if (wide) return GEMM_NCFG + 9;
   }
   if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a)) {
     const bool fold = a.ksplit > 1 && !(a.part && gemm_partial_wanted(GEMM_NCFG + 0, a));
