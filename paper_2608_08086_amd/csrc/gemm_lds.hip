@@ -33,6 +33,8 @@
 
 #include "gemm_common.h"
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
 namespace {
 
 // s_waitcnt immediates (gfx9 encoding)
@@ -63,6 +65,54 @@ __device__ __forceinline__ int gl_swz(int row) { return (row >> 1) & 3; }
 
 constexpr int BK = 32;      // k chunk per tile (one MFMA k step)
 constexpr int CPR = BK / 8; // 16-byte chunks per tile row
+
+// QKV projection, value heads.  A tile whose column pairs are all value pairs
+// is staged in LDS as the transposed tile (one row of BM + 8 keys per value
+// dimension) and written to V^T in 16-byte chunks along the key axis wherever
+// eight consecutive pass rows go to eight consecutive, aligned key columns of
+// one buffer; element stores otherwise.  Written one element per lane, the
+// transposed layout gives every two-byte store its own cache line, which the
+// L2 then reads whole to merge.  The stored values are those of
+// epi_tile_pair4.
+template <int BN>
+__device__ __forceinline__ bool qkv_value_tile(const GemmArgs& a, int tile_n) {
+  return tile_n * (BN / 2) >= (a.hq + a.hkv) * (a.hd / 2);
+}
+constexpr int VT_PAD = 8;
+template <int BM, int BN, int NTHREADS>
+__device__ __forceinline__ void store_value_tile(const GemmArgs& a, const f16* vs, int tile_n, int m0, int t) {
+  constexpr int KS = BM + VT_PAD, KC = BM / 8;
+  static_assert(NTHREADS % KC == 0, "a thread keeps one key chunk");
+  // this thread's chunk of eight keys is the same for every dimension row it stores
+  const int kc = t % KC, k0 = m0 + kc * 8;
+  if (k0 >= a.M) return;
+  const int nk = min(8, a.M - k0);
+  const int dst0 = a.row_dst[k0];
+  const bool fresh = dst_is_fresh(dst0);
+  const int col0 = fresh ? dst0 : dst_cache_row(dst0);
+  f16* vt = (f16*)(fresh ? a.Vtf : a.Vtc);
+  const int ld = fresh ? a.ldfresh : a.ldcache;
+  bool vec = nk == 8 && col0 % 8 == 0 && ld % 8 == 0 && ((uintptr_t)vt & 15) == 0;
+  for (int i = 1; i < 8 && vec; ++i) {
+    const int di = a.row_dst[k0 + i];
+    vec = dst_is_fresh(di) == fresh && (fresh ? di : dst_cache_row(di)) == col0 + i;
+  }
+  const int half = a.hd / 2, p0 = tile_n * (BN / 2);
+  for (int drow = t / KC; drow < BN; drow += NTHREADS / KC) {
+    const int p = p0 + (drow >> 1);
+    const int vh = p / half - a.hq - a.hkv, d = p % half + (drow & 1) * half;
+    const f16* src = vs + drow * KS + kc * 8;
+    if (vec) {
+      *(u32x4*)(vt + (size_t)(vh * a.hd + d) * ld + col0) = *(const u32x4*)src;
+    } else {
+      for (int i = 0; i < nk; ++i) {
+        const int di = a.row_dst[k0 + i];
+        if (dst_is_fresh(di)) ((f16*)a.Vtf)[(size_t)(vh * a.hd + d) * a.ldfresh + di] = src[i];
+        else ((f16*)a.Vtc)[(size_t)(vh * a.hd + d) * a.ldcache + dst_cache_row(di)] = src[i];
+      }
+    }
+  }
+}
 
 template <int BM, int BN, int WGM, int WGN, int NST, int EPI, bool SPLIT, int MODE>
 __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
@@ -145,6 +195,13 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
     }
     // the trailing loads must land before the workgroup's LDS is released
     __builtin_amdgcn_s_waitcnt(GL_VMCNT(0));
+    if constexpr (EPI == EPI_QKV && MODE == 0 && SPLIT) {
+      if (qkv_value_tile<BN>(a, tile_n)) {
+        __syncthreads();   // X_v1: every load landed, every fragment read done
+        __syncthreads();   // X_v2: the multiply waves staged the tile
+        store_value_tile<BM, BN, 512>(a, (const f16*)smem, tile_n, m0, tid);
+      }
+    }
     return;
   }
 
@@ -345,6 +402,30 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   }
   // accumulator (rb, cb)[e]: row wm*WM + 16*rb + lc, tile column tb[cb] + e,
   // tb[cb] = tc[cb] - lc + 4*lg (tc evaluated at lane lc = 4*lg)
+  if constexpr (EPI == EPI_QKV && MODE == 0 && SPLIT) {
+    if (qkv_value_tile<BN>(a, tile_n)) {
+      constexpr int KS = BM + VT_PAD;
+      static_assert(BN * KS * 2 <= NST * STAGE, "the staged value tile fits the LDS stages");
+      f16* vs = (f16*)smem;
+      __syncthreads();   // X_v1
+      // tile column c < BN / 2 is pair c (first dimension half), c + BN / 2 its partner
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int kl = wm * WM + rb * 16 + lc;
+#pragma unroll
+        for (int cb = 0; cb < CB / 2; ++cb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int c = tc[cb] - lc + 4 * lg + e;
+            vs[(2 * c) * KS + kl] = from_f32<f16>(acc[rb][cb][e]);
+            vs[(2 * c + 1) * KS + kl] = from_f32<f16>(acc[rb][cb + CB / 2][e]);
+          }
+      }
+      __syncthreads();   // X_v2
+      store_value_tile<BM, BN, 512>(a, vs, tile_n, m0, tid);
+      return;
+    }
+  }
   if constexpr (EPI == EPI_STORE && !FOLD && WGN == 2) {
     // decision statistics partial (tile tile_n, wave half wn) of each row, from
     // the fp32 results (the values the logits store would write); columns
