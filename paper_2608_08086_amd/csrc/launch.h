@@ -55,7 +55,11 @@ struct AttnArgs {
 // waves of 16).  The largest tile that still gives the pass enough
 // workgroups is used; the result of a query row does not depend on the tiling
 // (every softmax decision is per query).
-constexpr int ATTN_MAX_SPLIT = 8;          // split-KV bound (workspace is sized for it)
+// At most 4 splits: a long-prompt pass that would take 8 splits of 256-row
+// tiles takes 4 of 128-row tiles instead (the same number of workgroups, half
+// the partial bytes; measured at P 4096, 256 rows, 32 heads: 42.1 against
+// 43.3 us with the merge).
+constexpr int ATTN_MAX_SPLIT = 4;          // split-KV bound (workspace is sized for it)
 constexpr int ATTN_TILES_PER_SPLIT = 8;    // 64-key tiles per split (target)
 constexpr int ATTN_MIN_WGS = 256;          // workgroups wanted per pass (one per CU)
 int attn_qt_bf16(const int* rows, const int* nsplit, int n, int hq);

@@ -14,7 +14,7 @@ from gpu_util import archer, rand_f16, say
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    (256, 32, 32, 128, 4096, 256),   # the LLaDA-8B-shaped long-prompt cached pass: 8 splits, 34 MB of partials
+    (256, 32, 32, 128, 4096, 256),   # the LLaDA-8B-shaped long-prompt cached pass: 4 splits, 17 MB of partials
     (64, 8, 2, 64, 700, 40),         # smaller: GQA 4:1, 2 splits
 ]
 
