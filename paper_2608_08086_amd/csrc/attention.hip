@@ -169,7 +169,10 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_bf16_kernel(SeqPlan pl, AttnA
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lg = lane >> 4, lc = lane & 15;
-  const int gq = blockIdx.x, h = blockIdx.y, split = blockIdx.z;
+  // heads vary fastest in the dispatch order: workgroups are dealt to the 8
+  // XCDs round-robin, so every query tile and split of a head runs on one XCD
+  // and reads the head's keys and values through one L2
+  const int h = blockIdx.x, gq = blockIdx.y, split = blockIdx.z;
   const int s = plan_find(pl.qt_off, pl.n, gq);
   const int nsplit = pl.nsplit[s];
   if (split >= nsplit) return;
@@ -572,9 +575,9 @@ void attn_launch_hd(const SeqPlan& pl, const AttnArgs& a, dim3 grid, hipStream_t
 }
 
 int launch_attn_bf16(const SeqPlan& pl, const AttnArgs& a, hipStream_t st) {
-  const dim3 grid(pl.qt_off[pl.n], a.hq, pl.max_split);
-  if (grid.x == 0) return 0;
-  if (pl.max_split > 1 && (!a.Opart || !a.ML)) return 1;
+  const dim3 grid(a.hq, pl.qt_off[pl.n], pl.max_split);
+  if (grid.y == 0) return 0;
+  if (grid.y > 65535 || (pl.max_split > 1 && (!a.Opart || !a.ML))) return 1;
   if ((pl.qt != 256 && pl.qt != 128 && pl.qt != 64) || (a.hd != 128 && a.hd != 64)) return 1;
   if (a.hd == 128) attn_launch_hd<128>(pl, a, grid, st);
   else attn_launch_hd<64>(pl, a, grid, st);
