@@ -40,6 +40,7 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
   size_t rope, Kc, Vtc, Kf, Vtf, x, act, act2, Q, O, O2, H, H2, Cn, Cn2, logits, Opart, ML;
+  size_t xc, Qc;   // residual and query rows of the response rows in CachedForward order (last full layer)
   size_t part, row_pos, row_dst, out_row, g_anchor, gbuf0, gbuf1, dist, xhat, ell, qv, err, total;
   size_t tstat, targ, zg;   // decision statistics partials [Rmax][npmax], current-token logits [Rmax]
   int npmax;
@@ -93,6 +94,8 @@ Layout make_layout(const archer_model_cfg* c, const archer_limits* l) {
   L.act = take((size_t)L.Mmax * d * esz);
   L.act2 = take(lo * L.Mmax * d * esz);
   L.Q = take((size_t)hq * L.ldq * hd * esz);
+  L.xc = take((size_t)L.Rmax * d * 4);
+  L.Qc = take((size_t)hq * L.Rmax * hd * esz);
   L.O = take((size_t)L.Mmax * hq * hd * esz);
   L.O2 = take(lo * L.Mmax * hq * hd * esz);
   L.H = take((size_t)L.Mmax * c->d_ff * esz);
@@ -176,6 +179,7 @@ struct archer_ctx {
   bool stat_fused = false;
   // the most recent forward pass (for archer_read_state)
   SeqPlan last{};
+  size_t last_x = 0;   // workspace offset of the residual rows of the last forward (x, or xc after a full pass)
   bool have_last = false;
   uint32_t last_single = 0;
   // decode session: Algorithm 1 advanced a number of decisions at a time
@@ -305,10 +309,19 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   const archer_model_cfg& m = c->cfg;
   const Layout& L = c->L;
   const SeqPlan pl = build_plan(c, full, sel);
-  const int rows = pl.rows, d = m.d_model, hq = m.n_heads, hkv = m.n_kv_heads, hd = m.head_dim, F = m.d_ff;
+  const int d = m.d_model, hq = m.n_heads, hkv = m.n_kv_heads, hd = m.head_dim, F = m.d_ff;
+  // The layers run on plan P over R rows with residual X; in a full pass the
+  // last layer switches to the CachedForward plan of the same sequences after
+  // its QKV projection: the prompt rows' keys and values are then in the cache
+  // and nothing reads their attention, MLP or final residual.
+  const SeqPlan plc = full ? build_plan(c, false, sel) : pl;
+  const SeqPlan* P = &pl;
+  int rows = pl.rows;
   const int qkv_n = (hq + 2 * hkv) * hd;
   const size_t es = c->esz;
   float* x = c->at<float>(L.x);
+  void* qbuf = c->at<char>(L.Q);
+  int ldq = L.ldq;
   void* act = c->at<char>(L.act);
   // low terms of the activations feeding each projection class (null where the
   // class takes a single bf16 operand)
@@ -340,10 +353,10 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   auto norm = [&](const float* gain, int gather, int nrows, void* out, void* out2, int cap) {
     return timed(c, ARCHER_K_NORM, (double)nrows * d * (4 + es * (out2 ? 2 : 1)), 0.0, [&] {
       if (is_bf16(c))
-        launch_rmsnorm<bf16>(pl, gather, nrows, x, gain, out, out2, cap, 1, d, m.rms_eps, c->at<int>(L.out_row),
+        launch_rmsnorm<bf16>(*P, gather, nrows, x, gain, out, out2, cap, 1, d, m.rms_eps, c->at<int>(L.out_row),
                              c->stream);
       else
-        launch_rmsnorm<float>(pl, gather, nrows, x, gain, out, out2, d, 0, d, m.rms_eps, c->at<int>(L.out_row),
+        launch_rmsnorm<float>(*P, gather, nrows, x, gain, out, out2, d, 0, d, m.rms_eps, c->at<int>(L.out_row),
                               c->stream);
       return 0;
     });
@@ -351,9 +364,11 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
 
   double kv_keys = 0;
   for (int s = 0; s < pl.n; ++s) kv_keys += pl.p_len[s] + pl.G;
-  double attn_q_keys = 0;
-  for (int s = 0; s < pl.n; ++s)
-    attn_q_keys += (double)(pl.row_off[s + 1] - pl.row_off[s]) * (pl.p_len[s] + pl.G);
+  auto q_keys = [&](const SeqPlan& p) {
+    double v = 0;
+    for (int s = 0; s < p.n; ++s) v += (double)(p.row_off[s + 1] - p.row_off[s]) * (p.p_len[s] + p.G);
+    return v;
+  };
 
   // RMSNorms whose input is the residual just updated by a split-K GEMM run
   // inside that GEMM's reduction (same arithmetic as the stand-alone kernel)
@@ -377,10 +392,17 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       a.row_pos = row_pos; a.row_dst = row_dst; a.rope = c->at<float2>(L.rope);
       if ((st = gemm(c, full ? ARCHER_K_GEMM_QKV_FULL : ARCHER_K_GEMM_QKV, EPI_QKV, a))) return st;
     }
+    if (full && l + 1 == m.n_layers) {
+      float* xc = c->at<float>(L.xc);
+      void* qc = c->at<char>(L.Qc);
+      launch_gather_resp_rows(pl, x, xc, d, qbuf, qc, L.ldq, L.Rmax, hq, hd * (int)es, c->stream);
+      HIPCHK(hipGetLastError());
+      P = &plc; rows = plc.rows; x = xc; qbuf = qc; ldq = L.Rmax;
+    }
     {
       AttnArgs a;
       memset(&a, 0, sizeof(a));
-      a.Q = c->at<char>(L.Q); a.ldq = L.ldq;
+      a.Q = qbuf; a.ldq = ldq;
       a.Kc = c->at<char>(L.Kc) + (size_t)l * L.cache_layer_elems * es;
       a.Vtc = c->at<char>(L.Vtc) + (size_t)l * L.cache_layer_elems * es;
       a.ldcache = L.ldcache;
@@ -392,11 +414,11 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
       // Q read once, O written once (two terms for bf16), every real key's K
       // and V read once
       const double bytes = (double)rows * hq * hd * es * (a.O2 ? 3 : 2) + kv_keys * hkv * hd * es * 2;
-      const double flops = 4.0 * attn_q_keys * hq * hd;
+      const double flops = 4.0 * q_keys(*P) * hq * hd;
       int max_keys = 0;
-      for (int s = 0; s < pl.n; ++s) max_keys = std::max(max_keys, ((pl.p_len[s] + 63) & ~63) + pl.G);
+      for (int s = 0; s < P->n; ++s) max_keys = std::max(max_keys, ((P->p_len[s] + 63) & ~63) + P->G);
       st = timed(c, full ? ARCHER_K_ATTN_FULL : ARCHER_K_ATTN, bytes, flops, [&] {
-        return is_bf16(c) ? launch_attn_bf16(pl, a, c->stream) : launch_attn_f32(pl, a, max_keys, c->stream);
+        return is_bf16(c) ? launch_attn_bf16(*P, a, c->stream) : launch_attn_f32(*P, a, max_keys, c->stream);
       });
       if (st) return st;
     }
@@ -443,7 +465,8 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
     if ((st = gemm(c, ARCHER_K_GEMM_HEAD, EPI_STORE, a))) return st;
   }
   HIPCHK(hipGetLastError());
-  c->last = pl;
+  c->last = *P;
+  c->last_x = full ? L.xc : L.x;
   c->have_last = true;
   c->last_single = sm;
   return ARCHER_OK;
@@ -929,7 +952,7 @@ archer_status archer_read_state(archer_ctx* c, int32_t what, int32_t layer, int3
       else
         launch_read_act<float>(c->at<char>(L.Cn), nullptr, n, d, d, 0, (float*)dst, c->stream);
     } else {
-      const float* x = c->at<float>(L.x);
+      const float* x = c->at<float>(c->last_x);
       for (int s = 0; s < pl.n; ++s) {
         const size_t r0 = (size_t)pl.row_off[s] + (pl.full ? pl.p_len[s] : 0);
         HIPCHK(hipMemcpyAsync((float*)dst + (size_t)s * G * d, x + r0 * d, (size_t)G * d * 4,

@@ -376,6 +376,35 @@ void launch_fill_i32(int* p, int v, size_t n, hipStream_t st) {
 //
 // Two rows of n <= ARCHER_MAXB ints passed by value (per-sequence trace rows of
 // a session step); a null destination is skipped.
+// Response rows of a FullForward pass moved into the row layout of a
+// CachedForward pass (row s G + i of selected sequence s): the residual row
+// (d floats) and the query row of every head (Q [hq][ldq][hd], qbytes bytes
+// per row).  The last layer of a full pass needs nothing else of its prompt
+// rows once their keys and values are in the cache, so it continues on the
+// response rows only.
+__global__ __launch_bounds__(256) void gather_resp_rows_kernel(SeqPlan pl, const float* __restrict__ x,
+                                                               float* __restrict__ xc, int d,
+                                                               const char* __restrict__ Q, char* __restrict__ Qc,
+                                                               int ldq, int ldqc, int hq, int qbytes) {
+  const int r = blockIdx.x, s = r / pl.G, i = r % pl.G;
+  const int src = pl.row_off[s] + pl.p_len[s] + i;
+  const float4* xs = (const float4*)(x + (size_t)src * d);
+  float4* xd = (float4*)(xc + (size_t)r * d);
+  for (int k = threadIdx.x; k < d / 4; k += blockDim.x) xd[k] = xs[k];
+  const int nq = qbytes / 16;
+  for (int k = threadIdx.x; k < hq * nq; k += blockDim.x) {
+    const int h = k / nq, c = k % nq;
+    ((uint4*)(Qc + ((size_t)h * ldqc + r) * qbytes))[c] = ((const uint4*)(Q + ((size_t)h * ldq + src) * qbytes))[c];
+  }
+}
+
+void launch_gather_resp_rows(const SeqPlan& pl, const float* x, float* xc, int d, const void* Q, void* Qc, int ldq,
+                             int ldqc, int hq, int qbytes, hipStream_t st) {
+  const int n = pl.n * pl.G;
+  if (n > 0)
+    gather_resp_rows_kernel<<<n, 256, 0, st>>>(pl, x, xc, d, (const char*)Q, (char*)Qc, ldq, ldqc, hq, qbytes);
+}
+
 __global__ void store_rows_kernel(int* a, int* b, I32Row va, I32Row vb, int n) {
   const int i = threadIdx.x;
   if (i < n) {

@@ -96,6 +96,9 @@ void launch_fill_i32(int* p, int v, size_t n, hipStream_t st);
 // Session and state-read copies (kernels_misc.hip).
 struct I32Row { int v[ARCHER_MAXB]; };
 void launch_store_rows(int* a, int* b, const I32Row& va, const I32Row& vb, int n, hipStream_t st);
+// FullForward response rows (residual, queries) into CachedForward row order
+void launch_gather_resp_rows(const SeqPlan& pl, const float* x, float* xc, int d, const void* Q, void* Qc, int ldq,
+                             int ldqc, int hq, int qbytes, hipStream_t st);
 template <class T>
 void launch_read_cache(const void* K, const void* Vt, int ld, int off, int P, int hkv, int hd, void* Kd, void* Vd,
                        hipStream_t st);
