@@ -253,28 +253,32 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   // measured no faster.  Either orientation gives the same bits (each output
   // is the same sum of the same products).
   constexpr bool CT = !PARTIAL;
+  // one MFMA of weight fragment wf and activation fragment xf in the tile's orientation
+  auto mm = [&](const bf16x8& wf, const bf16x8& xf, const f32x4& c) __attribute__((always_inline)) {
+    return CT ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xf, c, 0, 0, 0)
+              : __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, wf, c, 0, 0, 0);
+  };
   auto mfma_term = [&](int buf, int t) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb)
-        acc[rb][cb] = CT ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[buf][cb], fa[buf][t][rb], acc[rb][cb], 0, 0, 0)
-                         : __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][t][rb], fb[buf][cb], acc[rb][cb], 0, 0, 0);
+      for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = mm(fb[buf][cb], fa[buf][t][rb], acc[rb][cb]);
   };
-  // Two-term tiles of at most 64 columns per wave: the fragment reads of tile
-  // g + 1 are spread one per lo-term MFMA of tile g, so that a burst of reads
-  // never holds up the MFMA issue (wider wave tiles, and the folded mode with
-  // its second set of accumulators, run out of registers with the reads in
-  // flight between the MFMAs, and keep the burst).
-  constexpr bool PIPE = NA == 2 && CB <= 4 && !FOLD;
-  // Two-term 64 x 128 wave tiles (one K slice): a second fragment set does
-  // not fit beside the 128 accumulator registers, so one set is refilled in
-  // place.  The lo-term fragments of tile g are read during its hi-term
-  // MFMAs; after X_g the lo-term MFMAs run weight block by weight block, and
-  // each weight fragment of tile g + 1 is read as soon as the MFMAs of its
-  // block have taken the old one (the hi-term fragments of tile g + 1 go in
-  // among the first blocks).
-  constexpr bool ROLL = NA == 2 && CB == 8 && MODE == 0;
+  // Two-term tiles of 64, 96 or 128 columns per wave, except in the folded
+  // mode (its second accumulator set leaves no room): one fragment set,
+  // refilled in place.  The lo-term fragments of tile g are read during its
+  // hi-term MFMAs; after X_g the lo-term MFMAs run weight block by weight
+  // block, and each weight fragment of tile g + 1 is read as soon as the
+  // MFMAs of its block have taken the old one (the hi-term fragments of tile
+  // g + 1 go in among the first blocks), so reads never come in a burst.
+  // Measured against two fragment sets (a burst of reads after X_g for 96
+  // columns, reads spread one per lo-term MFMA for 64): 128 x 192 tiles 5-10 %
+  // faster (LLaDA-8B gate/up and QKV shapes at 256 and 768 rows), 128 x 128
+  // tiles 0-3 %, bitwise the same.
+  constexpr bool ROLL = NA == 2 && (CB == 4 || CB == 6 || CB == 8) && !FOLD;
+  // Two-term tiles of 32 columns per wave: two fragment sets, the reads of
+  // tile g + 1 spread one per lo-term MFMA of tile g.
+  constexpr bool PIPE = NA == 2 && CB <= 4 && !FOLD && !ROLL;
   auto tile_roll = [&](int g, bool more) {
     if constexpr (ROLL) {
       const char* stg = smem + (g % NST) * STAGE;
@@ -282,7 +286,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb)
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[0][cb], fa[0][0][rb], acc[rb][cb], 0, 0, 0);
+          acc[rb][cb] = mm(fb[0][cb], fa[0][0][rb], acc[rb][cb]);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) fa[0][1][rb] = *(const bf16x8*)(stg + A_SL * 16 + a_lo[rb]);
 #pragma unroll
@@ -300,7 +304,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
         for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
-            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[0][cb], fa[0][1][rb], acc[rb][cb], 0, 0, 0);
+            acc[rb][cb] = mm(fb[0][cb], fa[0][1][rb], acc[rb][cb]);
           fb[0][cb] = *(const bf16x8*)(stn + b_lo[cb]);
           if (cb < RB) fa[0][0][cb] = *(const bf16x8*)(stn + a_lo[cb]);
         }
@@ -321,7 +325,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
         for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
-            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[0][cb], fa[0][1][rb], acc[rb][cb], 0, 0, 0);
+            acc[rb][cb] = mm(fb[0][cb], fa[0][1][rb], acc[rb][cb]);
       }
     }
   };
