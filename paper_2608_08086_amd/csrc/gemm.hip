@@ -20,9 +20,11 @@
 //
 // Tile order (tile_of in gemm_common.h).  Workgroups are dispatched
 // round-robin over the 8 XCDs; each XCD owns every eighth (N tile, slice)
-// group and walks blocks of its groups times all M tiles, so that the tiles
-// it runs at once share both operands through its L2 (with 8 slices each XCD
-// owns one K slice, whose part of A stays in its L2).
+// group (or, for passes with few groups and many M tiles, every second or
+// fourth group and a share of the M tiles) and walks blocks of its groups
+// times its M tiles, so that the tiles it runs at once share both operands
+// through its L2 (with 8 slices each XCD owns one K slice, whose part of A
+// stays in its L2).
 #include <algorithm>
 
 #include "launch.h"
@@ -32,7 +34,11 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 #include "gemm_common.h"
 
 
-int gemm_grid_size(int n_tiles, int m_tiles, int S) { return ((n_tiles * S + 7) / 8) * 8 * m_tiles; }
+int gemm_grid_size(int n_tiles, int m_tiles, int S) {
+  // 8 XCDs times the most workgroups tile_of gives one XCD
+  const int groups = n_tiles * S, py = tile_py(groups, m_tiles), px = 8 / py;
+  return 8 * ((groups + px - 1) / px) * ((m_tiles + py - 1) / py);
+}
 
 #define GEMM_GLOAD(slot, k0)                                                             \
   do {                                                                                   \

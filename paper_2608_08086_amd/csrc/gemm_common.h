@@ -193,27 +193,36 @@ __device__ __forceinline__ int logical_col(const GemmArgs& a, int tile_n, int r)
 }
 
 // XCD-aware decomposition of the linear workgroup id.  Workgroups are
-// dispatched round-robin over the 8 XCDs, so XCD x runs ids x, x + 8, ...;
-// it owns the (N tile, slice) groups g with g mod 8 = x.  With few M tiles
-// (M up to 1024 rows) all M tiles of one group run back to back, so a weight
-// tile is read from memory once and then hits the XCD's L2.  With many M
-// tiles, its workgroups walk blocks of 8 of its groups and inside a block all
-// M tiles, the groups varying fastest: the workgroups an XCD runs at once then
-// cover a few M tiles times 8 weight tiles, so that the activation rows are
-// not re-read from memory for every weight tile.
+// dispatched round-robin over the 8 XCDs, so XCD x runs ids x, x + 8, ....
+// With few M tiles (M up to 1024 rows) XCD x owns the (N tile, slice) groups
+// g with g mod 8 = x and runs all M tiles of one group back to back, so a
+// weight tile is read from memory once and then hits the XCD's L2.  With many
+// M tiles, an XCD's workgroups walk blocks of 8 of its groups and inside a
+// block its M tiles, the groups varying fastest: the workgroups an XCD runs
+// at once cover a few M tiles times 8 weight tiles, so that activation rows
+// are not re-read from memory for every weight tile.  An XCD needs 6 or more
+// groups for that; when 8 XCDs would leave it fewer (N = 4096 at 256-column
+// tiles: 2 each, and every XCD would read all of A), py = 2 or 4 XCDs share
+// one set of groups (g mod px with px = 8 / py) and split its M tiles
+// (m mod py), which cuts the L2-miss reads of such a pass by about a third.
+__host__ __device__ inline int tile_py(int groups, int m_tiles) {
+  return m_tiles > 8 && groups < 48 ? (groups < 24 ? 4 : 2) : 1;
+}
 __device__ __forceinline__ bool tile_of(int id, int n_tiles, int m_tiles, int S, int* tn, int* tm, int* z) {
   const int groups = n_tiles * S;
-  const int x = id % 8, rest = id / 8;
-  const int gx = (groups - x + 7) / 8;                 // groups owned by XCD x
-  if (rest >= gx * m_tiles) return false;
+  const int py = tile_py(groups, m_tiles), px = 8 / py;
+  const int x = id % 8, rest = id / 8, xn = x % px, xm = x / px;
+  const int gx = (groups - xn + px - 1) / px;          // groups of XCD x
+  const int mx = (m_tiles - xm + py - 1) / py;         // M tiles of XCD x
+  if (rest >= gx * mx) return false;
   const int gb = m_tiles > 8 ? 8 : 1;                  // groups per block
-  const int blk = rest / (gb * m_tiles);
+  const int blk = rest / (gb * mx);
   const int nb = min(gb, gx - blk * gb);               // groups in this block
-  const int within = rest - blk * gb * m_tiles;
-  const int group = (blk * gb + within % nb) * 8 + x;
+  const int within = rest - blk * gb * mx;
+  const int group = (blk * gb + within % nb) * px + xn;
   *tn = group / S;
   *z = group % S;
-  *tm = within / nb;
+  *tm = (within / nb) * py + xm;
   return true;
 }
 
