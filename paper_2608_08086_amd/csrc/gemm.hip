@@ -492,7 +492,7 @@ int gemm_pick_cfg(const GemmArgs& a, int epi) {
   // time of a 128 x 128 tile.  The LM head decides on N alone, so that the
   // column tile of its fused decision statistics does not depend on the row
   // count of a pass.
-  if (a.A2 && a.ksplit == 1 && a.N % 256 == 0 && gemm_lds_cfg_ok(9, a)) {
+  if (a.A2 && a.ksplit == 1 && a.N % 256 == 0 && gemm_lds_cfg_ok(2, a)) {
     bool wide;
     if (epi == EPI_STORE) {
       wide = a.N / 256 >= 256;
@@ -501,7 +501,7 @@ int gemm_pick_cfg(const GemmArgs& a, int epi) {
       const auto cost = [&](int bn, double t) { return (double)((a.N / bn * mt + 255) / 256) * t; };
       wide = cost(256, 1.77) < (a.N % 192 == 0 ? cost(192, 1.5) : cost(128, 1.0));
     }
-    if (wide) return GEMM_NCFG + 9;
+    if (wide) return GEMM_NCFG + 2;
   }
   if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a)) {
     const bool fold = a.ksplit > 1 && !(a.part && gemm_partial_wanted(GEMM_NCFG + 0, a));

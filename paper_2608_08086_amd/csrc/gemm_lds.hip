@@ -576,255 +576,6 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
 }
 
 
-// Exact wait: at most n (0 <= n, wave-uniform) tiles of I load instructions
-// each still outstanding, n capped at NS - 1.  s_waitcnt takes an immediate,
-// so the count is matched against every possible value.
-template <int I, int K>
-__device__ __forceinline__ void gl_wait_match(int n) {
-  if constexpr (K >= 0) {
-    if (n == K) {
-      __builtin_amdgcn_s_waitcnt(GL_VMCNT(K * I));
-      return;
-    }
-    gl_wait_match<I, K - 1>(n);
-  }
-}
-template <int NS, int I>
-__device__ __forceinline__ void gl_wait_tiles(int n) {
-  if (n >= NS - 1) __builtin_amdgcn_s_waitcnt(GL_VMCNT((NS - 1) * I));
-  else gl_wait_match<I, NS - 2>(n);
-}
-
-// Decoupled variant: loader waves 4-5 stream the A tiles through NSA stages,
-// loader waves 6-7 stream the weight tiles through NSW stages.  Each loader
-// wave has its own memory counter, so the weight stream (from HBM, long
-// latency) runs NSW - 1 tiles ahead of the multiply waves while the A stream
-// (from L2) needs only a few stages; no load is issued past the last tile.
-template <int BM, int BN, int WGM, int WGN, int NSA, int NSW, int EPI, bool SPLIT, int MODE>
-__global__ __launch_bounds__(512, 1) void gemm_ws_kernel(GemmArgs a) {
-  constexpr int WM = BM / WGM, WN = BN / WGN;
-  constexpr int RB = WM / 16, CB = WN / 16;
-  constexpr int NA = SPLIT ? 2 : 1;
-  constexpr int A_SL = BM * CPR, B_SL = BN * CPR;          // 16-byte slots per tile and term
-  constexpr int AJ = A_SL / 128, BJ = B_SL / 128;          // instructions per loader wave per term / tile
-  constexpr int IA = NA * AJ, IW = BJ;
-  constexpr int A_STAGE = NA * A_SL * 16, W_STAGE = B_SL * 16;
-  constexpr bool PARTIAL = MODE == 2, FOLD = MODE == 1;
-  static_assert(WGM * WGN == 4 && CB % 2 == 0 && RB >= 1, "bad wave grid");
-  static_assert(A_SL % 128 == 0 && B_SL % 128 == 0, "two loader waves per operand issue whole instructions");
-  static_assert(BN % (32 * WGN) == 0, "each wave takes 16-column blocks from both tile halves");
-  static_assert((NSA - 1) * IA <= 63 && (NSW - 1) * IW <= 63 && NSA >= 2 && NSW >= 2, "vmcnt range");
-  static_assert((BN / 2) % (64 / CPR) == 0, "pair halves must not share a load instruction");
-  static_assert(NSA * A_STAGE + NSW * W_STAGE <= 160 * 1024, "LDS");
-  __shared__ __attribute__((aligned(1024))) char smem[NSA * A_STAGE + NSW * W_STAGE];
-  char* const smemW = smem + NSA * A_STAGE;
-
-  const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
-  int tile_n, tile_m, z;
-  if (!tile_of(blockIdx.x, n_tiles, m_tiles, PARTIAL ? a.ksplit : 1, &tile_n, &tile_m, &z)) return;
-  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int m0 = tile_m * BM;
-  const int kslice = a.K / a.ksplit;
-  const int kbeg = PARTIAL ? z * kslice : 0;
-  const int nslices = FOLD ? a.ksplit : 1;
-  const int kt_slice = (PARTIAL || FOLD ? kslice : a.K) / BK;
-  const int ntot = nslices * kt_slice;
-
-  if (w >= 4) {
-    // ---- loader waves -------------------------------------------------------
-    const int wp = w & 1;
-    if (w < 6) {
-      const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
-      // rows past M load row M - 1: finite data, and those rows are never stored
-      unsigned a_go[AJ];
-#pragma unroll
-      for (int j = 0; j < AJ; ++j) {
-        const int q = j * 128 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
-        const int row = min(m0 + r, a.M - 1);
-        a_go[j] = ((unsigned)row * (a.a_tiled ? BK : a.lda) + (pc ^ gl_swz(r)) * 8) * 2;
-      }
-      const bf16* Abase[2] = {(const bf16*)a.A, (const bf16*)(SPLIT ? a.A2 : a.A)};
-      const size_t akmul = a.a_tiled ? (size_t)a.lda : 1;
-      auto issue = [&](int g) {
-        if (g >= ntot) return;
-        const int k0 = kbeg + g * BK;
-        const unsigned st = lds0 + (unsigned)((g % NSA) * A_STAGE);
-#pragma unroll
-        for (int t = 0; t < NA; ++t)
-#pragma unroll
-          for (int j = 0; j < AJ; ++j)
-            gl_dma16(Abase[t] + (size_t)k0 * akmul, a_go[j], st + (unsigned)((t * A_SL + j * 128 + wp * 64) * 16));
-      };
-#pragma unroll
-      for (int s = 0; s < NSA; ++s) issue(s);
-      gl_wait_tiles<NSA, IA>(min(NSA, ntot) - 1);            // tile 0 landed
-      gl_barrier();                                           // X_-1
-      for (int g = 0; g + 1 < ntot; ++g) {
-        gl_wait_tiles<NSA, IA>(min(g + NSA, ntot) - 2 - g);   // tile g + 1 landed
-        gl_barrier();                                         // X_g
-        issue(g + NSA);
-      }
-    } else {
-      const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) char*)smemW;
-      unsigned b_go[BJ];
-      bool b_hi[BJ];
-#pragma unroll
-      for (int j = 0; j < BJ; ++j) {
-        const int q = j * 128 + wp * 64 + lane, r = q / CPR, pc = q % CPR;
-        bool second;
-        const int wr = brow_index<EPI, BN>(a, tile_n, r, &second);
-        b_go[j] = ((unsigned)wr * (a.w_tiled ? BK : a.ldw) + (pc ^ gl_swz(r)) * 8) * 2;
-        // uniform over the instruction's 64 slots (16 consecutive tile rows)
-        b_hi[j] = __builtin_amdgcn_readfirstlane(second ? 1 : 0) != 0;
-      }
-      const bf16* Wlo = (const bf16*)a.W;
-      const bf16* Whi = (const bf16*)(a.W2 ? a.W2 : a.W);
-      const size_t wkmul = a.w_tiled ? (size_t)a.ldw : 1;
-      auto issue = [&](int g) {
-        if (g >= ntot) return;
-        const int k0 = kbeg + g * BK;
-        const unsigned st = lds0 + (unsigned)((g % NSW) * W_STAGE);
-#pragma unroll
-        for (int j = 0; j < BJ; ++j)
-          gl_dma16((b_hi[j] ? Whi : Wlo) + (size_t)k0 * wkmul, b_go[j], st + (unsigned)((j * 128 + wp * 64) * 16));
-      };
-#pragma unroll
-      for (int s = 0; s < NSW; ++s) issue(s);
-      gl_wait_tiles<NSW, IW>(min(NSW, ntot) - 1);
-      gl_barrier();                                           // X_-1
-      for (int g = 0; g + 1 < ntot; ++g) {
-        gl_wait_tiles<NSW, IW>(min(g + NSW, ntot) - 2 - g);
-        gl_barrier();                                         // X_g
-        issue(g + NSW);
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(GL_VMCNT(0));
-    return;
-  }
-
-  // ---- multiply waves --------------------------------------------------------
-  const int lg = lane >> 4, lc = lane & 15;
-  const int wm = w / WGN, wn = w % WGN;
-  unsigned a_lo[RB], b_lo[CB];
-  int tc[CB];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) tc[cb] = (cb / (CB / 2)) * (BN / 2) + wn * (WN / 2) + (cb % (CB / 2)) * 16 + lc;
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int r = wm * WM + rb * 16 + lc;
-    a_lo[rb] = (unsigned)((r * CPR + (lg ^ gl_swz(r))) * 16);
-  }
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) b_lo[cb] = (unsigned)((tc[cb] * CPR + (lg ^ gl_swz(tc[cb]))) * 16);
-
-  f32x4 acc[RB][CB];
-  f32x4 tot[FOLD ? RB : 1][FOLD ? CB : 1];
-#pragma unroll
-  for (int i = 0; i < RB; ++i)
-#pragma unroll
-    for (int j = 0; j < CB; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if constexpr (FOLD) {
-#pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-      for (int j = 0; j < CB; ++j) tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  bf16x8 fa[2][NA][RB], fb[2][CB];
-  auto read_frags = [&](int g, int buf) {
-    const char* sa = smem + (g % NSA) * A_STAGE;
-    const char* sw = smemW + (g % NSW) * W_STAGE;
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb) fb[buf][cb] = *(const bf16x8*)(sw + b_lo[cb]);
-#pragma unroll
-    for (int t = 0; t < NA; ++t)
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) fa[buf][t][rb] = *(const bf16x8*)(sa + t * A_SL * 16 + a_lo[rb]);
-  };
-  auto mfma_term = [&](int buf, int t) {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb)
-        acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][t][rb], fb[buf][cb], acc[rb][cb], 0, 0, 0);
-  };
-  auto tile_body = [&](int g, int cur) {
-    mfma_term(cur, 0);
-    if (g + 1 < ntot) {
-      __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
-      gl_barrier();                               // X_g
-      read_frags(g + 1, cur ^ 1);
-    }
-    if constexpr (NA == 2) mfma_term(cur, 1);
-    if constexpr (FOLD) {
-      if ((g + 1) % kt_slice == 0) {
-#pragma unroll
-        for (int i = 0; i < RB; ++i)
-#pragma unroll
-          for (int j = 0; j < CB; ++j) {
-            tot[i][j] += acc[i][j];
-            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-          }
-      }
-    }
-  };
-  gl_barrier();                                   // X_-1: tile 0 landed
-  read_frags(0, 0);
-  for (int g = 0; g < ntot; g += 2) {
-    tile_body(g, 0);
-    if (g + 1 < ntot) tile_body(g + 1, 1);
-  }
-
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = m0 + wm * WM + rb * 16 + lg * 4 + i;
-      if (row >= a.M) continue;
-      if constexpr (PARTIAL) {
-        float* pr = a.part + ((size_t)z * a.M + row) * a.N;
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) pr[logical_col<EPI, BN>(a, tile_n, tc[cb])] = acc[rb][cb][i];
-      } else if constexpr (epi_paired(EPI)) {
-#pragma unroll
-        for (int cb = 0; cb < CB / 2; ++cb) {
-          const float v1 = FOLD ? tot[rb % (FOLD ? RB : 1)][cb % (FOLD ? CB : 1)][i] : acc[rb][cb][i];
-          const float v2 = FOLD ? tot[rb % (FOLD ? RB : 1)][(cb + CB / 2) % (FOLD ? CB : 1)][i] : acc[rb][cb + CB / 2][i];
-          epi_tile_pair<EPI, bf16, BN>(a, tile_n, tc[cb], row, v1, v2);
-        }
-      } else {
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) {
-          const int col = tile_n * BN + tc[cb];
-          const float v = FOLD ? tot[rb % (FOLD ? RB : 1)][cb % (FOLD ? CB : 1)][i] : acc[rb][cb][i];
-          if constexpr (EPI == EPI_STORE) epi_store(a, row, col, v);
-          else epi_resid(a, row, col, v);
-        }
-      }
-    }
-  }
-}
-
-template <int BM, int BN, int WGM, int WGN, int NSA, int NSW, int EPI, int MODE>
-void ws_mode(const GemmArgs& a, int grid, hipStream_t st) {
-  if (a.A2) gemm_ws_kernel<BM, BN, WGM, WGN, NSA, NSW, EPI, true, MODE><<<grid, 512, 0, st>>>(a);
-  else gemm_ws_kernel<BM, BN, WGM, WGN, NSA, NSW, EPI, false, MODE><<<grid, 512, 0, st>>>(a);
-}
-
-template <int BM, int BN, int WGM, int WGN, int NSA, int NSW, int EPI>
-void ws_cfg(const GemmArgs& a, bool partial, hipStream_t st) {
-  const int n_tiles = a.N / BN, m_tiles = (a.M + BM - 1) / BM;
-  const int grid = gemm_grid_size(n_tiles, m_tiles, partial ? a.ksplit : 1);
-  if (partial) {
-    ws_mode<BM, BN, WGM, WGN, NSA, NSW, EPI, 2>(a, grid, st);
-    launch_gemm_reduce(EPI, a, st);
-  } else if (a.ksplit > 1) {
-    ws_mode<BM, BN, WGM, WGN, NSA, NSW, EPI, 1>(a, grid, st);
-  } else {
-    ws_mode<BM, BN, WGM, WGN, NSA, NSW, EPI, 0>(a, grid, st);
-  }
-}
-
 template <int BM, int BN, int WGM, int WGN, int NST, int EPI, int MODE>
 void lds_mode(const GemmArgs& a, int grid, hipStream_t st) {
   if (a.A2) gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, true, MODE><<<grid, 512, 0, st>>>(a);
@@ -849,14 +600,7 @@ struct LdsCfg { int BM, BN; };
 const LdsCfg kLds[GEMM_NCFG_LDS] = {
     {128, 192},   // 0: 2 x 2 multiply waves of 64 x 96, 4 stages
     {128, 128},   // 1: 2 x 2 multiply waves of 64 x 64, 4 stages
-    {128, 128},   // 2: as 1 with 6 stages
-    {64, 128},    // 3: 1 x 4 multiply waves of 64 x 32, 6 stages
-    {128, 192},   // 4: as 0 with 5 stages
-    {128, 192},   // 5: decoupled loaders, 3 A stages, 8 weight stages
-    {128, 192},   // 6: decoupled loaders, 4 A stages, 7 weight stages
-    {128, 128},   // 7: decoupled loaders, 4 A stages, 10 weight stages
-    {128, 128},   // 8: decoupled loaders, 3 A stages, 12 weight stages
-    {128, 256},   // 9: 2 x 2 multiply waves of 64 x 128, 4 stages, fragments refilled in place
+    {128, 256},   // 2: 2 x 2 multiply waves of 64 x 128, 4 stages, one K slice, two-term only
 };
 
 template <int EPI>
@@ -864,13 +608,6 @@ void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
   switch (c) {
     case 0: lds_cfg<128, 192, 2, 2, 4, EPI>(a, partial, st); break;
     case 1: lds_cfg<128, 128, 2, 2, 4, EPI>(a, partial, st); break;
-    case 2: lds_cfg<128, 128, 2, 2, 6, EPI>(a, partial, st); break;
-    case 3: lds_cfg<64, 128, 1, 4, 6, EPI>(a, partial, st); break;
-    case 4: lds_cfg<128, 192, 2, 2, 5, EPI>(a, partial, st); break;
-    case 5: ws_cfg<128, 192, 2, 2, 3, 8, EPI>(a, partial, st); break;
-    case 6: ws_cfg<128, 192, 2, 2, 4, 7, EPI>(a, partial, st); break;
-    case 7: ws_cfg<128, 128, 2, 2, 4, 10, EPI>(a, partial, st); break;
-    case 8: ws_cfg<128, 128, 2, 2, 3, 12, EPI>(a, partial, st); break;
     default: {
       // one K slice, two-term activations only (the in-place refill needs both terms)
       const int grid = gemm_grid_size(a.N / 256, (a.M + 127) / 128, 1);
@@ -885,7 +622,7 @@ void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
 int gemm_stats_bn(const GemmArgs& a) {
   // the configurations whose kernel is gemm_lds_kernel with a 2 x 2 wave grid
   const int cfg = gemm_pick_cfg(a, EPI_STORE) - GEMM_NCFG;
-  if ((cfg != 0 && cfg != 1 && cfg != 9) || a.ksplit != 1 || !gemm_lds_cfg_ok(cfg, a)) return 0;
+  if (cfg < 0 || a.ksplit != 1 || !gemm_lds_cfg_ok(cfg, a)) return 0;
   return kLds[cfg].BN;
 }
 
@@ -893,7 +630,7 @@ bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
   if (c < 0 || c >= GEMM_NCFG_LDS) return false;
   const LdsCfg& k = kLds[c];
   if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * BK)) return false;
-  if (c == 9 && (!a.A2 || a.ksplit != 1)) return false;
+  if (c == 2 && (!a.A2 || a.ksplit != 1)) return false;
   // 32-bit lane offsets
   if ((size_t)a.N * (a.w_tiled ? BK : a.ldw) * 2 >= (1ull << 32) || (size_t)a.M * (a.a_tiled ? BK : a.lda) * 2 >= (1ull << 32))
     return false;

@@ -110,7 +110,7 @@ void launch_read_act(const void* hi, const void* lo, int n, int d, int ld, int t
 // GEMM_NCFG .. GEMM_NCFG+GEMM_NCFG_LDS-1: direct-to-LDS multistage kernel
 // (gemm_lds.hip).  All give the same bits for the same (N, K) split.
 constexpr int GEMM_NCFG = 7;
-constexpr int GEMM_NCFG_LDS = 10;
+constexpr int GEMM_NCFG_LDS = 3;
 int gemm_ksplit(int N, int K, int rows);
 bool gemm_lds_cfg_ok(int c, const GemmArgs& a);
 int gemm_lds_tiles(int c, const GemmArgs& a);
