@@ -311,7 +311,7 @@ def main():
         sweep(args.sweep)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               f"(asked for --gpus {args.gpus}); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
