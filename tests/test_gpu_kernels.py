@@ -38,10 +38,14 @@ def test_gemm_f32_matches_oracle(M, N, K):
     np.testing.assert_allclose(Y, on.linear(A64, W64), rtol=0, atol=1e-4)
 
 
-@pytest.mark.parametrize("M,N,K", [(37, 192, 320), (256, 512, 4096), (300, 65536, 256)])
+@pytest.mark.parametrize("M,N,K", [(37, 192, 320), (256, 512, 4096), (300, 65536, 256), (3900, 4096, 256),
+                                   (2600, 4608, 192)])
 def test_gemm_two_term_activation_matches_oracle(M, N, K):
     """A = hi + lo (bf16 pair of an fp32 activation) against the unrounded activation; N 65536
-    runs the 128 x 256 tiles (enough column tiles), with a ragged last row tile."""
+    runs the 128 x 256 tiles (enough column tiles), with a ragged last row tile.  3900 x 4096
+    (16 column tiles of 256, 31 row tiles) and 2600 x 4608 (24 column tiles of 192, 21 row
+    tiles) have few column tiles and many row tiles, so their row tiles are split over 4 and 2
+    XCDs per column-tile set, in shares of unequal size."""
     say(f"gemm two-term bf16 M={M} N={N} K={K}")
     a = archer()
     import torch
