@@ -7,6 +7,7 @@
 * on the GPU, CachedForward on the cache of the same response equals
   FullForward bitwise, and a sequence's logits do not depend on the batch;
 * a ragged batch with per-sequence refresh (seq_sel);
+* the largest batch (64 sequences) with a one-token prompt;
 * the k-block weight layout: the pack kernel is the stated permutation, and a
   model gives the same bits in either layout (bf16 contexts use the k-block
   layout unless a test says otherwise, as the bench does);
@@ -164,6 +165,36 @@ def test_ragged_batch_per_sequence_refresh_and_batch_invariance():
     assert np.all(lz[1] == 3.0)
     np.testing.assert_array_equal(lz[0], zc[0])
     np.testing.assert_array_equal(lz[2], zc[2])
+
+
+def test_maximum_batch_of_64_with_one_token_prompt():
+    """The largest batch the library takes (64 sequences), prompts of 1 to 90 tokens (the
+    first sequence's prompt is a single token, whose 64-key cache tile holds one real key):
+    FullForward and CachedForward against the oracle for the shortest, a middle and the longest
+    sequence, and the one-token sequence alone in a context of the same limits gives the
+    same bits."""
+    m = SMALL_BF16["gqa_hd64"]
+    B, G = 64, 16
+    lens = [1 + (b * 37) % 90 for b in range(B)]
+    say(f"maximum batch bf16: B {B}, prompts {min(lens)}..{max(lens)} (total {sum(lens)}), G {G}")
+    W = with_gains(model_weights(m, seed=9), 9)
+    ps = [_prompt(m, n, 300 + b) for b, n in enumerate(lens)]
+    ctx = make_ctx(m, W, B, max(lens), sum(lens), G)
+    g = [_resp(m, G, 400 + b) for b in range(B)]
+    z = host(ctx.refresh_prompt(dev_i32(np.concatenate(ps)), lens, dev_i32(np.stack(g))))
+    g2 = [_resp(m, G, 500 + b, frac=0.5) for b in range(B)]
+    zc = host(ctx.step(dev_i32(np.stack(g2))))
+    for b in (0, B // 2, int(np.argmax(lens))):
+        zr, cache, _ = om.full_forward(W, m, ps[b], g[b])
+        zcr, _ = om.cached_forward(W, m, g2[b], cache, lens[b])
+        e_full, e_cached = np.max(np.abs(z[b] - zr)), np.max(np.abs(zc[b] - zcr))
+        say(f"  sequence {b} (P {lens[b]}): full {e_full:.3e}, cached {e_cached:.3e}")
+        assert e_full < 2e-2 and e_cached < 2e-2, b
+    solo = make_ctx(m, W, B, max(lens), sum(lens), G)
+    z0 = host(solo.refresh_prompt(dev_i32(ps[0]), [lens[0]], dev_i32(g[0][None])))[0]
+    np.testing.assert_array_equal(z0, z[0])
+    z0c = host(solo.step(dev_i32(g2[0][None])))[0]
+    np.testing.assert_array_equal(z0c, zc[0])
 
 
 def test_full_width_two_layer_llada_shape():
