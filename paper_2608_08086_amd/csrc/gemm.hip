@@ -471,8 +471,14 @@ int gemm_ksplit(int N, int K, int rows) {
   // within the K granularity.  The count is fixed per context (rows is the
   // context's response-row capacity), never per launch, so every pass of a
   // context sums every output in the same order.
+  // A 256-row launch that already has three quarters of a round of 128 x 128
+  // tiles (N >= 12288) also takes one slice: measured on the LLaDA-8B QKV
+  // projection, one slice is as fast as two at 256 rows (128 x 128 tiles)
+  // and 17 % faster in a 4352-row refresh pass (128 x 256 tiles, no partial
+  // planes or reduction).
   if (rows >= 2048) return 1;
   const int tiles = 2 * std::max(N / 128, 1);
+  if (tiles >= 192) return 1;
   int S = 1;
   while (S < 8 && tiles * S < 256 && K % (2 * S * 64) == 0) S *= 2;
   return S;
@@ -485,23 +491,32 @@ int gemm_pick_cfg(const GemmArgs& a, int epi) {
   // round of 256 workgroups; QKV), else with 128 x 128 tiles.  The 128 x 192
   // tile is not used for slices folded in one workgroup (its second
   // accumulator set does not fit the registers of two waves per SIMD).
-  // 128 x 256 tiles (64 x 128 wave tiles: fewer LDS bytes per MFMA) for
-  // two-term launches of one K slice, where they take fewer rounds of 256
-  // workgroups (one per CU) times the time of a tile: measured on the LLaDA-8B
-  // projections, a 128 x 192 tile takes 1.5x and a 128 x 256 tile 1.77x the
-  // time of a 128 x 128 tile.  The LM head decides on N alone, so that the
+  // Two-term launches of one K slice take the tile (128 x 256: 64 x 128 wave
+  // tiles, fewer LDS bytes per MFMA; 128 x 192; 128 x 128) with the fewest
+  // rounds of 256 workgroups (one per CU) times the time of a tile: measured
+  // on the LLaDA-8B projections, a 128 x 192 tile takes 1.5x and a 128 x 256
+  // tile 1.77x the time of a 128 x 128 tile.  The LM head decides on N alone, so that the
   // column tile of its fused decision statistics does not depend on the row
   // count of a pass.
-  if (a.A2 && a.ksplit == 1 && a.N % 256 == 0 && gemm_lds_cfg_ok(2, a)) {
-    bool wide;
-    if (epi == EPI_STORE) {
-      wide = a.N / 256 >= 256;
-    } else {
-      const long mt = (a.M + 127) / 128;
-      const auto cost = [&](int bn, double t) { return (double)((a.N / bn * mt + 255) / 256) * t; };
-      wide = cost(256, 1.77) < (a.N % 192 == 0 ? cost(192, 1.5) : cost(128, 1.0));
+  if (a.A2 && a.ksplit == 1 && epi == EPI_STORE) {
+    if (a.N % 256 == 0 && a.N / 256 >= 256 && gemm_lds_cfg_ok(2, a)) return GEMM_NCFG + 2;
+  } else if (a.A2 && a.ksplit == 1) {
+    // the tile with the fewest rounds times tile time; a narrower tile must
+    // be 5 % cheaper than a wider one to be taken
+    const long mt = (a.M + 127) / 128;
+    const auto cost = [&](int bn, double t) { return (double)((a.N / bn * mt + 255) / 256) * t; };
+    int best = -1;
+    double bc = 0;
+    if (a.N % 256 == 0 && gemm_lds_cfg_ok(2, a)) { best = 2; bc = cost(256, 1.77); }
+    if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a) && (best < 0 || cost(192, 1.5) < 0.95 * bc)) {
+      best = 0;
+      bc = cost(192, 1.5);
     }
-    if (wide) return GEMM_NCFG + 2;
+    if (a.N % 128 == 0 && gemm_lds_cfg_ok(1, a) && (best < 0 || cost(128, 1.0) < 0.95 * bc)) {
+      best = 1;
+      bc = cost(128, 1.0);
+    }
+    if (best >= 0) return GEMM_NCFG + best;
   }
   if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a)) {
     const bool fold = a.ksplit > 1 && !(a.part && gemm_partial_wanted(GEMM_NCFG + 0, a));
