@@ -485,19 +485,19 @@ int gemm_ksplit(int N, int K, int rows) {
 }
 
 int gemm_pick_cfg(const GemmArgs& a, int epi) {
-  // Measured on MI355X (LLaDA-8B cached step M = 256 and refresh M = 768,
-  // two-term activations): the warp-specialised direct-to-LDS kernel with
-  // 128 x 192 tiles when N is a multiple of 192 (gate/up: 128 column tiles, one
-  // round of 256 workgroups; QKV), else with 128 x 128 tiles.  The 128 x 192
-  // tile is not used for slices folded in one workgroup (its second
-  // accumulator set does not fit the registers of two waves per SIMD).
-  // Two-term launches of one K slice take the tile (128 x 256: 64 x 128 wave
-  // tiles, fewer LDS bytes per MFMA; 128 x 192; 128 x 128) with the fewest
-  // rounds of 256 workgroups (one per CU) times the time of a tile: measured
-  // on the LLaDA-8B projections, a 128 x 192 tile takes 1.5x and a 128 x 256
-  // tile 1.77x the time of a 128 x 128 tile.  The LM head decides on N alone, so that the
-  // column tile of its fused decision statistics does not depend on the row
-  // count of a pass.
+  // The warp-specialised direct-to-LDS kernel (gemm_lds.hip).  Two-term
+  // launches of one K slice take the tile (128 x 256: 64 x 128 wave tiles,
+  // fewer LDS bytes per MFMA; 128 x 192; 128 x 128) with the fewest rounds of
+  // 256 workgroups (one per CU) times the time of a tile: measured on the
+  // LLaDA-8B projections, a 128 x 192 tile takes 1.5x and a 128 x 256 tile
+  // 1.77x the time of a 128 x 128 tile (so, for example, 256-row gate/up
+  // passes take 128 x 192 tiles, one round, and 256-row QKV passes 128 x 128
+  // tiles).  The LM head decides on N alone, so that the column tile of its
+  // fused decision statistics does not depend on the row count of a pass.
+  // Split-K launches take 128 x 192 tiles when N is a multiple of 192, else
+  // 128 x 128; the 128 x 192 tile is not used for slices folded in one
+  // workgroup (its second accumulator set does not fit the registers of two
+  // waves per SIMD).
   if (a.A2 && a.ksplit == 1 && epi == EPI_STORE) {
     if (a.N % 256 == 0 && a.N / 256 >= 256 && gemm_lds_cfg_ok(2, a)) return GEMM_NCFG + 2;
   } else if (a.A2 && a.ksplit == 1) {
