@@ -551,7 +551,7 @@ int attn_nsplit_for_keys(int nkeys) {
 bool attn_split_wanted(const int* rows, int n, int hq) {
   long wgs = 0;
   for (int s = 0; s < n; ++s) wgs += (long)((rows[s] + 255) / 256) * hq;
-  return wgs < ATTN_MIN_WGS;
+  return 4 * wgs < 3 * ATTN_MIN_WGS;
 }
 
 int attn_split_rows_max(int hq) { return 256 * ((ATTN_MIN_WGS + hq - 1) / hq); }

@@ -64,9 +64,11 @@ constexpr int ATTN_TILES_PER_SPLIT = 8;    // 64-key tiles per split (target)
 constexpr int ATTN_MIN_WGS = 256;          // workgroups wanted per pass (one per CU)
 int attn_qt_bf16(const int* rows, const int* nsplit, int n, int hq);
 // Split-KV only for passes short of workgroups: false when the pass's 256-row
-// query tiles alone give ATTN_MIN_WGS workgroups (a split would only add
-// partial-result traffic).  A split pass therefore has fewer than
-// attn_split_rows_max(hq) rows (sizes the partial buffers).
+// query tiles alone give three quarters of ATTN_MIN_WGS workgroups (a split
+// would only add partial-result traffic and a merge; measured on the
+// Dream-7B-shaped cached pass, 224 workgroups unsplit take 67 us against
+// 101 us for three splits with the merge).  A split pass therefore has fewer
+// than attn_split_rows_max(hq) rows (sizes the partial buffers).
 bool attn_split_wanted(const int* rows, int n, int hq);
 int attn_split_rows_max(int hq);
 constexpr int ATTN_QT_F32 = 1;

@@ -44,8 +44,8 @@ def test_noalloc_attention_equals_the_workspace_call():
 
 def test_noalloc_attention_refuses_shapes_beyond_the_scratch():
     a = archer()
-    # 7 query tiles x 32 heads still split: 8 x 32 x 1792 x 128 fp32 partials = 235 MB > 64 MiB
-    args = _inputs(1792, 32, 32, 128, 4096, 256, 50)
+    # 5 query tiles x 32 heads still split: 4 x 32 x 1280 x 128 fp32 partials = 84 MB > 64 MiB
+    args = _inputs(1280, 32, 32, 128, 4096, 256, 50)
     with pytest.raises(a.ArcherError) as e:
         a.op_attention_noalloc(*args)
     assert e.value.status == a.E_SHAPE
