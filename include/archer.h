@@ -47,7 +47,9 @@ typedef enum {
   ARCHER_E_UNSUPPORTED = -6   /* model shape outside what the kernels implement       */
 } archer_status;
 
-typedef enum { ARCHER_BF16 = 0, ARCHER_FP32 = 1 } archer_dtype;
+/* ARCHER_FP16 is no model dtype: it is the element type of w_gate and w_up
+ * in bf16 models with gateup_fp16 set (and an archer_pack_weight dtype). */
+typedef enum { ARCHER_BF16 = 0, ARCHER_FP32 = 1, ARCHER_FP16 = 2 } archer_dtype;
 
 /* Refresh rules of the cache controller.
  * HAMMING: refresh when D_t = d_H(g_t, g_r) >= K (Sec. 4.2 Eq. archer-distance and
@@ -67,6 +69,14 @@ typedef struct {
   int32_t dtype;              /* archer_dtype of weights and activations; ARCHER_BF16
                                  models store queries, keys and values (and so the
                                  prompt cache) as fp16, ARCHER_FP32 models as fp32 */
+  int32_t gateup_fp16;        /* ARCHER_BF16 only (else ARCHER_E_UNSUPPORTED).  Nonzero:
+                                 the gate/up projection multiplies single fp16 operands
+                                 (one fp16 MFMA per fragment, half the matrix work of
+                                 the two-term bf16 form): its input, the normalised MLP
+                                 input, is stored as one fp16 rounding, and w_gate and
+                                 w_up are fp16 matrices (the bf16 weights converted,
+                                 exact for magnitudes in [2^-14, 65504]).  Zero: that
+                                 input is two-term bf16 and w_gate, w_up are bf16. */
 } archer_model_cfg;
 
 /* Layouts of the projection matrices (lm_head, w_qkv, w_o, w_gate, w_up,
@@ -78,7 +88,8 @@ typedef struct {
  * row-major. */
 typedef enum { ARCHER_LAYOUT_ROWMAJOR = 0, ARCHER_LAYOUT_KBLOCK = 1 } archer_weight_layout;
 
-/* Weights [out][in] in `layout`, element type = cfg.dtype; norm gains fp32.
+/* Weights [out][in] in `layout`, element type = cfg.dtype (w_gate and w_up:
+ * fp16 when cfg.gateup_fp16 is set); norm gains fp32.
  * Every pointer is a device pointer; the per-layer fields are HOST arrays of
  * n_layers device pointers.  Weights must outlive the context.  A zeroed
  * `layout` is row-major.                                                   */
@@ -149,9 +160,10 @@ size_t archer_workspace_bytes(const archer_model_cfg *cfg, const archer_limits *
 
 /* Layout helper (no operation of the method; the model is the same in
  * either layout and the results are bitwise the same): copy the row-major
- * bf16 matrix src [rows][cols] into dst in the KBLOCK layout.  Device
- * pointers, 16-byte aligned, not overlapping; rows >= 1, cols a positive
- * multiple of 32; dtype must be ARCHER_BF16 (else ARCHER_E_UNSUPPORTED).
+ * bf16 (or fp16) matrix src [rows][cols] into dst in the KBLOCK layout.
+ * Device pointers, 16-byte aligned, not overlapping; rows >= 1, cols a
+ * positive multiple of 32; dtype must be ARCHER_BF16 or ARCHER_FP16 (else
+ * ARCHER_E_UNSUPPORTED).
  * Enqueued on hip_stream (NULL = default stream); does not synchronise. */
 archer_status archer_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void *src, void *dst,
                                  void *hip_stream);

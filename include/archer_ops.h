@@ -134,7 +134,8 @@ archer_status archer_read_state(archer_ctx *ctx, int32_t what, int32_t layer, in
  * class's producer store and its GEMM read the single bf16 rounding hi = bf16(v)
  * instead (half the MFMA work of that projection).  Applies to forwards
  * enqueued after the call.  ARCHER_E_ARG for other bits, ARCHER_E_UNSUPPORTED
- * for a nonzero mask on an fp32 model. */
+ * for a nonzero mask on an fp32 model and for _GATEUP on a model with
+ * gateup_fp16 (whose gate/up operands are single fp16 values already). */
 archer_status archer_set_single_term(archer_ctx *ctx, uint32_t class_mask);
 
 #ifdef __cplusplus

@@ -32,7 +32,11 @@ output, "gateup": the normalised MLP input, "down": the SwiGLU product,
 "head": the final normalised hidden state) as a single bf16 value.  The bf16
 path carries the other activations, and the attention probabilities, at 16
 or more significant bits, so the oracle keeps those unrounded; the residual
-stream and the logits are not rounded either.  fp32 models round nowhere.
+stream and the logits are not rounded either.  With ``m.gateup_fp16`` the
+gate/up projection multiplies single fp16 operands: its input (the
+normalised MLP input) and its two weight matrices are each rounded to fp16
+(for the weights, bf16 values, this is exact unless a magnitude lies below
+2^-14).  fp32 models round nowhere.
 """
 
 from __future__ import annotations
@@ -47,10 +51,22 @@ def _qkv_store(m, x):
     return round_fp16(x) if m.dtype == "bf16" else x
 
 
+def _gateup_fp16(m) -> bool:
+    return m.dtype == "bf16" and bool(getattr(m, "gateup_fp16", False))
+
+
 def _operand(m, name, x):
-    """Activation operand of projection ``name``: single bf16 where the model says so."""
+    """Activation operand of projection ``name``: single bf16 where the model says
+    so, a single fp16 value for gate/up under ``gateup_fp16``."""
+    if name == "gateup" and _gateup_fp16(m):
+        return round_fp16(x)
     single = m.dtype == "bf16" and name in getattr(m, "single_term", ())
     return round_bf16(x) if single else x
+
+
+def _gateup_weight(m, w):
+    """A gate or up matrix as the path multiplies it (fp16 under ``gateup_fp16``)."""
+    return round_fp16(weights_f64(w)) if _gateup_fp16(m) else w
 
 
 def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
@@ -105,8 +121,8 @@ def transformer(W: dict, m, tokens: np.ndarray, positions: np.ndarray,
         x = x + linear(o, Wl["w_o"])
         # SwiGLU MLP block
         b = _operand(m, "gateup", rms_norm(x, Wl["mlp_norm"], m.rms_eps))
-        gate = linear(b, Wl["w_gate"])
-        up = linear(b, Wl["w_up"])
+        gate = linear(b, _gateup_weight(m, Wl["w_gate"]))
+        up = linear(b, _gateup_weight(m, Wl["w_up"]))
         hmid = _operand(m, "down", silu(gate) * up)
         x = x + linear(hmid, Wl["w_down"])
         if keep_hidden:

@@ -21,7 +21,7 @@ if not os.path.exists(_LIB_PATH):
 lib = C.CDLL(_LIB_PATH)
 
 OK, E_ARG, E_SHAPE, E_STATE, E_HIP, E_WORKSPACE, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
-BF16, FP32 = 0, 1
+BF16, FP32, FP16 = 0, 1, 2
 HAMMING, AGE, ALWAYS = 0, 1, 2
 LAYOUT_ROWMAJOR, LAYOUT_KBLOCK = 0, 1
 NEVER = 2**31 - 1
@@ -50,7 +50,7 @@ class ModelCfg(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ff", C.c_int32),
                 ("vocab", C.c_int32), ("mask_id", C.c_int32), ("rms_eps", C.c_float),
-                ("rope_theta", C.c_float), ("dtype", C.c_int32)]
+                ("rope_theta", C.c_float), ("dtype", C.c_int32), ("gateup_fp16", C.c_int32)]
 
 
 class Weights(C.Structure):
@@ -176,8 +176,15 @@ class Context:
                  resp_len: int):
         self.shape = shape
         self.dtype = BF16 if shape.dtype == "bf16" else FP32
+        gu16 = int(bool(getattr(shape, "gateup_fp16", False)))
         self.cfg = ModelCfg(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
-                            shape.d_ff, shape.vocab, shape.mask_id, shape.rms_eps, shape.rope_theta, self.dtype)
+                            shape.d_ff, shape.vocab, shape.mask_id, shape.rms_eps, shape.rope_theta, self.dtype,
+                            gu16)
+        want = torch.float16 if gu16 else torch_dtype(self.dtype)
+        for L_ in weights["layers"]:
+            for k in ("w_gate", "w_up"):
+                if L_[k].dtype != want:
+                    raise ArcherError(E_ARG, f"{k} must be {want} for this model (gateup_fp16={gu16})")
         self.lim = Limits(max_batch, max_prompt_len, max_prompt_total, resp_len)
         self.G = resp_len
         self.V = shape.vocab
@@ -365,8 +372,10 @@ class Context:
         return {K_NAMES[i]: dict(launches=n[i], ms=ms[i], bytes=by[i], flops=fl[i]) for i in range(K_COUNT)}
 
 
-def upload_weights(W: dict, dtype: str) -> dict:
-    """Host weights (synth layout: uint16 bf16 bits or float32) -> contiguous CUDA tensors."""
+def upload_weights(W: dict, dtype: str, gateup_fp16: bool = False) -> dict:
+    """Host weights (synth layout: uint16 bf16 bits or float32) -> contiguous CUDA tensors.
+    gateup_fp16 (bf16 models): w_gate and w_up are converted to fp16, the element type a
+    model with gateup_fp16 takes for them."""
     def dev(a):
         if a.dtype.name == "uint16":
             t = torch.from_numpy(a.view("int16")).view(torch.bfloat16)
@@ -374,8 +383,12 @@ def upload_weights(W: dict, dtype: str) -> dict:
             t = torch.from_numpy(a)
         return t.to("cuda").contiguous()
 
+    def dev_layer(k, v):
+        t = dev(v)
+        return t.to(torch.float16) if gateup_fp16 and dtype == "bf16" and k in ("w_gate", "w_up") else t
+
     out = {k: dev(W[k]) for k in ("tok_emb", "lm_head", "final_norm")}
-    out["layers"] = [{k: dev(v) for k, v in L.items()} for L in W["layers"]]
+    out["layers"] = [{k: dev_layer(k, v) for k, v in L.items()} for L in W["layers"]]
     return out
 
 
@@ -383,10 +396,12 @@ PROJECTIONS = ("w_qkv", "w_o", "w_gate", "w_up", "w_down")
 
 
 def pack_weight(w):
-    """Row-major bf16 [rows][cols] CUDA tensor -> a new tensor in the k-block layout (archer_pack_weight)."""
-    assert w.dtype == torch.bfloat16 and w.dim() == 2
+    """Row-major bf16 or fp16 [rows][cols] CUDA tensor -> a new tensor in the k-block layout
+    (archer_pack_weight)."""
+    assert w.dtype in (torch.bfloat16, torch.float16) and w.dim() == 2
     out = torch.empty_like(w)
-    _check(lib.archer_pack_weight(BF16, w.shape[0], w.shape[1], _ptr(w), _ptr(out), _stream()))
+    dt = BF16 if w.dtype == torch.bfloat16 else FP16
+    _check(lib.archer_pack_weight(dt, w.shape[0], w.shape[1], _ptr(w), _ptr(out), _stream()))
     return out
 
 

@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <type_traits>
 
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -82,15 +83,16 @@ __device__ __forceinline__ void store_act(T* hi, T* lo, size_t i, float v) {
 template <class T>
 __device__ __forceinline__ void store_act4(T* hi, T* lo, size_t i, float v0, float v1, float v2, float v3) {
   if constexpr (sizeof(T) == 2) {
+    using V4 = std::conditional_t<std::is_same_v<T, f16>, f16x4, bf16x4>;
     const float v[4] = {v0, v1, v2, v3};
-    bf16x4 h, l;
+    V4 h, l;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       h[e] = from_f32<T>(v[e]);
       l[e] = from_f32<T>(v[e] - to_f32((T)h[e]));
     }
-    *(bf16x4*)(hi + i) = h;
-    if (lo) *(bf16x4*)(lo + i) = l;
+    *(V4*)(hi + i) = h;
+    if (lo) *(V4*)(lo + i) = l;
   } else {
     store_act<T>(hi, lo, i + 0, v0);
     store_act<T>(hi, lo, i + 1, v1);

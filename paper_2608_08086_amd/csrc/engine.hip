@@ -61,6 +61,7 @@ std::string check_cfg(const archer_model_cfg* c, const archer_limits* l) {
   if (c->d_model % 64 || c->d_ff % 64 || c->vocab % 64) return "d_model, d_ff and vocab must be multiples of 64";
   if (c->mask_id < 0 || c->mask_id >= c->vocab) return "mask_id outside the vocabulary";
   if (c->dtype != ARCHER_BF16 && c->dtype != ARCHER_FP32) return "dtype must be ARCHER_BF16 or ARCHER_FP32";
+  if (c->gateup_fp16 && c->dtype != ARCHER_BF16) return "gateup_fp16 is a bf16-model option";
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 1.f)) return "rms_eps must be > 0 and rope_theta > 1";
   if (l->max_batch < 1 || l->max_batch > ARCHER_MAXB) return "max_batch must be in [1, 64]";
   if (l->max_prompt_len < 1 || l->max_prompt_total < l->max_prompt_len) return "bad prompt limits";
@@ -328,7 +329,9 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   const uint32_t sm = c->single_mask;
   auto lo_for = [&](int cls, size_t off) -> void* { return ((sm >> cls) & 1u) ? nullptr : lo_part(c, off); };
   void* act2_qkv = lo_for(ARCHER_K_GEMM_QKV, L.act2);
-  void* act2_mlp = lo_for(ARCHER_K_GEMM_GATEUP, L.act2);
+  // gate/up with fp16 operands: its input is a single fp16 value
+  const bool mlp16 = is_bf16(c) && m.gateup_fp16;
+  void* act2_mlp = mlp16 ? nullptr : lo_for(ARCHER_K_GEMM_GATEUP, L.act2);
   void* o2 = lo_for(ARCHER_K_GEMM_O, L.O2);
   void* h2 = lo_for(ARCHER_K_GEMM_DOWN, L.H2);
   void* cn2 = lo_for(ARCHER_K_GEMM_HEAD, L.Cn2);
@@ -350,9 +353,12 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
   // bf16 activations that feed a projection GEMM are stored k-block-major
   // with the buffer's row capacity as ld (act, O, H: Mmax rows; Cn: Rmax)
   const int tiled = is_bf16(c) ? 1 : 0;
-  auto norm = [&](const float* gain, int gather, int nrows, void* out, void* out2, int cap) {
+  auto norm = [&](const float* gain, int gather, int nrows, void* out, void* out2, int cap, bool half = false) {
     return timed(c, ARCHER_K_NORM, (double)nrows * d * (4 + es * (out2 ? 2 : 1)), 0.0, [&] {
-      if (is_bf16(c))
+      if (half)
+        launch_rmsnorm<f16>(*P, gather, nrows, x, gain, out, nullptr, cap, 1, d, m.rms_eps, c->at<int>(L.out_row),
+                            c->stream);
+      else if (is_bf16(c))
         launch_rmsnorm<bf16>(*P, gather, nrows, x, gain, out, out2, cap, 1, d, m.rms_eps, c->at<int>(L.out_row),
                              c->stream);
       else
@@ -372,9 +378,10 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
 
   // RMSNorms whose input is the residual just updated by a split-K GEMM run
   // inside that GEMM's reduction (same arithmetic as the stand-alone kernel)
-  auto fuse_norm = [&](GemmArgs& a, const float* gain, void* out2) {
+  auto fuse_norm = [&](GemmArgs& a, const float* gain, void* out2, bool half = false) {
     if (!is_bf16(c)) return;
     a.ngain = gain; a.nout = act; a.nout2 = out2; a.neps = m.rms_eps; a.nld = L.Mmax; a.ntiled = 1;
+    a.nf16 = half ? 1 : 0;
   };
   bool normed = false;   // attn_norm of the current layer already applied
   for (int l = 0; l < m.n_layers; ++l) {
@@ -427,15 +434,15 @@ archer_status run_forward(archer_ctx* c, bool full, const std::vector<int>& sel,
                          d, hq * hd);
       a.A2 = o2; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
       a.X = x; a.ldx = d;
-      fuse_norm(a, c->mlp_norm[l], act2_mlp);
+      fuse_norm(a, c->mlp_norm[l], act2_mlp, mlp16);
       if ((st = gemm(c, full ? ARCHER_K_GEMM_O_FULL : ARCHER_K_GEMM_O, EPI_RESID, a))) return st;
       normed = gemm_fuses_norm(a);
     }
-    if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2_mlp, L.Mmax))) return st;
+    if (!normed && (st = norm(c->mlp_norm[l], 0, rows, act, act2_mlp, L.Mmax, mlp16))) return st;
     normed = false;
     {
       GemmArgs a = gargs(act, tiled ? L.Mmax : d, c->w_gate[l], c->w_tiled ? F : d, rows, 2 * F, d);
-      a.A2 = act2_mlp; a.a_tiled = tiled; a.w_tiled = c->w_tiled;
+      a.A2 = act2_mlp; a.a_tiled = tiled; a.w_tiled = c->w_tiled; a.f16 = mlp16 ? 1 : 0;
       a.W2 = c->w_up[l];
       a.H = c->at<char>(L.H); a.H2 = h2; a.ldh = tiled ? L.Mmax : F; a.h_tiled = tiled;
       if ((st = gemm(c, full ? ARCHER_K_GEMM_GATEUP_FULL : ARCHER_K_GEMM_GATEUP, EPI_SWIGLU, a))) return st;
@@ -987,6 +994,8 @@ archer_status archer_set_single_term(archer_ctx* c, uint32_t class_mask) {
                            (1u << ARCHER_K_GEMM_DOWN) | (1u << ARCHER_K_GEMM_HEAD);
   if (class_mask & ~allowed) return fail(ARCHER_E_ARG, "class_mask names a class that is not a projection");
   if (class_mask && !is_bf16(c)) return fail(ARCHER_E_UNSUPPORTED, "single-term activations are a bf16 option");
+  if (((class_mask >> ARCHER_K_GEMM_GATEUP) & 1u) && c->cfg.gateup_fp16)
+    return fail(ARCHER_E_UNSUPPORTED, "gate/up of this model multiplies single fp16 operands already");
   c->single_mask = class_mask;
   return ARCHER_OK;
 }
@@ -1045,7 +1054,8 @@ archer_status archer_timing_end(archer_ctx* c, int64_t* launches, double* total_
 // ---------------------------------------------------------------------------
 archer_status archer_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void* src, void* dst,
                                  void* hip_stream) {
-  if (dtype != ARCHER_BF16) return fail(ARCHER_E_UNSUPPORTED, "the k-block weight layout is bf16 only");
+  if (dtype != ARCHER_BF16 && dtype != ARCHER_FP16)
+    return fail(ARCHER_E_UNSUPPORTED, "the k-block weight layout holds bf16 or fp16 matrices");
   if (!src || !dst) return fail(ARCHER_E_ARG, "null src or dst");
   if (((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return fail(ARCHER_E_ARG, "src and dst must be 16-byte aligned");
   if (rows < 1 || cols < 32 || cols % 32) return fail(ARCHER_E_SHAPE, "need rows >= 1 and cols a multiple of 32");

@@ -395,8 +395,13 @@ template <int EPI>
 static void reduce_epi(const GemmArgs& a, hipStream_t st) {
   if constexpr (EPI == EPI_RESID) {
     if (a.ngain) {
-      if (a.N <= 8 * NORM_THREADS) gemm_reduce_resid_norm_kernel<bf16, 2><<<a.M, NORM_THREADS, 0, st>>>(a);
-      else gemm_reduce_resid_norm_kernel<bf16, 4><<<a.M, NORM_THREADS, 0, st>>>(a);
+      if (a.nf16) {
+        if (a.N <= 8 * NORM_THREADS) gemm_reduce_resid_norm_kernel<f16, 2><<<a.M, NORM_THREADS, 0, st>>>(a);
+        else gemm_reduce_resid_norm_kernel<f16, 4><<<a.M, NORM_THREADS, 0, st>>>(a);
+      } else {
+        if (a.N <= 8 * NORM_THREADS) gemm_reduce_resid_norm_kernel<bf16, 2><<<a.M, NORM_THREADS, 0, st>>>(a);
+        else gemm_reduce_resid_norm_kernel<bf16, 4><<<a.M, NORM_THREADS, 0, st>>>(a);
+      }
       return;
     }
   }
@@ -498,9 +503,12 @@ int gemm_pick_cfg(const GemmArgs& a, int epi) {
   // 128 x 128; the 128 x 192 tile is not used for slices folded in one
   // workgroup (its second accumulator set does not fit the registers of two
   // waves per SIMD).
-  if (a.A2 && a.ksplit == 1 && epi == EPI_STORE) {
+  // Single-term fp16 launches choose like two-term ones (their tiles are
+  // timed in the same ratios).
+  const bool wide = (a.A2 || a.f16) && a.ksplit == 1;
+  if (wide && epi == EPI_STORE) {
     if (a.N % 256 == 0 && a.N / 256 >= 256 && gemm_lds_cfg_ok(2, a)) return GEMM_NCFG + 2;
-  } else if (a.A2 && a.ksplit == 1) {
+  } else if (wide) {
     // the tile with the fewest rounds times tile time; a narrower tile must
     // be 5 % cheaper than a wider one to be taken
     const long mt = (a.M + 127) / 128;
@@ -554,6 +562,7 @@ int gemm_partial_wanted(int cfg, const GemmArgs& a) {
 
 bool gemm_args_ok(int epi, const GemmArgs& a) {
   if (!a.A || !a.W || a.M <= 0 || a.N <= 0 || a.K <= 0 || a.ksplit < 1) return false;
+  if (a.f16 && (epi != EPI_SWIGLU || a.A2)) return false;   // fp16 operands: single-term gate/up only
   switch (epi) {
     case EPI_STORE: return (a.C && a.ldc >= a.N) || (a.tstat && a.targ && a.zg && a.tg);
     case EPI_RESID: return a.X && a.ldx >= a.N;
@@ -569,7 +578,7 @@ bool gemm_args_ok(int epi, const GemmArgs& a) {
 int launch_gemm_bf16_cfg(int epi, int cfg, bool partial, const GemmArgs& a, hipStream_t st) {
   if (!gemm_args_ok(epi, a)) return 1;
   if (cfg >= GEMM_NCFG) return launch_gemm_lds_cfg(epi, cfg - GEMM_NCFG, partial, a, st);
-  if (!gemm_cfg_ok(cfg, a, epi)) return 1;
+  if (a.f16 || !gemm_cfg_ok(cfg, a, epi)) return 1;   // the register-staged kernel is bf16 only
   if (partial && (!a.part || a.ksplit < 2)) return 1;
   switch (epi) {
     case EPI_STORE: run_epi<EPI_STORE>(cfg, a, partial, st); break;

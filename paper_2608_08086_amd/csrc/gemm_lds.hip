@@ -1,7 +1,8 @@
 // Projection GEMMs, multistage warp-specialised version.
 //
 // A workgroup has 8 waves: waves 0-3 multiply (a 2 x 2 or 4 x 1 grid of
-// wave tiles, MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulate), waves 4-7 only
+// wave tiles, MFMA v_mfma_f32_16x16x32_bf16 -- _f16 for the single-term fp16
+// operands of the gate/up projection -- fp32 accumulate), waves 4-7 only
 // load.  The loaders move the A (two-term: hi and lo) and W tiles of 32-wide k
 // chunks straight from global memory into NST LDS stages
 // (global_load_lds_dwordx4, no register staging).  With one wave per SIMD
@@ -19,8 +20,10 @@
 //
 // Synchronisation (one barrier per tile, all 8 waves).  The multiply waves
 // hold the fragments of tile g in registers (read during tile g - 1) and
-// place barrier X_g between the hi-term and lo-term MFMAs of tile g; after
-// X_g they read the fragments of tile g + 1, overlapping the lo-term MFMAs.
+// place barrier X_g between the hi-term and lo-term MFMAs of tile g (single
+// term: between the MFMAs of the first and second half of its weight blocks);
+// after X_g they read the fragments of tile g + 1, overlapping the MFMAs that
+// follow X_g.
 // A loader arrives at X_g once its loads of tile g + 1 have landed
 // (s_waitcnt vmcnt; the loads are issued from inline assembly, outside the
 // compiler's own wait tracking) and after X_g loads tile g + NST into the
@@ -28,7 +31,7 @@
 //
 // Results are bitwise identical to the register-staged kernel in gemm.hip:
 // the same k order (32-wide chunks in order, hi then lo term per chunk), the
-// same split-K slices and the same epilogues.
+// same split-K slices and the same epilogues.  fp16 operands run only here.
 #include <algorithm>
 
 #include "gemm_common.h"
@@ -148,7 +151,7 @@ __device__ __forceinline__ void store_qk_tile(const GemmArgs& a, const f16* qs, 
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int NST, int EPI, bool SPLIT, int MODE>
+template <int BM, int BN, int WGM, int WGN, int NST, int EPI, bool SPLIT, int MODE, bool F16 = false>
 __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int RB = WM / 16, CB = WN / 16;
@@ -159,6 +162,7 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   constexpr int STAGE = (NA * A_SL + B_SL) * 16;           // bytes
   constexpr bool PARTIAL = MODE == 2, FOLD = MODE == 1;
   static_assert(WGM * WGN == 4 && CB % 2 == 0 && RB >= 1, "bad wave grid");
+  static_assert(!F16 || !SPLIT, "fp16 operands are single-term");
   static_assert(A_SL % 256 == 0 && B_SL % 256 == 0, "each loader wave issues whole load instructions");
   static_assert(BN % (32 * WGN) == 0, "each wave takes 16-column blocks from both tile halves");
   static_assert((NST - 1) * IPT <= 63 && NST >= 2, "vmcnt range");
@@ -291,10 +295,17 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   // measured no faster.  Either orientation gives the same bits (each output
   // is the same sum of the same products).
   constexpr bool CT = !PARTIAL;
-  // one MFMA of weight fragment wf and activation fragment xf in the tile's orientation
+  // one MFMA of weight fragment wf and activation fragment xf in the tile's
+  // orientation (the fragments hold fp16 bits when F16)
   auto mm = [&](const bf16x8& wf, const bf16x8& xf, const f32x4& c) __attribute__((always_inline)) {
-    return CT ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xf, c, 0, 0, 0)
-              : __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, wf, c, 0, 0, 0);
+    if constexpr (F16) {
+      const f16x8 w16 = __builtin_bit_cast(f16x8, wf), x16 = __builtin_bit_cast(f16x8, xf);
+      return CT ? __builtin_amdgcn_mfma_f32_16x16x32_f16(w16, x16, c, 0, 0, 0)
+                : __builtin_amdgcn_mfma_f32_16x16x32_f16(x16, w16, c, 0, 0, 0);
+    } else {
+      return CT ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xf, c, 0, 0, 0)
+                : __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, wf, c, 0, 0, 0);
+    }
   };
   auto mfma_term = [&](int buf, int t) {
 #pragma unroll
@@ -317,6 +328,20 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
   // Two-term tiles of 32 columns per wave: two fragment sets, the reads of
   // tile g + 1 spread one per lo-term MFMA of tile g.
   constexpr bool PIPE = NA == 2 && CB <= 4 && !FOLD && !ROLL;
+  // Single-term tiles (except folded): the MFMAs of the first half of the
+  // weight blocks of tile g run before X_g, those of the second half after
+  // it.  After X_g the weight fragments of the first half are refilled with
+  // those of tile g + 1 at once, each of the second half as soon as its
+  // block's MFMAs have taken it (one weight fragment set, so that 64 x 128
+  // wave tiles fit the registers), and the activation fragments of tile
+  // g + 1 go to the second set in among them.
+  constexpr bool PIPE1 = NA == 1 && !FOLD;
+  auto mfma_blocks = [&](int buf, int cb0, int cb1) {
+#pragma unroll
+    for (int cb = cb0; cb < cb1; ++cb)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[rb][cb] = mm(fb[0][cb], fa[buf][0][rb], acc[rb][cb]);
+  };
   auto tile_roll = [&](int g, bool more) {
     if constexpr (ROLL) {
       const char* stg = smem + (g % NST) * STAGE;
@@ -364,6 +389,41 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
             acc[rb][cb] = mm(fb[0][cb], fa[0][1][rb], acc[rb][cb]);
+      }
+    }
+  };
+  auto tile_p1 = [&](int g, int cur, bool more) {
+    if constexpr (PIPE1) {
+      constexpr int H = CB / 2, NB2 = CB - H;
+      mfma_blocks(cur, 0, H);
+      if (more) {
+        __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
+        gl_barrier();                               // X_g
+        const char* stn = smem + ((g + 1) % NST) * STAGE;
+#pragma unroll
+        for (int cb = 0; cb < H; ++cb) fb[0][cb] = *(const bf16x8*)(stn + b_lo[cb]);
+#pragma unroll
+        for (int i = 0; i < NB2; ++i) {
+          const int cb = H + i;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) acc[rb][cb] = mm(fb[0][cb], fa[cur][0][rb], acc[rb][cb]);
+          fb[0][cb] = *(const bf16x8*)(stn + b_lo[cb]);
+#pragma unroll
+          for (int rb = RB * i / NB2; rb < RB * (i + 1) / NB2; ++rb)
+            fa[cur ^ 1][0][rb] = *(const bf16x8*)(stn + a_lo[rb]);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, H, 0);   // the first half's weight fragments
+#pragma unroll
+        for (int i = 0; i < NB2; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, RB, 0);   // the MFMAs of block H + i
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // its weight fragment
+#pragma unroll
+          for (int rb = RB * i / NB2; rb < RB * (i + 1) / NB2; ++rb)
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // activation fragments
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+        mfma_blocks(cur, H, CB);
       }
     }
   };
@@ -420,6 +480,11 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
     // the last tile peeled off: no branch in the loop body
     for (int g = 0; g + 1 < ntot; ++g) tile_roll(g, true);
     tile_roll(ntot - 1, false);
+  } else if constexpr (PIPE1) {
+    for (int g = 0; g < ntot; g += 2) {           // fragment buffer parity static in the two halves
+      tile_p1(g, 0, g + 1 < ntot);
+      if (g + 1 < ntot) tile_p1(g + 1, 1, g + 2 < ntot);
+    }
   } else {
     for (int g = 0; g < ntot; g += 2) {           // fragment buffer parity static in the two halves
       tile_body(g, 0);
@@ -578,8 +643,13 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
 
 template <int BM, int BN, int WGM, int WGN, int NST, int EPI, int MODE>
 void lds_mode(const GemmArgs& a, int grid, hipStream_t st) {
-  if (a.A2) gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, true, MODE><<<grid, 512, 0, st>>>(a);
-  else gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, false, MODE><<<grid, 512, 0, st>>>(a);
+  if (a.f16) {
+    if constexpr (EPI == EPI_SWIGLU) gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, false, MODE, true><<<grid, 512, 0, st>>>(a);
+  } else if (a.A2) {
+    gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, true, MODE><<<grid, 512, 0, st>>>(a);
+  } else {
+    gemm_lds_kernel<BM, BN, WGM, WGN, NST, EPI, false, MODE><<<grid, 512, 0, st>>>(a);
+  }
 }
 
 template <int BM, int BN, int WGM, int WGN, int NST, int EPI>

@@ -120,6 +120,8 @@ template void launch_rmsnorm<float>(const SeqPlan&, int, int, const float*, cons
                                     int, float, int*, hipStream_t);
 template void launch_rmsnorm<bf16>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int, int,
                                    int, float, int*, hipStream_t);
+template void launch_rmsnorm<f16>(const SeqPlan&, int, int, const float*, const float*, void*, void*, int, int,
+                                  int, float, int*, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Decision pass 1: per response row, over the non-MASK vocabulary:

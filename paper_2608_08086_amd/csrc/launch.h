@@ -16,6 +16,8 @@ struct GemmArgs {
   const void* A; int lda;               // [M][K] row-major (lda = row stride), or k-block-major (a_tiled,
   int a_tiled;                          //   lda = row capacity; see act_at in common.h)
   const void* A2;                       // optional low part of a two-term A (same layout), or null
+  int f16;                               // A, W and W2 are fp16 (A single-term, A2 null): one fp16
+                                         //   MFMA per fragment (EPI_SWIGLU, direct-to-LDS kernel only)
   const void* W; const void* W2; int ldw; // [N][K] (SWIGLU: W = gate [F][K], W2 = up [F][K], N = 2F)
   int w_tiled;                           //   k-block-major W (ldw = rows of each matrix), see act_at
   int M, N, K;
@@ -29,8 +31,9 @@ struct GemmArgs {
   float* X; int ldx;                     // EPI_RESID
   // EPI_RESID with a split-K reduction: optionally RMSNorm the updated rows of
   // X (gain ngain, epsilon neps) into the two-term activation (nout, nout2)
-  // laid out as act_at(row, k, nld, ntiled)
-  const float* ngain; void* nout; void* nout2; float neps; int nld, ntiled;
+  // laid out as act_at(row, k, nld, ntiled); nf16: into a single fp16 value
+  // (nout2 null) instead
+  const float* ngain; void* nout; void* nout2; float neps; int nld, ntiled, nf16;
   void* H; void* H2; int ldh, h_tiled;   // EPI_SWIGLU: H = hi part, H2 = lo part (or null), act_at layout
   // EPI_QKV
   void* Qb; int ldq;                     // Q [Hq][ldq][hd]

@@ -27,6 +27,11 @@ def _normal(shape, seed, stream, std, dtype):
     return out
 
 
+def _gateup(m: ModelShape, w):
+    """A bf16 gate or up matrix as the model stores it: fp16 under gateup_fp16."""
+    return w.to(torch.float16) if m.dtype == "bf16" and m.gateup_fp16 else w
+
+
 def model_weights_cuda(m: ModelShape, seed: int = 0) -> dict:
     dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
     d, hd, s = m.d_model, m.head_dim, m.init_std
@@ -40,8 +45,8 @@ def model_weights_cuda(m: ModelShape, seed: int = 0) -> dict:
             "w_qkv": _normal((m.qkv_dim, d), seed, b + 0, s, dt),
             "w_o": _normal((d, m.n_heads * hd), seed, b + 1, s, dt),
             "mlp_norm": ones(),
-            "w_gate": _normal((m.d_ff, d), seed, b + 2, s, dt),
-            "w_up": _normal((m.d_ff, d), seed, b + 3, s, dt),
+            "w_gate": _gateup(m, _normal((m.d_ff, d), seed, b + 2, s, dt)),
+            "w_up": _gateup(m, _normal((m.d_ff, d), seed, b + 3, s, dt)),
             "w_down": _normal((d, m.d_ff), seed, b + 4, s, dt),
         })
     return W

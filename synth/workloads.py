@@ -37,6 +37,9 @@ class ModelShape:
     # (names from "qkv", "o", "gateup", "down", "head"); the others take the
     # two-term (about 16-bit) activation
     single_term: tuple = ()
+    # bf16 models: the gate/up projection multiplies single fp16 operands (its
+    # input and w_gate, w_up rounded to fp16) instead of the two-term pair
+    gateup_fp16: bool = False
 
     @property
     def mask_id(self) -> int:
@@ -77,9 +80,9 @@ class Workload:
 
 
 _LLADA = ModelShape(n_layers=32, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128,
-                    d_ff=12288, vocab=126464, dtype="bf16")
+                    d_ff=12288, vocab=126464, dtype="bf16", gateup_fp16=True)
 _DREAM = ModelShape(n_layers=28, d_model=3584, n_heads=28, n_kv_heads=4, head_dim=128,
-                    d_ff=18944, vocab=152064, dtype="bf16")
+                    d_ff=18944, vocab=152064, dtype="bf16", gateup_fp16=True)
 
 WORKLOADS = {
     "tiny": Workload(

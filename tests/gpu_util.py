@@ -56,7 +56,7 @@ def make_ctx(shape, W, max_batch, max_prompt_len, max_prompt_total, resp_len, la
     """Context over host weights W.  layout None: the k-block weight layout for bf16 models
     (the one the bench runs), row-major for fp32."""
     a = archer()
-    Wd = a.upload_weights(W, shape.dtype)
+    Wd = a.upload_weights(W, shape.dtype, getattr(shape, "gateup_fp16", False))
     if layout is None:
         layout = a.LAYOUT_KBLOCK if shape.dtype == "bf16" else a.LAYOUT_ROWMAJOR
     if layout == a.LAYOUT_KBLOCK:

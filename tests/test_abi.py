@@ -55,10 +55,14 @@ def test_workspace_bytes_and_host_side_errors():
     lim = archer.Limits(1, 64, 64, 32)
     n = archer.lib.archer_workspace_bytes(C.byref(_cfg(archer)), C.byref(lim))
     assert n > 0 and n % 256 == 0
+    # fp16 gate/up operands are a bf16-model option (rejected above for fp32)
+    assert archer.lib.archer_workspace_bytes(C.byref(_cfg(archer, dtype=archer.BF16, gateup_fp16=1)),
+                                             C.byref(lim)) > 0
     # bigger limits need more workspace
     lim2 = archer.Limits(2, 128, 256, 32)
     assert archer.lib.archer_workspace_bytes(C.byref(_cfg(archer)), C.byref(lim2)) > n
-    bad = [dict(head_dim=96), dict(n_kv_heads=3), dict(d_model=250), dict(mask_id=1024), dict(dtype=7)]
+    bad = [dict(head_dim=96), dict(n_kv_heads=3), dict(d_model=250), dict(mask_id=1024), dict(dtype=7),
+           dict(gateup_fp16=1), dict(dtype=archer.FP16)]
     for kw in bad:
         assert archer.lib.archer_workspace_bytes(C.byref(_cfg(archer, **kw)), C.byref(lim)) == 0
         assert archer.lib.archer_last_error()

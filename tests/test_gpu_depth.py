@@ -80,9 +80,9 @@ def _err(name, got, want, bar=BAR):
     return e
 
 
-def _device_weights(W):
+def _device_weights(W, m):
     a = archer()
-    return a.pack_weights(a.upload_weights(W, "bf16"), drop_source=True)
+    return a.pack_weights(a.upload_weights(W, "bf16", m.gateup_fp16), drop_source=True)
 
 
 def _ctx(m, Wd, max_batch, max_prompt_len, max_prompt_total, G, layers=None):
@@ -106,7 +106,7 @@ def llada32():
     say(f"LLaDA-8B shape, {m.n_layers} layers: generating host weights")
     W = model_weights(m, seed=w.weight_seed)
     say(f"  host weights in {time.time() - t0:.1f} s; uploading")
-    Wd = _device_weights(W)
+    Wd = _device_weights(W, m)
     p = prompts(w)[0]
     g0 = np.full(G, m.mask_id)
     g0[:48] = (np.arange(48) * 131) % (m.vocab - 1)
@@ -230,7 +230,7 @@ def test_dream_all_28_layers():
     say(f"Dream shape, {m.n_layers} layers, B 1, P {P}, G {G}: generating host weights")
     W = model_weights(m, seed=w.weight_seed)
     say(f"  host weights in {time.time() - t0:.1f} s")
-    Wd = _device_weights(W)
+    Wd = _device_weights(W, m)
     p = prompts(w)[0]
     ctx = _ctx(m, Wd, 1, P, P, G)
     rng = np.random.default_rng(73)
@@ -266,7 +266,7 @@ def test_dream_two_layers_full_width_batch2():
     P, G, B = w.decode.prompt_len, w.decode.resp_len, 2
     say(f"Dream shape, 2 layers, B {B}, P {P}, G {G}: generating host weights")
     W = model_weights(m, seed=w.weight_seed)
-    Wd = _device_weights(W)
+    Wd = _device_weights(W, m)
     ps = prompts(w)[:B]
     ctx = _ctx(m, Wd, w.decode.batch, P, P * w.decode.batch, G)
     rng = np.random.default_rng(71)
@@ -310,7 +310,7 @@ def test_ragged16_two_layers_full_width_sampled():
     ps = prompts(w, lens)
     say(f"ragged batch, 2 layers, B {B}, P {lens}: generating host weights")
     W = model_weights(m, seed=w.weight_seed)
-    Wd = _device_weights(W)
+    Wd = _device_weights(W, m)
     ctx = _ctx(m, Wd, B, max(lens), sum(lens), G)
     rng = np.random.default_rng(72)
     g0 = np.full((B, G), m.mask_id)
@@ -349,7 +349,7 @@ def test_teacher_forced_decisions_full_width():
     P, G, k, tau, K = w.decode.prompt_len, w.decode.resp_len, 1, 0.1, 3
     say("teacher-forced decisions, 2 full-width LLaDA layers, age rule K 3, 6 steps")
     W = model_weights(m, seed=w.weight_seed)
-    Wd = _device_weights(W)
+    Wd = _device_weights(W, m)
     p = prompts(w)[0]
     ctx = _ctx(m, Wd, 1, P, P, G)
     g = np.full(G, m.mask_id)

@@ -36,6 +36,9 @@ SMALL_BF16 = {
     "mha_hd128": ModelShape(n_layers=2, d_model=256, n_heads=2, n_kv_heads=2, head_dim=128, d_ff=768,
                             vocab=1024, dtype="bf16", init_std=0.05),
 }
+# the same models with fp16 gate/up operands (split-K gate/up partials, the fp16 RMSNorm
+# fused into the O projection's split-K reduction)
+SMALL_BF16.update({k + "_gateup_fp16": dataclasses.replace(v, gateup_fp16=True) for k, v in list(SMALL_BF16.items())})
 
 
 def _resp(m, G, seed, frac=0.3):
@@ -93,22 +96,26 @@ def test_small_bf16_full_and_cached(name):
     assert np.max(np.abs(zc - zc_ref)) < 2e-2
 
 
-@pytest.mark.parametrize("rows,cols", [(1, 32), (100, 96), (257, 4096)])
-def test_pack_weight_is_the_k_block_permutation(rows, cols):
+@pytest.mark.parametrize("rows,cols,half", [(1, 32, False), (100, 96, False), (257, 4096, False),
+                                            (100, 96, True)])
+def test_pack_weight_is_the_k_block_permutation(rows, cols, half):
     a = archer()
-    say(f"pack weight {rows}x{cols}")
+    say(f"pack weight {rows}x{cols}{' fp16' if half else ''}")
     w, _ = rand_bf16((rows, cols), 61, rows * 7 + cols)
+    if half:
+        w = w.to(torch.float16)
     got = a.pack_weight(w)
     # element (r, c) at ((c / 32) * rows + r) * 32 + c % 32
     want = w.view(rows, cols // 32, 32).permute(1, 0, 2).contiguous().view(rows, cols)
     assert torch.equal(got.view(torch.int16), want.view(torch.int16))
 
 
-def test_weight_layouts_give_the_same_bits():
+@pytest.mark.parametrize("name", ["gqa_hd64", "gqa_hd64_gateup_fp16"])
+def test_weight_layouts_give_the_same_bits(name):
     """The k-block and row-major weight layouts feed the same tiles in the same order."""
     a = archer()
-    m = SMALL_BF16["gqa_hd64"]
-    say("bf16 model, row-major vs k-block weights")
+    m = SMALL_BF16[name]
+    say(f"bf16 model {name}, row-major vs k-block weights")
     W = with_gains(model_weights(m, seed=12), 12)
     P, G = 77, 32
     p = _prompt(m, P, 13)
@@ -122,6 +129,30 @@ def test_weight_layouts_give_the_same_bits():
         ctx.close()
     np.testing.assert_array_equal(out[0][0], out[1][0])
     np.testing.assert_array_equal(out[0][1], out[1][1])
+
+
+def test_gateup_fp16_full_pass_with_folded_slices():
+    """A full pass above the partial-plane row capacity (4608 rows) runs the split-K
+    projections with their slices folded in one workgroup, fp16 gate/up included, and
+    the stand-alone fp16 RMSNorm before it."""
+    m = SMALL_BF16["gqa_hd64_gateup_fp16"]
+    say("small bf16 model, fp16 gate/up, P 4700: folded split-K slices in the full pass")
+    W = with_gains(model_weights(m, seed=21), 21)
+    P, G = 4700, 32
+    p = _prompt(m, P, 22)
+    ctx = make_ctx(m, W, 1, P, P, G)
+    g0 = _resp(m, G, 23)
+    z = host(ctx.refresh_prompt(dev_i32(p), [P], dev_i32(g0[None])))[0]
+    z_ref, cache, _ = om.full_forward(W, m, p, g0)
+    e = np.max(np.abs(z - z_ref))
+    say(f"  full pass logits max abs err {e:.3e}")
+    assert e < 2e-2
+    g1 = _resp(m, G, 24, frac=0.6)
+    zc = host(ctx.step(dev_i32(g1[None])))[0]
+    zc_ref, _ = om.cached_forward(W, m, g1, cache, P)
+    e = np.max(np.abs(zc - zc_ref))
+    say(f"  cached pass logits max abs err {e:.3e}")
+    assert e < 2e-2
 
 
 def test_ragged_batch_per_sequence_refresh_and_batch_invariance():

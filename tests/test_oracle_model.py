@@ -2,7 +2,8 @@
 
 * a scalar-loop float64 transformer written independently here (pure Python,
   its own fp16 and bf16 rounding via frexp) must match
-  ``oracle.model.transformer``, with and without single-term operands;
+  ``oracle.model.transformer``, with and without single-term operands and
+  with the fp16 gate/up operands (weights below fp16's normal range planted);
 * permutation consistency of bidirectional attention, by brute force over all
   orders of tiny inputs;
 * CachedForward(g; C_p(g)) equals FullForward(p, g) (D_t = 0 case of
@@ -46,12 +47,16 @@ def _w(a):
     return on.weights_f64(a).tolist()
 
 
-def _loop_model(W, m, tokens, positions, out_rows):
+def _loop_model(W, m, tokens, positions, out_rows, round_gateup_w=True):
     ident = lambda t: t   # noqa: E731
     rnd = _fp16 if m.dtype == "bf16" else ident
+    gu16 = m.dtype == "bf16" and m.gateup_fp16
 
     def op(name, row):
-        """Activation operand of a projection: single bf16 where the model says so."""
+        """Activation operand of a projection: single bf16 where the model says so,
+        single fp16 for gate/up under gateup_fp16."""
+        if name == "gateup" and gu16:
+            return [_fp16(t) for t in row]
         single = m.dtype == "bf16" and name in m.single_term
         return [_bf16(t) for t in row] if single else row
     d, hq, hkv, hd, F = m.d_model, m.n_heads, m.n_kv_heads, m.head_dim, m.d_ff
@@ -78,6 +83,9 @@ def _loop_model(W, m, tokens, positions, out_rows):
 
     for L in W["layers"]:
         wqkv, wo, wg, wu, wd = (_w(L[k]) for k in ("w_qkv", "w_o", "w_gate", "w_up", "w_down"))
+        if gu16 and round_gateup_w:
+            wg = [[_fp16(t) for t in r] for r in wg]
+            wu = [[_fp16(t) for t in r] for r in wu]
         Q, K, V = [], [], []
         for i in range(n):
             a = op("qkv", norm(x[i], L["attn_norm"]))
@@ -111,17 +119,45 @@ def _loop_model(W, m, tokens, positions, out_rows):
     return np.array(z)
 
 
-@pytest.mark.parametrize("dtype,single", [("fp32", ()), ("bf16", ()),
-                                          ("bf16", ("qkv", "o", "gateup", "down", "head")),
-                                          ("bf16", ("o", "head"))])
-def test_transformer_matches_scalar_loops(dtype, single):
-    m = tiny_shape(dtype, single_term=single)
+@pytest.mark.parametrize("dtype,single,gu16", [("fp32", (), False), ("bf16", (), False),
+                                               ("bf16", ("qkv", "o", "gateup", "down", "head"), False),
+                                               ("bf16", ("o", "head"), False),
+                                               ("bf16", (), True), ("bf16", ("o", "head"), True)])
+def test_transformer_matches_scalar_loops(dtype, single, gu16):
+    m = tiny_shape(dtype, single_term=single, gateup_fp16=gu16)
     W = random_weights(m, seed=3)
     tokens = np.array([1, 4, 9, 2, 9, 0])
     positions = np.arange(6)
     z, _, _ = om.transformer(W, m, tokens, positions)
     ref = _loop_model(W, m, tokens.tolist(), positions.tolist(), range(6))
     np.testing.assert_allclose(z, ref, rtol=0, atol=1e-11 if dtype == "fp32" else 1e-9)
+
+
+def _bf16_bits(v):
+    """float64 values -> uint16 bf16 bit patterns (round to nearest even via float32)."""
+    f = np.asarray(v, dtype=np.float32).view(np.uint32)
+    return ((f + np.uint32(0x7FFF) + ((f >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
+
+
+def test_gateup_fp16_rounds_weights_below_the_fp16_normal_range():
+    """bf16 gate weights of magnitude 2^-21..2^-19 are not fp16 values (fp16 spaces
+    them 2^-24 apart): the oracle must multiply their fp16 roundings.  The plant is
+    large enough that leaving the weights unrounded misses the scalar loops by far
+    more than the tolerance."""
+    m = tiny_shape("bf16", gateup_fp16=True)
+    W = random_weights(m, seed=5)
+    rng = np.random.default_rng(17)
+    for L in W["layers"]:
+        v = rng.uniform(2.0 ** -21, 2.0 ** -19, size=(3, m.d_model)) * rng.choice([-1.0, 1.0], size=(3, m.d_model))
+        L["w_gate"][:3] = _bf16_bits(v)
+        L["w_up"][:3] = _bf16_bits(64.0 * rng.standard_normal((3, m.d_model)))
+    tokens = np.array([3, 1, 4, 1, 5])
+    positions = np.arange(5)
+    z, _, _ = om.transformer(W, m, tokens, positions)
+    ref = _loop_model(W, m, tokens.tolist(), positions.tolist(), range(5))
+    np.testing.assert_allclose(z, ref, rtol=0, atol=1e-9)
+    unrounded = _loop_model(W, m, tokens.tolist(), positions.tolist(), range(5), round_gateup_w=False)
+    assert np.max(np.abs(unrounded - ref)) > 1e-7
 
 
 # --- permutation consistency (brute force over all orders) -------------------
