@@ -503,9 +503,11 @@ int gemm_pick_cfg(const GemmArgs& a, int epi) {
   // 128 x 128; the 128 x 192 tile is not used for slices folded in one
   // workgroup (its second accumulator set does not fit the registers of two
   // waves per SIMD).
-  // Single-term fp16 launches choose like two-term ones (their tiles are
-  // timed in the same ratios).
+  // Single-term fp16 launches (gate/up) choose the same way with their own
+  // tile times: 1.34x (128 x 192) and 1.66x (128 x 256) that of a 128 x 128
+  // tile, measured on the LLaDA-8B gate/up shape at 24853 rows.
   const bool wide = (a.A2 || a.f16) && a.ksplit == 1;
+  const double t192 = a.f16 ? 1.34 : 1.5, t256 = a.f16 ? 1.66 : 1.77;
   if (wide && epi == EPI_STORE) {
     if (a.N % 256 == 0 && a.N / 256 >= 256 && gemm_lds_cfg_ok(2, a)) return GEMM_NCFG + 2;
   } else if (wide) {
@@ -515,10 +517,10 @@ int gemm_pick_cfg(const GemmArgs& a, int epi) {
     const auto cost = [&](int bn, double t) { return (double)((a.N / bn * mt + 255) / 256) * t; };
     int best = -1;
     double bc = 0;
-    if (a.N % 256 == 0 && gemm_lds_cfg_ok(2, a)) { best = 2; bc = cost(256, 1.77); }
-    if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a) && (best < 0 || cost(192, 1.5) < 0.95 * bc)) {
+    if (a.N % 256 == 0 && gemm_lds_cfg_ok(2, a)) { best = 2; bc = cost(256, t256); }
+    if (a.N % 192 == 0 && gemm_lds_cfg_ok(0, a) && (best < 0 || cost(192, t192) < 0.95 * bc)) {
       best = 0;
-      bc = cost(192, 1.5);
+      bc = cost(192, t192);
     }
     if (a.N % 128 == 0 && gemm_lds_cfg_ok(1, a) && (best < 0 || cost(128, 1.0) < 0.95 * bc)) {
       best = 1;

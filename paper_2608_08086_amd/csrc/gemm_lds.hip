@@ -392,8 +392,53 @@ __global__ __launch_bounds__(512, 1) void gemm_lds_kernel(GemmArgs a) {
       }
     }
   };
+  // 64 x 128 wave tiles (8 weight blocks) keep one activation fragment set
+  // too: the last block's MFMAs take the activation fragments one by one and
+  // each is refilled right after, and the next tile starts with the MFMAs of
+  // the first activation fragment over its first half of blocks.
+  constexpr bool FA1 = PIPE1 && CB == 8;
   auto tile_p1 = [&](int g, int cur, bool more) {
-    if constexpr (PIPE1) {
+    if constexpr (FA1) {
+      constexpr int H = CB / 2;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < H; ++cb) acc[rb][cb] = mm(fb[0][cb], fa[0][0][rb], acc[rb][cb]);
+      if (more) {
+        __builtin_amdgcn_s_waitcnt(GL_LGKMCNT0);   // this wave's reads of tile g are done
+        gl_barrier();                               // X_g
+        const char* stn = smem + ((g + 1) % NST) * STAGE;
+#pragma unroll
+        for (int cb = 0; cb < H; ++cb) fb[0][cb] = *(const bf16x8*)(stn + b_lo[cb]);
+#pragma unroll
+        for (int cb = H; cb < CB - 1; ++cb) {
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) acc[rb][cb] = mm(fb[0][cb], fa[0][0][rb], acc[rb][cb]);
+          fb[0][cb] = *(const bf16x8*)(stn + b_lo[cb]);
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          acc[rb][CB - 1] = mm(fb[0][CB - 1], fa[0][0][rb], acc[rb][CB - 1]);
+          fa[0][0][rb] = *(const bf16x8*)(stn + a_lo[rb]);
+        }
+        fb[0][CB - 1] = *(const bf16x8*)(stn + b_lo[CB - 1]);
+        __builtin_amdgcn_sched_group_barrier(0x100, H, 0);   // the first half's weight fragments
+#pragma unroll
+        for (int cb = H; cb < CB - 1; ++cb) {
+          __builtin_amdgcn_sched_group_barrier(0x008, RB, 0);   // the MFMAs of block cb
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // its weight fragment
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // last block, activation fragment rb
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // its refill
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // the last weight fragment
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+        mfma_blocks(0, H, CB);
+      }
+    } else if constexpr (PIPE1) {
       constexpr int H = CB / 2, NB2 = CB - H;
       mfma_blocks(cur, 0, H);
       if (more) {
@@ -670,7 +715,7 @@ struct LdsCfg { int BM, BN; };
 const LdsCfg kLds[GEMM_NCFG_LDS] = {
     {128, 192},   // 0: 2 x 2 multiply waves of 64 x 96, 4 stages
     {128, 128},   // 1: 2 x 2 multiply waves of 64 x 64, 4 stages
-    {128, 256},   // 2: 2 x 2 multiply waves of 64 x 128, 4 stages, one K slice, two-term only
+    {128, 256},   // 2: 2 x 2 multiply waves of 64 x 128, 4 stages, one K slice, two-term or fp16
 };
 
 template <int EPI>
@@ -679,9 +724,14 @@ void lds_epi(int c, const GemmArgs& a, bool partial, hipStream_t st) {
     case 0: lds_cfg<128, 192, 2, 2, 4, EPI>(a, partial, st); break;
     case 1: lds_cfg<128, 128, 2, 2, 4, EPI>(a, partial, st); break;
     default: {
-      // one K slice, two-term activations only (the in-place refill needs both terms)
+      // one K slice; two-term activations (the in-place refill needs both
+      // terms) or single-term fp16 ones (one fragment set of each kind)
       const int grid = gemm_grid_size(a.N / 256, (a.M + 127) / 128, 1);
-      gemm_lds_kernel<128, 256, 2, 2, 4, EPI, true, 0><<<grid, 512, 0, st>>>(a);
+      if (a.f16) {
+        if constexpr (EPI == EPI_SWIGLU) gemm_lds_kernel<128, 256, 2, 2, 4, EPI, false, 0, true><<<grid, 512, 0, st>>>(a);
+      } else {
+        gemm_lds_kernel<128, 256, 2, 2, 4, EPI, true, 0><<<grid, 512, 0, st>>>(a);
+      }
       break;
     }
   }
@@ -700,7 +750,7 @@ bool gemm_lds_cfg_ok(int c, const GemmArgs& a) {
   if (c < 0 || c >= GEMM_NCFG_LDS) return false;
   const LdsCfg& k = kLds[c];
   if (a.M <= 0 || a.N % k.BN || a.ksplit < 1 || a.K % (a.ksplit * BK)) return false;
-  if (c == 2 && (!a.A2 || a.ksplit != 1)) return false;
+  if (c == 2 && ((!a.A2 && !a.f16) || a.ksplit != 1)) return false;
   // 32-bit lane offsets
   if ((size_t)a.N * (a.w_tiled ? BK : a.ldw) * 2 >= (1ull << 32) || (size_t)a.M * (a.a_tiled ? BK : a.lda) * 2 >= (1ull << 32))
     return false;
