@@ -42,7 +42,8 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_TFLOPS = 157.3
 
-# classes whose bf16 launches multiply two-term activations (two MFMAs per fragment)
+# classes whose bf16 launches multiply two-term activations (two MFMAs per fragment),
+# except gate/up in models with fp16 gate/up operands
 GEMM_CLASSES = ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "gemm_head",
                 "gemm_qkv_full", "gemm_o_full", "gemm_gateup_full", "gemm_down_full")
 SINGLE_TERM_OF = {c: c.replace("gemm_", "").replace("_full", "") for c in GEMM_CLASSES}
@@ -293,6 +294,8 @@ def main():
     ap.add_argument("--policy", default="age", choices=["age", "hamming", "always"])
     ap.add_argument("--single-term", default="",
                     help="comma-separated projections (qkv,o,gateup,down,head) with single-bf16 activations")
+    ap.add_argument("--two-term-gateup", action="store_true",
+                    help="gate/up with two-term bf16 operands instead of the model's fp16 ones")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-refresh", action="store_true")
     ap.add_argument("--timing-every", type=int, default=7,
@@ -328,13 +331,15 @@ def main():
     w = get_workload(args.workload)
     if args.single_term:
         w = w.with_model(single_term=tuple(x for x in args.single_term.split(",") if x))
+    if args.two_term_gateup:
+        w = w.with_model(gateup_fp16=False)
     m, dec = w.model, w.decode
     B, G, T, k = dec.batch, dec.resp_len, dec.steps, dec.unmask_per_step
     Kr = dec.refresh_every
     lens = prompt_lengths(w)
     pol = {"age": archer.AGE, "hamming": archer.HAMMING, "always": archer.ALWAYS}[args.policy]
     log(f"bench: workload {w.name} B={B} P={lens if len(lens) <= 4 else (min(lens), max(lens))} G={G} T={T} "
-        f"k={k} policy={args.policy} K={Kr} single_term={list(m.single_term)}")
+        f"k={k} policy={args.policy} K={Kr} single_term={list(m.single_term)} gateup_fp16={m.gateup_fp16}")
     t0 = time.perf_counter()
     Wd = model_weights_cuda(m, seed=w.weight_seed)
     if m.dtype == "bf16":
@@ -435,6 +440,8 @@ def main():
     single = set(m.single_term)
 
     def two_term(cls):
+        if m.gateup_fp16 and SINGLE_TERM_OF.get(cls) == "gateup":
+            return False   # one fp16 MFMA per fragment
         return m.dtype == "bf16" and cls in GEMM_CLASSES and SINGLE_TERM_OF[cls] not in single
 
     gemm_roofs = {}
@@ -476,6 +483,7 @@ def main():
                    "unmask_per_step": k, "policy": args.policy, "K": Kr,
                    "bench_step": f"one refresh period: {period} decisions with their forwards",
                    "single_term_activations": sorted(single),
+                   "gateup_fp16": bool(m.dtype == "bf16" and m.gateup_fp16),
                    "weight_layout": "kblock" if m.dtype == "bf16" else "rowmajor"},
         "response_tok_per_s": round(tok, 3),
         "recomputed_positions_per_s": round(sps * B * G, 1),
