@@ -90,3 +90,27 @@ def test_timing_stride(ctx):
             assert t[k]["launches"] == want, (every, k, t[k])
             assert t[k]["ms"] > 0 and t[k]["flops"] > 0
         assert t["attn"]["launches"] == 0
+
+
+def test_gateup_fp16_option_errors():
+    """A model with fp16 gate/up operands takes fp16 w_gate / w_up (the binding refuses
+    bf16 ones) and refuses a single-term request for gate/up (its operands are single
+    fp16 values already); other classes still switch."""
+    import dataclasses
+    a = archer()
+    m = ModelShape(n_layers=1, d_model=64, n_heads=1, n_kv_heads=1, head_dim=64, d_ff=64, vocab=128,
+                   dtype="bf16", gateup_fp16=True)
+    W = model_weights(m, seed=3)
+    with pytest.raises(a.ArcherError) as e:
+        a.Context(m, a.upload_weights(W, "bf16"), 1, 16, 16, 8)   # bf16 gate/up weights
+    assert e.value.status == a.E_ARG
+    c = make_ctx(m, W, 1, 16, 16, 8)
+    with pytest.raises(a.ArcherError) as e:
+        c.set_single_term(["gateup"])
+    assert e.value.status == a.E_UNSUPPORTED
+    c.set_single_term(["o"])
+    c.set_single_term([])
+    # the same shape without the option accepts a single-term gate/up
+    m2 = dataclasses.replace(m, gateup_fp16=False)
+    c2 = make_ctx(m2, W, 1, 16, 16, 8)
+    c2.set_single_term(["gateup"])
