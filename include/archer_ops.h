@@ -129,7 +129,8 @@ archer_status archer_read_state(archer_ctx *ctx, int32_t what, int32_t layer, in
 
 /* Precision of the activation operand of each projection class (bf16 models).
  * By default every projection multiplies a two-term bf16 activation
- * (hi + lo, about 16 significant bits; two MFMAs per fragment).  A set bit
+ * (hi + lo, about 16 significant bits; two MFMAs per fragment), except the
+ * gate/up projection of a model with gateup_fp16 (single fp16).  A set bit
  * ARCHER_K_GEMM_QKV, _O, _GATEUP, _DOWN or _HEAD in class_mask makes that
  * class's producer store and its GEMM read the single bf16 rounding hi = bf16(v)
  * instead (half the MFMA work of that projection).  Applies to forwards

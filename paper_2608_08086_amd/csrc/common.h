@@ -138,8 +138,9 @@ __device__ __forceinline__ size_t act_at(int row, int k, int ld, int tiled) {
 // split-K reduction; both must use the same count to give the same bits).
 constexpr int NORM_THREADS = 512;
 
-// RMSNorm of one row of x (d columns) into a two-term activation row, by a
-// block of NORM_THREADS threads: thread t owns the float4 chunks at
+// RMSNorm of one row of x (d columns) into a two-term activation row (with T
+// = f16 and out2 null: one fp16 rounding per element), by a block of
+// NORM_THREADS threads: thread t owns the float4 chunks at
 // t * 4 + k * 4 * NORM_THREADS.
 // Shared by the stand-alone RMSNorm kernel and the split-K reduction that
 // fuses it, so that both give the same bits.
