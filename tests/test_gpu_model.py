@@ -228,10 +228,12 @@ def test_maximum_batch_of_64_with_one_token_prompt():
     np.testing.assert_array_equal(z0c, zc[0])
 
 
-def test_full_width_two_layer_llada_shape():
-    """d 4096, 32 heads x 128, F 12288, vocab 126464, P 512, G 256 (two layers)."""
+@pytest.mark.parametrize("gateup_fp16", [True, False])
+def test_full_width_two_layer_llada_shape(gateup_fp16):
+    """d 4096, 32 heads x 128, F 12288, vocab 126464, P 512, G 256 (two layers); gate/up
+    with fp16 operands (the workload's model) and with two-term bf16 ones."""
     w = get_workload("llada_p512")
-    m = dataclasses.replace(w.model, n_layers=2)
+    m = dataclasses.replace(w.model, n_layers=2, gateup_fp16=gateup_fp16)
     P, G = w.decode.prompt_len, w.decode.resp_len
     say("full-width 2-layer LLaDA shape: generating weights")
     W = model_weights(m, seed=w.weight_seed)
@@ -255,11 +257,13 @@ def test_full_width_two_layer_llada_shape():
     assert err < 2e-2
 
 
-def test_full_width_two_layer_llada_long_prompt():
-    """d 4096, 32 heads x 128, F 12288, vocab 126464, P 4096, G 256 (two layers)."""
+@pytest.mark.parametrize("gateup_fp16", [True, False])
+def test_full_width_two_layer_llada_long_prompt(gateup_fp16):
+    """d 4096, 32 heads x 128, F 12288, vocab 126464, P 4096, G 256 (two layers); the
+    4352-row refresh runs 128 x 256 gate/up tiles, fp16 or two-term."""
     import time
     w = get_workload("llada_p4096")
-    m = dataclasses.replace(w.model, n_layers=2)
+    m = dataclasses.replace(w.model, n_layers=2, gateup_fp16=gateup_fp16)
     P, G = w.decode.prompt_len, w.decode.resp_len
     say("full-width 2-layer LLaDA shape, P 4096: generating weights")
     W = model_weights(m, seed=w.weight_seed)
