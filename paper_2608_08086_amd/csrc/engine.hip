@@ -284,7 +284,8 @@ archer_status gemm(archer_ctx* c, int cls, int epi, GemmArgs& a) {
   const double es = (double)c->esz;
   double bytes = (double)a.M * a.K * es * (a.A2 ? 2 : 1) + (double)a.N * a.K * es;
   if (epi == EPI_STORE) bytes += (a.C ? (double)a.M * a.N * 4 : 0.0) + (a.tstat ? (double)a.M * c->np * 12 : 0.0);
-  else if (epi == EPI_RESID) bytes += 2.0 * a.M * a.N * 4 + (gemm_fuses_norm(a) ? (double)a.M * a.N * es * 2 : 0.0);
+  else if (epi == EPI_RESID)
+    bytes += 2.0 * a.M * a.N * 4 + (gemm_fuses_norm(a) ? (double)a.M * a.N * es * (a.nout2 ? 2 : 1) : 0.0);
   else if (epi == EPI_SWIGLU) bytes += (double)a.M * (a.N / 2) * es * (a.H2 ? 2 : 1);
   else bytes += (double)a.M * a.N * es;
   const double flops = 2.0 * a.M * a.N * a.K;
